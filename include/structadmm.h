@@ -1,0 +1,242 @@
+/*
+ * structadmm.h -- C ABI of the MI355X (gfx950) StructADMM hot path.
+ *
+ * Method: "StructADMM: A Systematic, High-Efficiency Framework of Structured
+ * Weight Pruning for DNNs" (arXiv 1807.11091).
+ *
+ * The library computes, on one GPU:
+ *   - the Z-update of the ADMM regularisation step (Section 4, eq. (4) and
+ *     "Solving the second subproblem"): Z = Euclidean projection of W + U
+ *     onto a filter-, channel-, filter-shape-wise or non-structured sparsity
+ *     set (Section 3), fused optionally with the dual update
+ *     U <- U + W - Z (Section 4, below eq. (3)) and the gradient of the
+ *     quadratic term of eq. (3), G = rho * (W - Z + U);
+ *   - the standalone dual update / gradient;
+ *   - the compaction of a pruned layer into the smaller dense GEMM matrix
+ *     that filter (row) and channel / shape (column) pruning leave
+ *     (Section 3, "Combination of structured sparsities");
+ *   - the CONV over that compacted matrix as an implicit GEMM on the bf16
+ *     matrix cores (the same kernel with an uncompacted matrix is the dense
+ *     baseline).
+ *
+ * Conventions shared by every entry point
+ *   - Every tensor argument is DEVICE memory owned by the caller.  The
+ *     library never allocates or frees device memory; scratch space comes
+ *     from the caller (see structadmm_project_workspace).
+ *   - Weights are binary32, contiguous, in [A, B, C, D] order (filters,
+ *     channels per conv group, kernel height, kernel width), i.e. PyTorch /
+ *     Caffe OIHW.  The flat index of (a, b, c, d) is ((a*B + b)*C + c)*D + d
+ *     and the GEMM column of (b, c, d) is j = (b*C + c)*D + d.
+ *   - Work is enqueued asynchronously on the given HIP stream (0 = the null
+ *     stream).  Only structadmm_compact synchronises with the host.
+ *   - Return value 0 = success; negative = error (codes below).  All
+ *     arguments are validated on the host before anything is enqueued, so
+ *     an error return leaves every output untouched.
+ *     structadmm_last_error() gives a message for the calling thread.
+ *   - Identical inputs give bitwise identical outputs (no floating-point
+ *     atomics; every reduction has a fixed order).
+ *   - Calls on different streams over disjoint buffers may overlap; calls
+ *     that share output buffers must be ordered by the caller.
+ */
+#ifndef STRUCTADMM_H
+#define STRUCTADMM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- error codes ---------------------------------------------------- */
+#define SA_OK 0
+#define SA_E_ARG (-1)         /* null required pointer, bad size, k out of range, ... */
+#define SA_E_ALIGN (-2)       /* a pointer lacks the alignment stated below */
+#define SA_E_WORKSPACE (-3)   /* workspace missing or smaller than the size query */
+#define SA_E_UNSUPPORTED (-4) /* valid request outside what the kernels implement */
+#define SA_E_HIP (-5)         /* a HIP runtime call or kernel launch failed */
+
+/* ---- constraint sets (Section 3) ------------------------------------ */
+typedef enum {
+    SA_FILTER = 0,  /* at most k nonzero filters  X[a,:,:,:]; n_groups = A        */
+    SA_CHANNEL = 1, /* at most k nonzero channels X[:,b,:,:]; n_groups = B        */
+    SA_SHAPE = 2,   /* at most k nonzero vectors  X[:,b,c,d]; n_groups = B*C*D    */
+    SA_ELEMENT = 3  /* at most k nonzero weights;             n_groups = A*B*C*D  */
+} sa_kind;
+
+/* Largest group count the structured selection handles (filter / channel /
+ * shape).  The element-wise selection has no such limit (n < 2^31). */
+#define SA_MAX_STRUCT_GROUPS 8192
+/* Largest number of conv groups of a layer. */
+#define SA_MAX_CONV_GROUPS 16
+
+/* ---- Z-update: structadmm_project ----------------------------------- */
+/*
+ * One layer of the Z-update (Section 4).  With V = fl32(W + U) (one binary32
+ * add per entry):
+ *   score of group g: O_g = sum over the group of (double)v * (double)v
+ *     (squared Frobenius norm, binary64 accumulation); element-wise: |v|;
+ *   the k groups with the largest scores are kept, exactly k of them; ties
+ *     at the k-th score go to the lowest group index;
+ *   Z = v on kept groups, +0 elsewhere.
+ * Fused step (G != NULL): with the same W, U' = fl32(v - Z) is written to U
+ *   (the dual update U + W - Z) and G = fl32(rho * fl32(fl32(W - Z) + U'))
+ *   (the gradient of rho/2 ||W - Z + U'||^2, eq. (3)).
+ * in_ch_mask (optional): a fixed input-channel support.  Entry gc*B + b
+ *   (conv group gc = a / (A/groups)) set to 0 forces Z to 0 on the slice
+ *   X[a in group gc, b, :, :]; those entries do not enter any score, so the
+ *   result is the projection onto the intersection of the two sets.
+ *   Supported with every kind.  When in_ch_mask aliases the mask output of an
+ *   earlier layer of the same call (same pointer), that layer is completed
+ *   first: layers are processed in array order of such dependencies.
+ */
+typedef struct sa_project_desc {
+    int64_t A, B, C, D;        /* weight tensor shape, each >= 1; A*B*C*D < 2^31 */
+    int32_t groups;            /* conv groups, >= 1, A % groups == 0            */
+    int32_t kind;              /* sa_kind                                       */
+    int64_t k;                 /* kept groups, 0 <= k <= n_groups               */
+    const float *W;            /* [A,B,C,D] binary32, 16-byte aligned            */
+    float *U;                  /* [A,B,C,D] binary32, 16-byte aligned; read, and
+                                  overwritten with U' when G != NULL            */
+    const uint8_t *in_ch_mask; /* [groups*B] or NULL                            */
+    float *Z;                  /* out [A,B,C,D], 16-byte aligned; must not alias W or U */
+    uint8_t *mask;             /* out [n_groups]: 1 = kept, 0 = pruned          */
+    int32_t *kept_idx;         /* out [k]: kept group indices, ascending (may be NULL when k == 0) */
+    double *scores;            /* out [n_groups] scores, or NULL                */
+    float rho;                 /* penalty rho of eq. (3) (fused step only)      */
+    float *G;                  /* out [A,B,C,D], 16-byte aligned, or NULL (no fused step) */
+} sa_project_desc;
+
+/* Workspace bytes that structadmm_project needs for these layers (0 if none).
+ * Returns 0 also for invalid descriptors; structadmm_project reports those. */
+size_t structadmm_project_workspace(const sa_project_desc *layers, int n_layers);
+
+/* Z-update (and optional fused dual update + gradient) of n_layers layers.
+ * ws: device workspace of at least structadmm_project_workspace() bytes,
+ * 256-byte aligned, reused freely by the library during the call's kernels
+ * (calls sharing one workspace must be ordered). */
+int structadmm_project(const sa_project_desc *layers, int n_layers, void *ws, size_t ws_bytes,
+                       hipStream_t stream);
+
+/* ---- dual update / gradient: structadmm_dual_update ------------------ */
+/*
+ * U <- fl32(fl32(U + W) - Z) (Section 4, below eq. (3)) when update_dual != 0,
+ * and G = fl32(rho * fl32(fl32(W - Z) + U)) with the (new) U: the gradient of
+ * rho/2 ||W - Z + U||_F^2 (eq. (3)) that each SGD step of the W-subproblem adds.
+ * G may be NULL (dual update only).  All arrays binary32 [n], 16-byte aligned.
+ */
+typedef struct sa_dual_desc {
+    int64_t n;          /* entries, 1 <= n < 2^31 */
+    const float *W;
+    const float *Z;
+    float *U;           /* in/out */
+    float rho;
+    float *G;           /* out or NULL */
+    int32_t update_dual;
+} sa_dual_desc;
+
+int structadmm_dual_update(const sa_dual_desc *layers, int n_layers, hipStream_t stream);
+
+/* ---- compaction: structadmm_compact --------------------------------- */
+/*
+ * Builds, per conv group gc, the dense GEMM matrix that remains after row and
+ * column pruning (Section 3):
+ *   rows: the filters a in [gc*A/groups, (gc+1)*A/groups) with row_mask[a] set
+ *         (every row when row_mask is NULL), ascending;
+ *   columns: the pairs (tap t = c*D + d, channel b) with col_mask[b*C*D + t],
+ *         chan_mask[b] and in_ch_mask[gc*B + b] all set (a NULL mask sets
+ *         nothing aside), in tap-major order: t ascending, then b ascending;
+ *   entries: Wc[m][j] = Z[row m, column j] rounded to bfloat16 (nearest even).
+ * Matrices are concatenated over conv groups, each row-major [M_g][ldk_g]
+ * with ldk_g = K_g rounded up to a multiple of 8; the padding columns
+ * j in [K_g, ldk_g) hold +0 (so every row starts 16-byte aligned).
+ * Column tables: col_tap[j] = c*D + d, col_ch[j] = input channel of column j,
+ * i.e. gc*B + b, or, when in_compacted is set, the position of channel
+ * gc*B + b among the channels with in_ch_mask set (the input then holds only
+ * those channels, ascending).  row_idx lists the kept filters (the output
+ * channel order of structadmm_conv_fwd).
+ * Masks are byte arrays (0 = pruned) such as structadmm_project's mask.
+ * Synchronises with the host and fills *sizes.
+ */
+typedef struct sa_compact_desc {
+    int64_t A, B, C, D;          /* shape of Z */
+    int32_t groups;              /* 1 <= groups <= SA_MAX_CONV_GROUPS, A % groups == 0 */
+    const float *Z;              /* [A,B,C,D] binary32 */
+    const uint8_t *row_mask;     /* [A] or NULL            */
+    const uint8_t *col_mask;     /* [B*C*D] or NULL        */
+    const uint8_t *chan_mask;    /* [B] or NULL            */
+    const uint8_t *in_ch_mask;   /* [groups*B] or NULL     */
+    int32_t in_compacted;        /* requires in_ch_mask    */
+    uint16_t *Wc;                /* out, capacity A * roundup(B*C*D, 8) bfloat16 */
+    int32_t *row_idx;            /* out, capacity A                     */
+    int32_t *col_ch;             /* out, capacity groups*B*C*D          */
+    int32_t *col_tap;            /* out, capacity groups*B*C*D          */
+    void *ws;                    /* device scratch, >= SA_COMPACT_WS_BYTES, 256-byte aligned */
+} sa_compact_desc;
+
+#define SA_COMPACT_WS_BYTES 4096
+
+typedef struct sa_compact_sizes {
+    int32_t groups;
+    int32_t M[SA_MAX_CONV_GROUPS];          /* kept rows of each conv group     */
+    int32_t K[SA_MAX_CONV_GROUPS];          /* kept columns of each conv group  */
+    int32_t ldk[SA_MAX_CONV_GROUPS];        /* row stride of group gc in Wc     */
+    int64_t wc_offset[SA_MAX_CONV_GROUPS];  /* element offset of group gc in Wc */
+    int32_t row_offset[SA_MAX_CONV_GROUPS]; /* offset in row_idx / output channels */
+    int32_t col_offset[SA_MAX_CONV_GROUPS]; /* offset in col_ch / col_tap       */
+    /* run[gc] > 0 when the group's columns are every tap times one run of
+     * run[gc] consecutive input channels starting at run_base[gc] (a dense
+     * channel block: filter / channel pruning); 0 for a general gather. */
+    int32_t run[SA_MAX_CONV_GROUPS];
+    int32_t run_base[SA_MAX_CONV_GROUPS];
+} sa_compact_sizes;
+
+int structadmm_compact(const sa_compact_desc *desc, sa_compact_sizes *sizes, hipStream_t stream);
+
+/* ---- input layout: structadmm_pack_nhwc ------------------------------ */
+/*
+ * X binary32 NCHW [N, Cin, H, W] -> Xp bfloat16 NHWC [N, H, W, Cx] (round to
+ * nearest even), keeping the channels with keep[ch] set (all when NULL) in
+ * ascending order; Cx must equal the number of kept channels.
+ */
+int structadmm_pack_nhwc(const float *X, int32_t N, int32_t Cin, int32_t H, int32_t W,
+                         const uint8_t *keep, int32_t Cx, uint16_t *Xp, hipStream_t stream);
+
+/* ---- compacted CONV: structadmm_conv_fwd ----------------------------- */
+/*
+ * Y[n, p, q, o] = sum_j Wc_g[m, j] * X[n, p*stride - pad + c_j, q*stride - pad + d_j, col_ch[j]]
+ * for conv group g, output channel o = sizes->row_offset[g] + m, (c_j, d_j) =
+ * (col_tap[j] / D, col_tap[j] % D); zero outside the image (cross-correlation,
+ * no bias, no dilation).  bfloat16 inputs, binary32 accumulation on the
+ * matrix cores, bfloat16 output (nearest even).
+ * X: bfloat16 NHWC [N, H, W, Cx], 16-byte aligned.
+ * Y: bfloat16 NHWC [N, P, Q, sum_g M_g], P = (H + 2*pad - C)/stride + 1, same for Q.
+ * sizes: host struct filled by structadmm_compact for the same Wc / tables.
+ */
+typedef struct sa_conv_desc {
+    int32_t N, H, W, Cx;         /* input */
+    int32_t C, D;                /* kernel height, width */
+    int32_t stride, pad;
+    const sa_compact_sizes *sizes; /* host pointer */
+    const uint16_t *X;
+    const uint16_t *Wc;
+    const int32_t *col_ch;
+    const int32_t *col_tap;
+    uint16_t *Y;
+} sa_conv_desc;
+
+int structadmm_conv_fwd(const sa_conv_desc *desc, hipStream_t stream);
+
+/* Message describing the last error on the calling thread ("" if none). */
+const char *structadmm_last_error(void);
+
+/* Library version string. */
+const char *structadmm_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* STRUCTADMM_H */

@@ -1,0 +1,246 @@
+"""Python binding of libstructadmm (gfx950): the StructADMM hot path.
+
+Thin ctypes marshalling over the C ABI in ``include/structadmm.h``: every
+step runs in the library's HIP kernels; torch is used only for device memory
+(tensor allocation) and streams.  There is no fallback: if the library is
+missing or a call fails, an exception is raised.
+
+Entry points (same names as the C ABI):
+  project(layers, ws=None, stream=None)
+  project_workspace(layers)
+  dual_update(layers, stream=None)
+  compact(Z, groups, ..., ws=None, stream=None) -> (Wc, row_idx, col_ch, col_tap, sizes)
+  pack_nhwc(X, keep=None, Cx=None, stream=None)
+  conv_fwd(X, Wc, col_ch, col_tap, sizes, C, D, stride, pad, Y=None, stream=None)
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import List, Optional, Sequence
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libstructadmm.so")
+
+FILTER, CHANNEL, SHAPE, ELEMENT = 0, 1, 2, 3
+MAX_CONV_GROUPS = 16
+MAX_STRUCT_GROUPS = 8192
+COMPACT_WS_BYTES = 4096
+ERRORS = {-1: "SA_E_ARG", -2: "SA_E_ALIGN", -3: "SA_E_WORKSPACE", -4: "SA_E_UNSUPPORTED", -5: "SA_E_HIP"}
+
+_vp = ctypes.c_void_p
+
+
+class ProjectDesc(ctypes.Structure):
+    _fields_ = [("A", ctypes.c_int64), ("B", ctypes.c_int64), ("C", ctypes.c_int64), ("D", ctypes.c_int64),
+                ("groups", ctypes.c_int32), ("kind", ctypes.c_int32), ("k", ctypes.c_int64),
+                ("W", _vp), ("U", _vp), ("in_ch_mask", _vp), ("Z", _vp), ("mask", _vp),
+                ("kept_idx", _vp), ("scores", _vp), ("rho", ctypes.c_float), ("G", _vp)]
+
+
+class DualDesc(ctypes.Structure):
+    _fields_ = [("n", ctypes.c_int64), ("W", _vp), ("Z", _vp), ("U", _vp), ("rho", ctypes.c_float),
+                ("G", _vp), ("update_dual", ctypes.c_int32)]
+
+
+class CompactDesc(ctypes.Structure):
+    _fields_ = [("A", ctypes.c_int64), ("B", ctypes.c_int64), ("C", ctypes.c_int64), ("D", ctypes.c_int64),
+                ("groups", ctypes.c_int32), ("Z", _vp), ("row_mask", _vp), ("col_mask", _vp),
+                ("chan_mask", _vp), ("in_ch_mask", _vp), ("in_compacted", ctypes.c_int32),
+                ("Wc", _vp), ("row_idx", _vp), ("col_ch", _vp), ("col_tap", _vp), ("ws", _vp)]
+
+
+_G = MAX_CONV_GROUPS
+
+
+class CompactSizes(ctypes.Structure):
+    _fields_ = [("groups", ctypes.c_int32), ("M", ctypes.c_int32 * _G), ("K", ctypes.c_int32 * _G),
+                ("ldk", ctypes.c_int32 * _G), ("wc_offset", ctypes.c_int64 * _G),
+                ("row_offset", ctypes.c_int32 * _G), ("col_offset", ctypes.c_int32 * _G),
+                ("run", ctypes.c_int32 * _G), ("run_base", ctypes.c_int32 * _G)]
+
+    def as_dict(self):
+        g = self.groups
+        return {k: list(getattr(self, k))[:g] for k in
+                ("M", "K", "ldk", "wc_offset", "row_offset", "col_offset", "run", "run_base")}
+
+
+class ConvDesc(ctypes.Structure):
+    _fields_ = [("N", ctypes.c_int32), ("H", ctypes.c_int32), ("W", ctypes.c_int32), ("Cx", ctypes.c_int32),
+                ("C", ctypes.c_int32), ("D", ctypes.c_int32), ("stride", ctypes.c_int32), ("pad", ctypes.c_int32),
+                ("sizes", ctypes.POINTER(CompactSizes)), ("X", _vp), ("Wc", _vp), ("col_ch", _vp),
+                ("col_tap", _vp), ("Y", _vp)]
+
+
+class StructAdmmError(RuntimeError):
+    pass
+
+
+_lib = None
+
+
+def lib():
+    """Loads libstructadmm.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise StructAdmmError(f"{LIB_PATH} is missing: build it with paper_1807_11091_amd/build.py")
+        L = ctypes.CDLL(LIB_PATH)
+        L.structadmm_project_workspace.argtypes = [ctypes.POINTER(ProjectDesc), ctypes.c_int]
+        L.structadmm_project_workspace.restype = ctypes.c_size_t
+        L.structadmm_project.argtypes = [ctypes.POINTER(ProjectDesc), ctypes.c_int, _vp, ctypes.c_size_t, _vp]
+        L.structadmm_project.restype = ctypes.c_int
+        L.structadmm_dual_update.argtypes = [ctypes.POINTER(DualDesc), ctypes.c_int, _vp]
+        L.structadmm_dual_update.restype = ctypes.c_int
+        L.structadmm_compact.argtypes = [ctypes.POINTER(CompactDesc), ctypes.POINTER(CompactSizes), _vp]
+        L.structadmm_compact.restype = ctypes.c_int
+        L.structadmm_pack_nhwc.argtypes = [_vp, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                           _vp, ctypes.c_int32, _vp, _vp]
+        L.structadmm_pack_nhwc.restype = ctypes.c_int
+        L.structadmm_conv_fwd.argtypes = [ctypes.POINTER(ConvDesc), _vp]
+        L.structadmm_conv_fwd.restype = ctypes.c_int
+        L.structadmm_last_error.argtypes = []
+        L.structadmm_last_error.restype = ctypes.c_char_p
+        L.structadmm_version.argtypes = []
+        L.structadmm_version.restype = ctypes.c_char_p
+        _lib = L
+    return _lib
+
+
+def _check(rc: int, what: str):
+    if rc != 0:
+        msg = lib().structadmm_last_error().decode(errors="replace")
+        raise StructAdmmError(f"{what} failed: {ERRORS.get(rc, rc)} ({rc}): {msg}")
+
+
+def _ptr(t) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    return stream if isinstance(stream, int) else stream.cuda_stream
+
+
+@dataclass
+class ProjectLayer:
+    """One layer of a projection call: tensors are torch device tensors."""
+    W: "object"
+    U: "object"
+    Z: "object"
+    mask: "object"
+    kept_idx: "object"
+    kind: int
+    k: int
+    groups: int = 1
+    in_ch_mask: "object" = None
+    scores: "object" = None
+    rho: float = 0.0
+    G: "object" = None
+
+    def desc(self) -> ProjectDesc:
+        A, B, C, D = self.W.shape
+        return ProjectDesc(A, B, C, D, self.groups, self.kind, self.k, _ptr(self.W), _ptr(self.U),
+                           _ptr(self.in_ch_mask), _ptr(self.Z), _ptr(self.mask), _ptr(self.kept_idx),
+                           _ptr(self.scores), self.rho, _ptr(self.G))
+
+
+def _descs(layers: Sequence[ProjectLayer]):
+    arr = (ProjectDesc * len(layers))()
+    for i, l in enumerate(layers):
+        arr[i] = l.desc()
+    return arr
+
+
+def project_workspace(layers: Sequence[ProjectLayer]) -> int:
+    return int(lib().structadmm_project_workspace(_descs(layers), len(layers)))
+
+
+def project(layers: Sequence[ProjectLayer], ws=None, stream=None, descs=None):
+    """structadmm_project over the layers; ``ws`` is a uint8 device tensor."""
+    d = descs if descs is not None else _descs(layers)
+    nbytes = 0 if ws is None else ws.numel() * ws.element_size()
+    _check(lib().structadmm_project(d, len(layers), _ptr(ws), nbytes, _stream(stream)), "structadmm_project")
+
+
+def dual_descs(items) -> "ctypes.Array":
+    """items: iterable of (W, Z, U, rho, G, update_dual)."""
+    items = list(items)
+    arr = (DualDesc * len(items))()
+    for i, (W, Z, U, rho, G, upd) in enumerate(items):
+        arr[i] = DualDesc(W.numel(), _ptr(W), _ptr(Z), _ptr(U), rho, _ptr(G), 1 if upd else 0)
+    return arr
+
+
+def dual_update(items, stream=None, descs=None):
+    d = descs if descs is not None else dual_descs(items)
+    _check(lib().structadmm_dual_update(d, len(d), _stream(stream)), "structadmm_dual_update")
+
+
+def compact(Z, groups: int = 1, row_mask=None, col_mask=None, chan_mask=None, in_ch_mask=None,
+            in_compacted: bool = False, ws=None, stream=None, out=None):
+    """structadmm_compact; returns (Wc, row_idx, col_ch, col_tap, sizes)."""
+    import torch
+    A, B, C, D = Z.shape
+    dev = Z.device
+    K = B * C * D
+    if out is None:
+        Wc = torch.empty(A * ((K + 7) // 8 * 8), dtype=torch.uint16, device=dev)
+        row_idx = torch.empty(A, dtype=torch.int32, device=dev)
+        col_ch = torch.empty(groups * K, dtype=torch.int32, device=dev)
+        col_tap = torch.empty(groups * K, dtype=torch.int32, device=dev)
+    else:
+        Wc, row_idx, col_ch, col_tap = out
+    if ws is None:
+        ws = torch.empty(COMPACT_WS_BYTES, dtype=torch.uint8, device=dev)
+    desc = CompactDesc(A, B, C, D, groups, _ptr(Z), _ptr(row_mask), _ptr(col_mask), _ptr(chan_mask),
+                       _ptr(in_ch_mask), 1 if in_compacted else 0, _ptr(Wc), _ptr(row_idx), _ptr(col_ch),
+                       _ptr(col_tap), _ptr(ws))
+    sizes = CompactSizes()
+    _check(lib().structadmm_compact(ctypes.byref(desc), ctypes.byref(sizes), _stream(stream)), "structadmm_compact")
+    return Wc, row_idx, col_ch, col_tap, sizes
+
+
+def pack_nhwc(X, keep=None, Cx: Optional[int] = None, out=None, stream=None):
+    """fp32 NCHW -> bf16 NHWC (uint16 bits) with an optional channel keep mask."""
+    import torch
+    N, Cin, H, W = X.shape
+    if Cx is None:
+        Cx = Cin if keep is None else int(keep.count_nonzero().item())
+    Xp = out if out is not None else torch.empty((N, H, W, Cx), dtype=torch.uint16, device=X.device)
+    _check(lib().structadmm_pack_nhwc(_ptr(X), N, Cin, H, W, _ptr(keep), Cx, _ptr(Xp), _stream(stream)),
+           "structadmm_pack_nhwc")
+    return Xp
+
+
+def conv_out_shape(N, H, W, C, D, stride, pad, sizes: CompactSizes):
+    P = (H + 2 * pad - C) // stride + 1
+    Q = (W + 2 * pad - D) // stride + 1
+    return (N, P, Q, int(sum(sizes.M[g] for g in range(sizes.groups))))
+
+
+def conv_desc(Xp, Wc, col_ch, col_tap, sizes: CompactSizes, C, D, stride, pad, Y) -> ConvDesc:
+    N, H, W, Cx = Xp.shape
+    return ConvDesc(N, H, W, Cx, C, D, stride, pad, ctypes.pointer(sizes), _ptr(Xp), _ptr(Wc),
+                    _ptr(col_ch), _ptr(col_tap), _ptr(Y))
+
+
+def conv_fwd(Xp, Wc, col_ch, col_tap, sizes: CompactSizes, C: int, D: int, stride: int, pad: int,
+             Y=None, stream=None, desc: Optional[ConvDesc] = None):
+    """structadmm_conv_fwd; Xp bf16 NHWC (uint16), returns Y bf16 NHWC (uint16)."""
+    import torch
+    if desc is None:
+        N, H, W, Cx = Xp.shape
+        if Y is None:
+            Y = torch.empty(conv_out_shape(N, H, W, C, D, stride, pad, sizes), dtype=torch.uint16,
+                            device=Xp.device)
+        desc = conv_desc(Xp, Wc, col_ch, col_tap, sizes, C, D, stride, pad, Y)
+    _check(lib().structadmm_conv_fwd(ctypes.byref(desc), _stream(stream)), "structadmm_conv_fwd")
+    return Y
+
+
+def version() -> str:
+    return lib().structadmm_version().decode()

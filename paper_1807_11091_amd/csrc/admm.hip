@@ -1,0 +1,1053 @@
+// gfx950 kernels and entry points of the ADMM Z-update (projection onto the
+// sparsity sets of Section 3, as solved in Section 4) and of the dual update /
+// gradient of eq. (3).
+//
+// Data flow of structadmm_project for one dependency level of layers:
+//   k_expand_allowed  (layers with an input-channel support) per-column support bytes
+//   k_row_scores      filter sets: one wavefront per weight row, O_a in binary64
+//   k_col_partials    channel / shape sets: binary64 column sums per band of rows
+//   k_select          one workgroup per structured layer: final scores, LDS radix
+//                     select on the 64-bit score bits, lowest-index tie-break,
+//                     mask + ascending kept_idx, per-column keep bytes
+//   k_elem_*          non-structured sets: 3 histogram passes over |v| bits, then an
+//                     order-preserving count / scan / apply
+//   k_apply           row-streaming Z (+ fused U', G) writer
+// Every reduction has a fixed order; no floating-point atomics are used.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdint>
+#include <cstring>
+#include <vector>
+
+#include "sa_device.h"
+#include "sa_host.h"
+#include "structadmm.h"
+
+namespace sa {
+namespace {
+
+constexpr int kTab = 16;           // layers per launch (kernel-argument table)
+constexpr int kRowThreads = 256;   // 4 wavefronts, one weight row each at a time
+constexpr int kColThreads = 256;
+constexpr int kColBand = 16;       // rows per band of column partial sums
+constexpr int kSelThreads = 1024;
+constexpr int kElemThreads = 256;
+constexpr int kElemPerThread = 8;
+constexpr int kElemChunk = kElemThreads * kElemPerThread;  // elements per workgroup
+constexpr int kElemHistBlocks = 1024;
+
+// ---------------------------------------------------------------- tables
+struct RowLayer {
+    const float *W;
+    float *U;
+    float *Z;
+    float *G;
+    const uint8_t *rowkeep;  // [A] or null: every row kept
+    const uint8_t *colkeep;  // [groups*K] or null: every column kept
+    const uint8_t *allowed;  // [groups*K] or null: every entry inside the support
+    double *scores;          // [A] (row scores)
+    int32_t A, K, Ag, rpb;   // rows, row length, rows per conv group, rows per workgroup
+    int32_t vec;             // K % 4 == 0: float4 path
+    float rho;
+};
+struct RowTab {
+    RowLayer L[kTab];
+    int32_t begin[kTab + 1];
+    int32_t nl;
+};
+
+struct ColLayer {
+    const float *W;
+    const float *U;
+    const uint8_t *allowed;
+    double *partials;  // [nbands][K]
+    int32_t A, K, Ag, nbands, ctiles, vec;
+};
+struct ColTab {
+    ColLayer L[kTab];
+    int32_t begin[kTab + 1];
+    int32_t nl;
+};
+
+struct SelLayer {
+    const double *partials;  // channel / shape: [nbands][K]
+    double *scores;          // [G]: filter: input; channel / shape: output
+    uint8_t *mask;           // [G]
+    int32_t *kept_idx;       // [k]
+    uint8_t *colkeep;        // [groups*K] or null
+    const uint8_t *allowed;  // [groups*K] or null
+    int32_t kind, G, k, K, CD, nbands, groups;
+};
+struct SelTab {
+    SelLayer L[kTab];
+    int32_t nl;
+};
+
+struct DualLayer {
+    const float *W;
+    const float *Z;
+    float *U;
+    float *G;
+    int32_t n, update;
+    float rho;
+};
+struct DualTab {
+    DualLayer L[kTab];
+    int32_t begin[kTab + 1];
+    int32_t nl;
+};
+
+__device__ inline int find_layer(const int32_t *begin, int nl, int b) {
+    int li = 0;
+    while (li + 1 < nl && b >= begin[li + 1]) ++li;
+    return li;
+}
+
+// ---------------------------------------------------------------- support
+// allowed[gc*K + j] = in_ch_mask[gc*B + j / CD]
+__global__ void k_expand_allowed(const uint8_t *__restrict__ in_ch_mask, uint8_t *__restrict__ allowed,
+                                 int groups, int B, int CD, int K) {
+    int64_t total = (int64_t)groups * K;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        int gc = (int)(i / K);
+        int j = (int)(i - (int64_t)gc * K);
+        allowed[i] = in_ch_mask[gc * B + j / CD] ? 1 : 0;
+    }
+}
+
+// ---------------------------------------------------------------- scores
+__device__ inline float masked(float v, uint8_t keep) { return keep ? v : 0.0f; }
+
+// O_a = sum_j (double)v_aj^2 for each filter a (Section 4, filter-wise set).
+__global__ __launch_bounds__(kRowThreads) void k_row_scores(RowTab tab) {
+    const int li = find_layer(tab.begin, tab.nl, blockIdx.x);
+    const RowLayer &L = tab.L[li];
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int r0 = (blockIdx.x - tab.begin[li]) * L.rpb;
+    const int r1 = min(L.A, r0 + L.rpb);
+    for (int a = r0 + wave; a < r1; a += kRowThreads / kWave) {
+        const int64_t base = (int64_t)a * L.K;
+        const uint8_t *al = L.allowed ? L.allowed + (int64_t)(a / L.Ag) * L.K : nullptr;
+        double acc = 0.0;
+        if (L.vec) {
+            const float4 *w4 = reinterpret_cast<const float4 *>(L.W + base);
+            const float4 *u4 = reinterpret_cast<const float4 *>(L.U + base);
+            const uchar4 *a4 = reinterpret_cast<const uchar4 *>(al);
+            const int K4 = L.K >> 2;
+            for (int i0 = 0; i0 < K4; i0 += 4 * kWave) {
+                float4 x[4], y[4];
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    int i = i0 + u * kWave + lane;
+                    if (i < K4) {
+                        x[u] = w4[i];
+                        y[u] = u4[i];
+                    } else {
+                        x[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+                        y[u] = x[u];
+                    }
+                }
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    int i = i0 + u * kWave + lane;
+                    float v0 = x[u].x + y[u].x, v1 = x[u].y + y[u].y;
+                    float v2 = x[u].z + y[u].z, v3 = x[u].w + y[u].w;
+                    if (a4 && i < K4) {
+                        uchar4 m = a4[i];
+                        v0 = masked(v0, m.x); v1 = masked(v1, m.y);
+                        v2 = masked(v2, m.z); v3 = masked(v3, m.w);
+                    }
+                    acc += (double)v0 * (double)v0;
+                    acc += (double)v1 * (double)v1;
+                    acc += (double)v2 * (double)v2;
+                    acc += (double)v3 * (double)v3;
+                }
+            }
+        } else {
+            for (int i = lane; i < L.K; i += kWave) {
+                float v = L.W[base + i] + L.U[base + i];
+                if (al) v = masked(v, al[i]);
+                acc += (double)v * (double)v;
+            }
+        }
+        acc = wave_sum(acc);
+        if (lane == 0) L.scores[a] = acc;
+    }
+}
+
+// partials[band][j] = sum over rows a of the band of (double)v_aj^2
+// (column sums; channel and shape scores are finished in k_select).
+__global__ __launch_bounds__(kColThreads) void k_col_partials(ColTab tab) {
+    const int li = find_layer(tab.begin, tab.nl, blockIdx.x);
+    const ColLayer &L = tab.L[li];
+    const int lb = blockIdx.x - tab.begin[li];
+    const int band = lb / L.ctiles, ct = lb - band * L.ctiles;
+    const int a0 = band * kColBand, a1 = min(L.A, a0 + kColBand);
+    if (L.vec) {
+        const int j = (ct * kColThreads + threadIdx.x) * 4;
+        if (j >= L.K) return;
+        double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
+        for (int a = a0; a < a1; ++a) {
+            const int64_t off = (int64_t)a * L.K + j;
+            float4 x = *reinterpret_cast<const float4 *>(L.W + off);
+            float4 y = *reinterpret_cast<const float4 *>(L.U + off);
+            float v0 = x.x + y.x, v1 = x.y + y.y, v2 = x.z + y.z, v3 = x.w + y.w;
+            if (L.allowed) {
+                uchar4 m = *reinterpret_cast<const uchar4 *>(L.allowed + (int64_t)(a / L.Ag) * L.K + j);
+                v0 = masked(v0, m.x); v1 = masked(v1, m.y);
+                v2 = masked(v2, m.z); v3 = masked(v3, m.w);
+            }
+            s0 += (double)v0 * (double)v0;
+            s1 += (double)v1 * (double)v1;
+            s2 += (double)v2 * (double)v2;
+            s3 += (double)v3 * (double)v3;
+        }
+        double *p = L.partials + (int64_t)band * L.K + j;
+        p[0] = s0; p[1] = s1; p[2] = s2; p[3] = s3;
+    } else {
+        const int j = ct * kColThreads + threadIdx.x;
+        if (j >= L.K) return;
+        double s = 0.0;
+        for (int a = a0; a < a1; ++a) {
+            const int64_t off = (int64_t)a * L.K + j;
+            float v = L.W[off] + L.U[off];
+            if (L.allowed) v = masked(v, L.allowed[(int64_t)(a / L.Ag) * L.K + j]);
+            s += (double)v * (double)v;
+        }
+        L.partials[(int64_t)band * L.K + j] = s;
+    }
+}
+
+// ---------------------------------------------------------------- select
+// One workgroup per structured layer.  Keeps exactly k groups: those whose
+// score exceeds the k-th largest score T, plus the lowest-index groups whose
+// score equals T.  Scores are non-negative binary64 values, so their bit
+// patterns order like unsigned integers; T is found by an 8-pass MSB-first
+// radix select (8-bit digits) over those bits in LDS.
+__global__ __launch_bounds__(kSelThreads) void k_select(SelTab tab) {
+    __shared__ uint64_t skey[SA_MAX_STRUCT_GROUPS];
+    __shared__ uint8_t smask[SA_MAX_STRUCT_GROUPS];
+    __shared__ uint32_t hist[256];
+    __shared__ uint32_t scan_tmp[kSelThreads / kWave + 1];
+    __shared__ uint64_t s_prefix;
+    __shared__ uint32_t s_kk;
+
+    const SelLayer &L = tab.L[blockIdx.x];
+    const int tid = threadIdx.x;
+    const int G = L.G;
+
+    // 1. final scores
+    for (int g = tid; g < G; g += kSelThreads) {
+        double s;
+        if (L.kind == SA_FILTER) {
+            s = L.scores[g];
+        } else if (L.kind == SA_SHAPE) {
+            s = 0.0;
+            for (int b = 0; b < L.nbands; ++b) s += L.partials[(int64_t)b * L.K + g];
+        } else {  // channel: sum over taps, then bands
+            s = 0.0;
+            for (int t = 0; t < L.CD; ++t)
+                for (int b = 0; b < L.nbands; ++b) s += L.partials[(int64_t)b * L.K + g * L.CD + t];
+        }
+        if (L.kind != SA_FILTER) L.scores[g] = s;
+        skey[g] = __double_as_longlong(s);
+    }
+    if (tid == 0) {
+        s_prefix = 0;
+        s_kk = (uint32_t)L.k;
+    }
+    __syncthreads();
+
+    // 2. T = k-th largest key (k >= 1)
+    if (L.k > 0) {
+        for (int pass = 0; pass < 8; ++pass) {
+            const int shift = 56 - 8 * pass;
+            if (tid < 256) hist[tid] = 0;
+            __syncthreads();
+            const uint64_t prefix = s_prefix;
+            for (int g = tid; g < G; g += kSelThreads) {
+                uint64_t key = skey[g];
+                bool match = pass == 0 || (key >> (shift + 8)) == prefix;
+                if (match) atomicAdd(&hist[(uint32_t)(key >> shift) & 255u], 1u);
+            }
+            __syncthreads();
+            if (tid < kWave) {
+                // lane l owns digits 255-4l .. 252-4l (descending)
+                uint32_t c[4];
+                uint32_t sum = 0;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    c[q] = hist[255 - 4 * tid - q];
+                    sum += c[q];
+                }
+                uint32_t incl = wave_incl_scan(sum);
+                uint32_t excl = incl - sum;
+                const uint32_t kk = s_kk;
+                if (excl < kk && kk <= incl) {
+                    uint32_t above = excl;
+                    int d = 0;
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        if (above + c[q] >= kk) {
+                            d = 255 - 4 * tid - q;
+                            break;
+                        }
+                        above += c[q];
+                    }
+                    s_prefix = (prefix << 8) | (uint64_t)d;
+                    s_kk = kk - above;
+                }
+            }
+            __syncthreads();
+        }
+    }
+    const uint64_t T = s_prefix;
+    const uint32_t need = L.k > 0 ? s_kk : 0u;  // ties at T to keep
+
+    // 3. ordered scans: tie ranks, then kept positions
+    const int per = (G + kSelThreads - 1) / kSelThreads;
+    const int g0 = min(G, tid * per), g1 = min(G, g0 + per);
+    uint32_t eq_local = 0;
+    if (L.k > 0)
+        for (int g = g0; g < g1; ++g) eq_local += skey[g] == T;
+    uint32_t total;
+    uint32_t eq_before = block_excl_scan(eq_local, scan_tmp, &total);
+    uint32_t kept_local = 0;
+    {
+        uint32_t r = eq_before;
+        for (int g = g0; g < g1; ++g) {
+            bool keep = false;
+            if (L.k > 0) {
+                uint64_t key = skey[g];
+                if (key > T) keep = true;
+                else if (key == T) keep = (r++ < need);
+            }
+            smask[g] = keep ? 1 : 0;
+            kept_local += keep;
+        }
+    }
+    uint32_t kept_before = block_excl_scan(kept_local, scan_tmp, &total);
+    {
+        uint32_t pos = kept_before;
+        for (int g = g0; g < g1; ++g) {
+            L.mask[g] = smask[g];
+            if (smask[g] && pos < (uint32_t)L.k) L.kept_idx[pos] = g;
+            pos += smask[g];
+        }
+    }
+    __syncthreads();
+
+    // 4. per-column keep bytes for the apply pass
+    if (L.colkeep) {
+        const int64_t total_cols = (int64_t)L.groups * L.K;
+        for (int64_t i = tid; i < total_cols; i += kSelThreads) {
+            const int gc = (int)(i / L.K);
+            const int j = (int)(i - (int64_t)gc * L.K);
+            uint8_t sel = 1;
+            if (L.kind == SA_SHAPE) sel = smask[j];
+            else if (L.kind == SA_CHANNEL) sel = smask[j / L.CD];
+            uint8_t al = L.allowed ? L.allowed[i] : 1;
+            L.colkeep[i] = (sel && al) ? 1 : 0;
+        }
+    }
+}
+
+// ---------------------------------------------------------------- apply
+// Z = v on kept entries, +0 elsewhere; fused: U' = v - Z, G = rho * ((W - Z) + U').
+__global__ __launch_bounds__(kRowThreads) void k_apply(RowTab tab) {
+    const int li = find_layer(tab.begin, tab.nl, blockIdx.x);
+    const RowLayer &L = tab.L[li];
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int r0 = (blockIdx.x - tab.begin[li]) * L.rpb;
+    const int r1 = min(L.A, r0 + L.rpb);
+    const bool fused = L.G != nullptr;
+    for (int a = r0 + wave; a < r1; a += kRowThreads / kWave) {
+        const int64_t base = (int64_t)a * L.K;
+        const bool rk = L.rowkeep ? (L.rowkeep[a] != 0) : true;
+        const uint8_t *ck = L.colkeep ? L.colkeep + (int64_t)(a / L.Ag) * L.K : nullptr;
+        if (L.vec) {
+            const int K4 = L.K >> 2;
+            float4 *z4 = reinterpret_cast<float4 *>(L.Z + base);
+            if (!rk && !fused) {
+                // pruned row, projection only: Z = 0 without touching W, U
+                for (int i = lane; i < K4; i += kWave) z4[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+                continue;
+            }
+            const float4 *w4 = reinterpret_cast<const float4 *>(L.W + base);
+            float4 *u4 = reinterpret_cast<float4 *>(L.U + base);
+            float4 *g4 = fused ? reinterpret_cast<float4 *>(L.G + base) : nullptr;
+            const uchar4 *c4 = reinterpret_cast<const uchar4 *>(ck);
+            for (int i0 = 0; i0 < K4; i0 += 4 * kWave) {
+                float4 x[4], y[4];
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    int i = i0 + u * kWave + lane;
+                    if (i < K4) {
+                        x[u] = w4[i];
+                        y[u] = u4[i];
+                    }
+                }
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    int i = i0 + u * kWave + lane;
+                    if (i >= K4) continue;
+                    uchar4 m = c4 ? c4[i] : make_uchar4(1, 1, 1, 1);
+                    float v[4] = {x[u].x + y[u].x, x[u].y + y[u].y, x[u].z + y[u].z, x[u].w + y[u].w};
+                    float w[4] = {x[u].x, x[u].y, x[u].z, x[u].w};
+                    uint8_t mk[4] = {m.x, m.y, m.z, m.w};
+                    float z[4], un[4], gg[4];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        z[e] = (rk && mk[e]) ? v[e] : 0.0f;
+                        un[e] = v[e] - z[e];
+                        float wz = w[e] - z[e];
+                        float s = wz + un[e];
+                        gg[e] = L.rho * s;
+                    }
+                    z4[i] = make_float4(z[0], z[1], z[2], z[3]);
+                    if (fused) {
+                        u4[i] = make_float4(un[0], un[1], un[2], un[3]);
+                        g4[i] = make_float4(gg[0], gg[1], gg[2], gg[3]);
+                    }
+                }
+            }
+        } else {
+            for (int i = lane; i < L.K; i += kWave) {
+                float w = L.W[base + i];
+                float v = w + L.U[base + i];
+                float z = (rk && (!ck || ck[i])) ? v : 0.0f;
+                L.Z[base + i] = z;
+                if (fused) {
+                    float un = v - z;
+                    float wz = w - z;
+                    float s = wz + un;
+                    L.U[base + i] = un;
+                    L.G[base + i] = L.rho * s;
+                }
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------- element-wise
+struct ElemState {
+    uint32_t prefix;  // digits of T found so far; after the last pass, T itself
+    uint32_t kk;      // rank of T among keys matching the prefix
+    uint32_t gt;      // keys known to exceed T
+    uint32_t pad;
+};
+
+struct ElemArgs {
+    const float *W;
+    float *U;
+    float *Z;
+    float *G;
+    uint8_t *mask;
+    int32_t *kept_idx;
+    double *scores;          // [n] keys as |v| in binary64, or null
+    const uint8_t *allowed;  // [groups*K] or null
+    uint32_t *hist;          // [3][2048]
+    ElemState *state;
+    uint32_t *chunk_counts;  // [nchunks][2]: (gt, eq)
+    uint32_t *chunk_prefix;  // [nchunks][2]: exclusive prefixes
+    FastDiv divK;            // e -> row
+    int32_t n, K, Ag, k, nchunks, vec;
+    float rho;
+};
+
+// Is entry e inside the input-channel support?
+__device__ inline bool elem_allowed(uint32_t e, const ElemArgs &a) {
+    if (!a.allowed) return true;
+    uint32_t row = fdiv(e, a.divK);
+    uint32_t j = e - row * (uint32_t)a.K;
+    return a.allowed[(int64_t)(row / a.Ag) * a.K + j] != 0;
+}
+
+// Key of entry e: |v| as binary32 bits (sign cleared); 0 outside the support.
+__device__ inline uint32_t elem_key(float v, uint32_t e, const ElemArgs &a) {
+    uint32_t key = __float_as_uint(v) & 0x7fffffffu;
+    return elem_allowed(e, a) ? key : 0u;
+}
+
+__device__ inline void elem_load8(const ElemArgs &a, int64_t e0, float *w, float *v) {
+    if (a.vec && e0 + 8 <= a.n) {
+        float4 w0 = *reinterpret_cast<const float4 *>(a.W + e0);
+        float4 w1 = *reinterpret_cast<const float4 *>(a.W + e0 + 4);
+        float4 u0 = *reinterpret_cast<const float4 *>(a.U + e0);
+        float4 u1 = *reinterpret_cast<const float4 *>(a.U + e0 + 4);
+        w[0] = w0.x; w[1] = w0.y; w[2] = w0.z; w[3] = w0.w;
+        w[4] = w1.x; w[5] = w1.y; w[6] = w1.z; w[7] = w1.w;
+        v[0] = w0.x + u0.x; v[1] = w0.y + u0.y; v[2] = w0.z + u0.z; v[3] = w0.w + u0.w;
+        v[4] = w1.x + u1.x; v[5] = w1.y + u1.y; v[6] = w1.z + u1.z; v[7] = w1.w + u1.w;
+    } else {
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            int64_t e = e0 + q;
+            if (e < a.n) {
+                w[q] = a.W[e];
+                v[q] = w[q] + a.U[e];
+            } else {
+                w[q] = 0.f;
+                v[q] = 0.f;
+            }
+        }
+    }
+}
+
+__global__ void k_elem_init(ElemArgs a) {
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < 3 * 2048) a.hist[i] = 0;
+    if (i == 0) {
+        a.state->prefix = a.k > 0 ? 0u : 0x80000000u;  // k = 0: T above every key
+        a.state->kk = (uint32_t)a.k;
+        a.state->gt = 0;
+        a.state->pad = 0;
+    }
+}
+
+// Histogram of one digit of the keys that match the digits found so far.
+// Digits: pass 0 = bits 30..20, pass 1 = bits 19..9, pass 2 = bits 8..0.
+__global__ __launch_bounds__(kElemThreads) void k_elem_hist(ElemArgs a, int pass) {
+    __shared__ uint32_t h[2048];
+    for (int i = threadIdx.x; i < 2048; i += kElemThreads) h[i] = 0;
+    __syncthreads();
+    const uint32_t prefix = a.state->prefix;
+    const int dshift = pass == 0 ? 20 : (pass == 1 ? 9 : 0);
+    const uint32_t dmask = pass == 2 ? 0x1ffu : 0x7ffu;
+    const int mshift = pass == 0 ? 31 : (pass == 1 ? 20 : 9);
+    for (int c = blockIdx.x; c < a.nchunks; c += gridDim.x) {
+        const int64_t e0 = (int64_t)c * kElemChunk + (int64_t)threadIdx.x * kElemPerThread;
+        float w[8], v[8];
+        elem_load8(a, e0, w, v);
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            if (e0 + q >= a.n) break;
+            uint32_t key = elem_key(v[q], (uint32_t)(e0 + q), a);
+            if (pass == 0 || (key >> mshift) == prefix) atomicAdd(&h[(key >> dshift) & dmask], 1u);
+        }
+    }
+    __syncthreads();
+    uint32_t *gh = a.hist + pass * 2048;
+    for (int i = threadIdx.x; i < 2048; i += kElemThreads)
+        if (h[i]) atomicAdd(&gh[i], h[i]);
+}
+
+// Picks the digit holding the kk-th largest key (one wavefront).
+__global__ void k_elem_find(ElemArgs a, int pass) {
+    const int lane = threadIdx.x;
+    const int bins = pass == 2 ? 512 : 2048;
+    const int bits = pass == 2 ? 9 : 11;
+    const int per = bins / kWave;
+    const uint32_t *gh = a.hist + pass * 2048;
+    const uint32_t kk = a.state->kk;
+    const uint32_t prefix = a.state->prefix;
+    uint32_t sum = 0;
+    for (int q = 0; q < per; ++q) sum += gh[bins - 1 - lane * per - q];
+    uint32_t incl = wave_incl_scan(sum);
+    uint32_t excl = incl - sum;
+    if (excl < kk && kk <= incl) {
+        uint32_t above = excl;
+        int d = 0;
+        for (int q = 0; q < per; ++q) {
+            int dig = bins - 1 - lane * per - q;
+            uint32_t c = gh[dig];
+            if (above + c >= kk) {
+                d = dig;
+                break;
+            }
+            above += c;
+        }
+        a.state->prefix = (prefix << bits) | (uint32_t)d;
+        a.state->kk = kk - above;
+        a.state->gt += above;
+    }
+}
+
+// Per-chunk counts of keys above T and equal to T.
+__global__ __launch_bounds__(kElemThreads) void k_elem_count(ElemArgs a) {
+    __shared__ uint32_t red[2][kElemThreads / kWave];
+    const int c = blockIdx.x;
+    const uint32_t T = a.state->prefix;
+    const int64_t e0 = (int64_t)c * kElemChunk + (int64_t)threadIdx.x * kElemPerThread;
+    float w[8], v[8];
+    elem_load8(a, e0, w, v);
+    uint32_t gt = 0, eq = 0;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+        if (e0 + q >= a.n) break;
+        uint32_t key = elem_key(v[q], (uint32_t)(e0 + q), a);
+        gt += key > T;
+        eq += key == T;
+    }
+    gt = wave_sum_u32(gt);
+    eq = wave_sum_u32(eq);
+    const int wave = threadIdx.x >> 6;
+    if ((threadIdx.x & 63) == 0) {
+        red[0][wave] = gt;
+        red[1][wave] = eq;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        uint32_t g = 0, e = 0;
+        for (int i = 0; i < kElemThreads / kWave; ++i) {
+            g += red[0][i];
+            e += red[1][i];
+        }
+        a.chunk_counts[2 * c] = g;
+        a.chunk_counts[2 * c + 1] = e;
+    }
+}
+
+// Exclusive prefixes of the per-chunk counts (one workgroup, chunk order).
+__global__ __launch_bounds__(1024) void k_elem_scan(ElemArgs a) {
+    __shared__ uint32_t tmp[1024 / kWave + 1];
+    uint32_t carry_gt = 0, carry_eq = 0;
+    for (int base = 0; base < a.nchunks; base += 1024) {
+        const int c = base + threadIdx.x;
+        uint32_t g = c < a.nchunks ? a.chunk_counts[2 * c] : 0u;
+        uint32_t e = c < a.nchunks ? a.chunk_counts[2 * c + 1] : 0u;
+        uint32_t tg, te;
+        uint32_t pg = block_excl_scan(g, tmp, &tg);
+        uint32_t pe = block_excl_scan(e, tmp, &te);
+        if (c < a.nchunks) {
+            a.chunk_prefix[2 * c] = carry_gt + pg;
+            a.chunk_prefix[2 * c + 1] = carry_eq + pe;
+        }
+        carry_gt += tg;
+        carry_eq += te;
+    }
+}
+
+// Mask, ascending kept_idx, Z (+ fused U', G) for the non-structured set.
+__global__ __launch_bounds__(kElemThreads) void k_elem_apply(ElemArgs a) {
+    __shared__ uint32_t tmp[kElemThreads / kWave + 1];
+    const int c = blockIdx.x;
+    const uint32_t T = a.state->prefix;
+    const uint32_t need = a.state->kk;  // ties at T kept overall (0 when k = 0)
+    const uint32_t gt_before = a.chunk_prefix[2 * c];
+    const uint32_t eq_before = a.chunk_prefix[2 * c + 1];
+    const int64_t e0 = (int64_t)c * kElemChunk + (int64_t)threadIdx.x * kElemPerThread;
+    float w[8], v[8];
+    elem_load8(a, e0, w, v);
+    uint32_t key[8];
+    uint32_t eq = 0;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+        key[q] = (e0 + q < a.n) ? elem_key(v[q], (uint32_t)(e0 + q), a) : 0u;
+        eq += (e0 + q < a.n) && key[q] == T;
+    }
+    uint32_t total;
+    uint32_t eq_rank = eq_before + block_excl_scan(eq, tmp, &total);
+    bool keep[8];
+    uint32_t kept = 0;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+        keep[q] = false;
+        if (e0 + q < a.n && a.k > 0) {
+            if (key[q] > T) keep[q] = true;
+            else if (key[q] == T) keep[q] = (eq_rank++ < need);
+        }
+        kept += keep[q];
+    }
+    const uint32_t kept_chunk_before = gt_before + min(eq_before, need);
+    uint32_t pos = kept_chunk_before + block_excl_scan(kept, tmp, &total);
+    const bool fused = a.G != nullptr;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+        const int64_t e = e0 + q;
+        if (e >= a.n) break;
+        // a kept entry outside the support (score 0) still projects to 0
+        const float z = (keep[q] && elem_allowed((uint32_t)e, a)) ? v[q] : 0.0f;
+        a.Z[e] = z;
+        a.mask[e] = keep[q] ? 1 : 0;
+        if (a.scores) a.scores[e] = (double)__uint_as_float(key[q]);
+        if (keep[q] && pos < (uint32_t)a.k) a.kept_idx[pos] = (int32_t)e;
+        pos += keep[q] ? 1u : 0u;
+        if (fused) {
+            float un = v[q] - z;
+            float wz = w[q] - z;
+            float s = wz + un;
+            a.U[e] = un;
+            a.G[e] = a.rho * s;
+        }
+    }
+}
+
+// ---------------------------------------------------------------- dual
+constexpr int kDualThreads = 256;
+constexpr int kDualVecPerThread = 4;  // float4 per thread per workgroup pass
+constexpr int kDualChunk = kDualThreads * kDualVecPerThread * 4;
+
+// U <- (U + W) - Z;  G = rho * ((W - Z) + U)   (U new, or unchanged if !update)
+__global__ __launch_bounds__(kDualThreads) void k_dual(DualTab tab) {
+    const int li = find_layer(tab.begin, tab.nl, blockIdx.x);
+    const DualLayer &L = tab.L[li];
+    const int64_t c0 = (int64_t)(blockIdx.x - tab.begin[li]) * kDualChunk;
+    const int n4 = L.n >> 2;
+#pragma unroll
+    for (int u = 0; u < kDualVecPerThread; ++u) {
+        const int64_t i = (c0 >> 2) + (int64_t)u * kDualThreads + threadIdx.x;
+        if (i < n4) {
+            float4 w = reinterpret_cast<const float4 *>(L.W)[i];
+            float4 z = reinterpret_cast<const float4 *>(L.Z)[i];
+            float4 uu = reinterpret_cast<float4 *>(L.U)[i];
+            float wv[4] = {w.x, w.y, w.z, w.w}, zv[4] = {z.x, z.y, z.z, z.w};
+            float uv[4] = {uu.x, uu.y, uu.z, uu.w}, gv[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                if (L.update) {
+                    float s = uv[e] + wv[e];
+                    uv[e] = s - zv[e];
+                }
+                float wz = wv[e] - zv[e];
+                float t = wz + uv[e];
+                gv[e] = L.rho * t;
+            }
+            if (L.update) reinterpret_cast<float4 *>(L.U)[i] = make_float4(uv[0], uv[1], uv[2], uv[3]);
+            if (L.G) reinterpret_cast<float4 *>(L.G)[i] = make_float4(gv[0], gv[1], gv[2], gv[3]);
+        }
+    }
+    // scalar tail (n % 4 entries), handled by the layer's first workgroup
+    if (blockIdx.x == tab.begin[li] && threadIdx.x < (L.n & 3)) {
+        const int64_t e = (int64_t)n4 * 4 + threadIdx.x;
+        float u = L.U[e];
+        if (L.update) {
+            float s = u + L.W[e];
+            u = s - L.Z[e];
+            L.U[e] = u;
+        }
+        if (L.G) {
+            float wz = L.W[e] - L.Z[e];
+            float t = wz + u;
+            L.G[e] = L.rho * t;
+        }
+    }
+}
+
+// ---------------------------------------------------------------- host planning
+struct LayerPlan {
+    int64_t G;
+    int K, CD, Ag, rpb, nbands, ctiles, vec, nchunks;
+    size_t off_scores, off_partials, off_allowed, off_colkeep, off_elem;
+    size_t end;
+};
+
+size_t align256(size_t x) { return (x + 255) / 256 * 256; }
+
+void plan_layer(const sa_project_desc &d, size_t start, LayerPlan &p) {
+    p.G = n_groups(d);
+    p.K = (int)(d.B * d.C * d.D);
+    p.CD = (int)(d.C * d.D);
+    p.Ag = (int)(d.A / d.groups);
+    p.vec = (p.K % 4 == 0) ? 1 : 0;
+    int rpb = (int)std::max<int64_t>(4, std::min<int64_t>(64, 16384 / std::max(1, p.K)));
+    p.rpb = rpb / 4 * 4;
+    p.nbands = (int)((d.A + kColBand - 1) / kColBand);
+    const int cols_per_block = p.vec ? kColThreads * 4 : kColThreads;
+    p.ctiles = (p.K + cols_per_block - 1) / cols_per_block;
+    const int64_t n = d.A * d.B * d.C * d.D;
+    p.nchunks = (int)((n + kElemChunk - 1) / kElemChunk);
+    size_t off = align256(start);
+    p.off_scores = p.off_partials = p.off_allowed = p.off_colkeep = p.off_elem = SIZE_MAX;
+    if (d.kind != SA_ELEMENT && !d.scores) {
+        p.off_scores = off;
+        off = align256(off + sizeof(double) * p.G);
+    }
+    if (d.kind == SA_CHANNEL || d.kind == SA_SHAPE) {
+        p.off_partials = off;
+        off = align256(off + sizeof(double) * (size_t)p.nbands * p.K);
+    }
+    if (d.in_ch_mask) {
+        p.off_allowed = off;
+        off = align256(off + (size_t)d.groups * p.K);
+    }
+    if (d.kind == SA_CHANNEL || d.kind == SA_SHAPE) {
+        p.off_colkeep = off;
+        off = align256(off + (size_t)d.groups * p.K);
+    }
+    if (d.kind == SA_ELEMENT) {
+        p.off_elem = off;
+        off = align256(off + sizeof(uint32_t) * 3 * 2048 + sizeof(ElemState) +
+                       sizeof(uint32_t) * 4 * (size_t)p.nchunks + 256);
+    }
+    p.end = off;
+}
+
+template <typename T>
+T *ws_at(void *ws, size_t off) {
+    return reinterpret_cast<T *>(static_cast<char *>(ws) + off);
+}
+
+int launch_check(const char *what) { return check_hip(hipGetLastError(), what); }
+
+}  // namespace
+}  // namespace sa
+
+using namespace sa;
+
+extern "C" size_t structadmm_project_workspace(const sa_project_desc *layers, int n_layers) {
+    if (!layers || n_layers <= 0) return 0;
+    size_t off = 0;
+    for (int i = 0; i < n_layers; ++i) {
+        if (validate_project(layers[i], i) != SA_OK) {
+            clear_error();
+            return 0;
+        }
+        LayerPlan p;
+        plan_layer(layers[i], off, p);
+        off = p.end;
+    }
+    return off;
+}
+
+extern "C" int structadmm_project(const sa_project_desc *layers, int n_layers, void *ws,
+                                  size_t ws_bytes, hipStream_t stream) {
+    clear_error();
+    if (!layers || n_layers <= 0) return fail(SA_E_ARG, "project: layers must be a non-empty array");
+    std::vector<LayerPlan> plan(n_layers);
+    size_t off = 0;
+    for (int i = 0; i < n_layers; ++i) {
+        int rc = validate_project(layers[i], i);
+        if (rc) return rc;
+        plan_layer(layers[i], off, plan[i]);
+        off = plan[i].end;
+    }
+    if (off > 0) {
+        if (!ws) return fail(SA_E_WORKSPACE, "project: workspace of %zu bytes required", off);
+        if (ws_bytes < off)
+            return fail(SA_E_WORKSPACE, "project: workspace %zu bytes < required %zu", ws_bytes, off);
+        if (!aligned(ws, 256)) return fail(SA_E_ALIGN, "project: workspace must be 256-byte aligned");
+    }
+    // dependency levels: a layer whose in_ch_mask is an earlier layer's mask runs after it
+    std::vector<int> level(n_layers, 0);
+    int max_level = 0;
+    for (int i = 0; i < n_layers; ++i) {
+        for (int j = 0; j < i; ++j)
+            if (layers[i].in_ch_mask && (const void *)layers[i].in_ch_mask == (const void *)layers[j].mask)
+                level[i] = std::max(level[i], level[j] + 1);
+        max_level = std::max(max_level, level[i]);
+    }
+
+    for (int lv = 0; lv <= max_level; ++lv) {
+        std::vector<int> ids;
+        for (int i = 0; i < n_layers; ++i)
+            if (level[i] == lv) ids.push_back(i);
+
+        // allowed bytes for layers with a channel support
+        for (int i : ids) {
+            const sa_project_desc &d = layers[i];
+            if (!d.in_ch_mask) continue;
+            const LayerPlan &p = plan[i];
+            int64_t total = (int64_t)d.groups * p.K;
+            int blocks = (int)std::min<int64_t>(1024, (total + 255) / 256);
+            hipLaunchKernelGGL(k_expand_allowed, dim3(blocks), dim3(256), 0, stream, d.in_ch_mask,
+                               ws_at<uint8_t>(ws, p.off_allowed), d.groups, (int)d.B, p.CD, p.K);
+            if (int rc = launch_check("k_expand_allowed")) return rc;
+        }
+
+        auto fill_row = [&](int i, RowLayer &R) {
+            const sa_project_desc &d = layers[i];
+            const LayerPlan &p = plan[i];
+            R.W = d.W;
+            R.U = d.U;
+            R.Z = d.Z;
+            R.G = d.G;
+            R.rowkeep = d.kind == SA_FILTER ? d.mask : nullptr;
+            if (d.kind == SA_FILTER)
+                R.colkeep = d.in_ch_mask ? ws_at<uint8_t>(ws, p.off_allowed) : nullptr;
+            else
+                R.colkeep = ws_at<uint8_t>(ws, p.off_colkeep);
+            R.allowed = d.in_ch_mask ? ws_at<uint8_t>(ws, p.off_allowed) : nullptr;
+            R.scores = d.scores ? d.scores : (p.off_scores != SIZE_MAX ? ws_at<double>(ws, p.off_scores) : nullptr);
+            R.A = (int)d.A;
+            R.K = p.K;
+            R.Ag = p.Ag;
+            R.rpb = p.rpb;
+            R.vec = p.vec;
+            R.rho = d.rho;
+        };
+
+        // filter scores
+        {
+            std::vector<int> f;
+            for (int i : ids)
+                if (layers[i].kind == SA_FILTER) f.push_back(i);
+            for (size_t s = 0; s < f.size(); s += kTab) {
+                RowTab tab;
+                memset(&tab, 0, sizeof tab);
+                int blocks = 0;
+                tab.nl = (int)std::min<size_t>(kTab, f.size() - s);
+                for (int t = 0; t < tab.nl; ++t) {
+                    fill_row(f[s + t], tab.L[t]);
+                    tab.begin[t] = blocks;
+                    blocks += (tab.L[t].A + tab.L[t].rpb - 1) / tab.L[t].rpb;
+                }
+                tab.begin[tab.nl] = blocks;
+                hipLaunchKernelGGL(k_row_scores, dim3(blocks), dim3(kRowThreads), 0, stream, tab);
+                if (int rc = launch_check("k_row_scores")) return rc;
+            }
+        }
+        // channel / shape column partials
+        {
+            std::vector<int> c;
+            for (int i : ids)
+                if (layers[i].kind == SA_CHANNEL || layers[i].kind == SA_SHAPE) c.push_back(i);
+            for (size_t s = 0; s < c.size(); s += kTab) {
+                ColTab tab;
+                memset(&tab, 0, sizeof tab);
+                int blocks = 0;
+                tab.nl = (int)std::min<size_t>(kTab, c.size() - s);
+                for (int t = 0; t < tab.nl; ++t) {
+                    const sa_project_desc &d = layers[c[s + t]];
+                    const LayerPlan &p = plan[c[s + t]];
+                    ColLayer &L = tab.L[t];
+                    L.W = d.W;
+                    L.U = d.U;
+                    L.allowed = d.in_ch_mask ? ws_at<uint8_t>(ws, p.off_allowed) : nullptr;
+                    L.partials = ws_at<double>(ws, p.off_partials);
+                    L.A = (int)d.A;
+                    L.K = p.K;
+                    L.Ag = p.Ag;
+                    L.nbands = p.nbands;
+                    L.ctiles = p.ctiles;
+                    L.vec = p.vec;
+                    tab.begin[t] = blocks;
+                    blocks += p.nbands * p.ctiles;
+                }
+                tab.begin[tab.nl] = blocks;
+                hipLaunchKernelGGL(k_col_partials, dim3(blocks), dim3(kColThreads), 0, stream, tab);
+                if (int rc = launch_check("k_col_partials")) return rc;
+            }
+        }
+        // selection for every structured layer
+        {
+            std::vector<int> sl;
+            for (int i : ids)
+                if (layers[i].kind != SA_ELEMENT) sl.push_back(i);
+            for (size_t s = 0; s < sl.size(); s += kTab) {
+                SelTab tab;
+                memset(&tab, 0, sizeof tab);
+                tab.nl = (int)std::min<size_t>(kTab, sl.size() - s);
+                for (int t = 0; t < tab.nl; ++t) {
+                    const sa_project_desc &d = layers[sl[s + t]];
+                    const LayerPlan &p = plan[sl[s + t]];
+                    SelLayer &L = tab.L[t];
+                    L.partials = p.off_partials != SIZE_MAX ? ws_at<double>(ws, p.off_partials) : nullptr;
+                    L.scores = d.scores ? d.scores : ws_at<double>(ws, p.off_scores);
+                    L.mask = d.mask;
+                    L.kept_idx = d.kept_idx;
+                    L.colkeep = p.off_colkeep != SIZE_MAX ? ws_at<uint8_t>(ws, p.off_colkeep) : nullptr;
+                    L.allowed = d.in_ch_mask ? ws_at<uint8_t>(ws, p.off_allowed) : nullptr;
+                    L.kind = d.kind;
+                    L.G = (int)p.G;
+                    L.k = (int)d.k;
+                    L.K = p.K;
+                    L.CD = p.CD;
+                    L.nbands = p.nbands;
+                    L.groups = d.groups;
+                }
+                hipLaunchKernelGGL(k_select, dim3(tab.nl), dim3(kSelThreads), 0, stream, tab);
+                if (int rc = launch_check("k_select")) return rc;
+            }
+        }
+        // element-wise layers
+        for (int i : ids) {
+            const sa_project_desc &d = layers[i];
+            if (d.kind != SA_ELEMENT) continue;
+            const LayerPlan &p = plan[i];
+            ElemArgs a;
+            memset(&a, 0, sizeof a);
+            a.W = d.W;
+            a.U = d.U;
+            a.Z = d.Z;
+            a.G = d.G;
+            a.mask = d.mask;
+            a.kept_idx = d.kept_idx;
+            a.scores = d.scores;
+            a.allowed = d.in_ch_mask ? ws_at<uint8_t>(ws, p.off_allowed) : nullptr;
+            char *eb = ws_at<char>(ws, p.off_elem);
+            a.hist = reinterpret_cast<uint32_t *>(eb);
+            a.state = reinterpret_cast<ElemState *>(eb + sizeof(uint32_t) * 3 * 2048);
+            a.chunk_counts = reinterpret_cast<uint32_t *>(eb + sizeof(uint32_t) * 3 * 2048 + 256);
+            a.chunk_prefix = a.chunk_counts + 2 * (size_t)p.nchunks;
+            a.divK = make_fastdiv((uint32_t)p.K);
+            a.n = (int32_t)(d.A * d.B * d.C * d.D);
+            a.K = p.K;
+            a.Ag = p.Ag;
+            a.k = (int32_t)d.k;
+            a.nchunks = p.nchunks;
+            a.vec = 1;  // n is a multiple of 4 only sometimes; elem_load8 checks the tail
+            a.rho = d.rho;
+            hipLaunchKernelGGL(k_elem_init, dim3((3 * 2048 + 255) / 256), dim3(256), 0, stream, a);
+            if (int rc = launch_check("k_elem_init")) return rc;
+            if (d.k > 0) {
+                const int hb = std::min(p.nchunks, kElemHistBlocks);
+                for (int pass = 0; pass < 3; ++pass) {
+                    hipLaunchKernelGGL(k_elem_hist, dim3(hb), dim3(kElemThreads), 0, stream, a, pass);
+                    if (int rc = launch_check("k_elem_hist")) return rc;
+                    hipLaunchKernelGGL(k_elem_find, dim3(1), dim3(kWave), 0, stream, a, pass);
+                    if (int rc = launch_check("k_elem_find")) return rc;
+                }
+            }
+            hipLaunchKernelGGL(k_elem_count, dim3(p.nchunks), dim3(kElemThreads), 0, stream, a);
+            if (int rc = launch_check("k_elem_count")) return rc;
+            hipLaunchKernelGGL(k_elem_scan, dim3(1), dim3(1024), 0, stream, a);
+            if (int rc = launch_check("k_elem_scan")) return rc;
+            hipLaunchKernelGGL(k_elem_apply, dim3(p.nchunks), dim3(kElemThreads), 0, stream, a);
+            if (int rc = launch_check("k_elem_apply")) return rc;
+        }
+        // apply for every structured layer
+        {
+            std::vector<int> sl;
+            for (int i : ids)
+                if (layers[i].kind != SA_ELEMENT) sl.push_back(i);
+            for (size_t s = 0; s < sl.size(); s += kTab) {
+                RowTab tab;
+                memset(&tab, 0, sizeof tab);
+                int blocks = 0;
+                tab.nl = (int)std::min<size_t>(kTab, sl.size() - s);
+                for (int t = 0; t < tab.nl; ++t) {
+                    fill_row(sl[s + t], tab.L[t]);
+                    tab.begin[t] = blocks;
+                    blocks += (tab.L[t].A + tab.L[t].rpb - 1) / tab.L[t].rpb;
+                }
+                tab.begin[tab.nl] = blocks;
+                hipLaunchKernelGGL(k_apply, dim3(blocks), dim3(kRowThreads), 0, stream, tab);
+                if (int rc = launch_check("k_apply")) return rc;
+            }
+        }
+    }
+    return SA_OK;
+}
+
+extern "C" int structadmm_dual_update(const sa_dual_desc *layers, int n_layers, hipStream_t stream) {
+    clear_error();
+    if (!layers || n_layers <= 0) return fail(SA_E_ARG, "dual_update: layers must be a non-empty array");
+    for (int i = 0; i < n_layers; ++i)
+        if (int rc = validate_dual(layers[i], i)) return rc;
+    for (int s = 0; s < n_layers; s += kTab) {
+        DualTab tab;
+        memset(&tab, 0, sizeof tab);
+        tab.nl = std::min(kTab, n_layers - s);
+        int blocks = 0;
+        for (int t = 0; t < tab.nl; ++t) {
+            const sa_dual_desc &d = layers[s + t];
+            DualLayer &L = tab.L[t];
+            L.W = d.W;
+            L.Z = d.Z;
+            L.U = d.U;
+            L.G = d.G;
+            L.n = (int32_t)d.n;
+            L.update = d.update_dual ? 1 : 0;
+            L.rho = d.rho;
+            tab.begin[t] = blocks;
+            blocks += (int)std::max<int64_t>(1, (d.n + kDualChunk - 1) / kDualChunk);
+        }
+        tab.begin[tab.nl] = blocks;
+        hipLaunchKernelGGL(k_dual, dim3(blocks), dim3(kDualThreads), 0, stream, tab);
+        if (int rc = launch_check("k_dual")) return rc;
+    }
+    return SA_OK;
+}

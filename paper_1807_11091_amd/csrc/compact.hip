@@ -1,0 +1,311 @@
+// gfx950 kernels and entry points that lay data out for the compacted CONV:
+//   structadmm_compact    the dense GEMM matrix left after row (filter) and
+//                         column (channel / filter-shape) pruning (Section 3,
+//                         "Combination of structured sparsities"), in bfloat16
+//   structadmm_pack_nhwc  binary32 NCHW activations -> bfloat16 NHWC, with an
+//                         optional channel gather (the input a compacted
+//                         predecessor layer would emit)
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdint>
+#include <cstring>
+
+#include "sa_device.h"
+#include "sa_host.h"
+#include "structadmm.h"
+
+namespace sa {
+namespace {
+
+constexpr int kCompThreads = 1024;
+
+struct CompArgs {
+    const float *Z;
+    const uint8_t *row_mask, *col_mask, *chan_mask, *in_ch_mask;
+    uint16_t *Wc;
+    int32_t *row_idx, *col_ch, *col_tap;
+    int32_t *counts;  // ws: [groups][4] = M, K, run, run_base
+    int32_t A, B, C, D, groups, in_compacted;
+};
+
+// Is column candidate (tap t, channel b) of conv group gc kept?
+__device__ inline bool col_kept(const CompArgs &a, int gc, int t, int b) {
+    const int taps = a.C * a.D;
+    if (a.col_mask && !a.col_mask[b * taps + t]) return false;
+    if (a.chan_mask && !a.chan_mask[b]) return false;
+    if (a.in_ch_mask && !a.in_ch_mask[gc * a.B + b]) return false;
+    return true;
+}
+
+// Input-channel position of full channel `full` (compacted input: rank among set in_ch_mask).
+__device__ inline int in_position(const CompArgs &a, int full) {
+    if (!a.in_compacted) return full;
+    int pos = 0;
+    for (int q = 0; q < full; ++q) pos += a.in_ch_mask[q] != 0;
+    return pos;
+}
+
+// Per conv group: M (kept rows), K (kept columns) and, when every tap keeps
+// the same channels and their input positions are consecutive, the channel run.
+__global__ __launch_bounds__(kCompThreads) void k_compact_count(CompArgs a) {
+    __shared__ uint32_t tmp[kCompThreads / kWave + 1];
+    __shared__ int s_first, s_last;
+    const int gc = blockIdx.x;
+    const int Ag = a.A / a.groups, taps = a.C * a.D;
+    uint32_t m = 0, kc = 0, nb = 0;
+    for (int r = threadIdx.x; r < Ag; r += kCompThreads) m += (!a.row_mask || a.row_mask[gc * Ag + r]) ? 1 : 0;
+    for (int64_t i = threadIdx.x; i < (int64_t)taps * a.B; i += kCompThreads) {
+        int t = (int)(i / a.B), b = (int)(i - (int64_t)t * a.B);
+        kc += col_kept(a, gc, t, b) ? 1 : 0;
+    }
+    if (threadIdx.x == 0) {
+        s_first = -1;
+        s_last = -1;
+    }
+    __syncthreads();
+    // kept channels ignoring the shape mask (defines the run when there is no shape mask)
+    for (int b = threadIdx.x; b < a.B; b += kCompThreads) {
+        bool keep = (!a.chan_mask || a.chan_mask[b]) && (!a.in_ch_mask || a.in_ch_mask[gc * a.B + b]);
+        nb += keep ? 1 : 0;
+        if (keep) {
+            atomicMin(reinterpret_cast<unsigned *>(&s_first), (unsigned)b);  // -1 is the largest unsigned
+            atomicMax(&s_last, b);
+        }
+    }
+    uint32_t tot_m, tot_k, tot_b;
+    block_excl_scan(m, tmp, &tot_m);
+    block_excl_scan(kc, tmp, &tot_k);
+    block_excl_scan(nb, tmp, &tot_b);
+    if (threadIdx.x == 0) {
+        int run = 0, base = 0;
+        if (!a.col_mask && tot_b > 0) {
+            int p0 = in_position(a, gc * a.B + s_first);
+            int p1 = in_position(a, gc * a.B + s_last);
+            if (p1 - p0 + 1 == (int)tot_b) {
+                run = (int)tot_b;
+                base = p0;
+            }
+        }
+        a.counts[4 * gc + 0] = (int)tot_m;
+        a.counts[4 * gc + 1] = (int)tot_k;
+        a.counts[4 * gc + 2] = run;
+        a.counts[4 * gc + 3] = base;
+    }
+}
+
+// Column tables (full input channel for now) and kept rows, concatenated over groups.
+__global__ __launch_bounds__(kCompThreads) void k_compact_tables(CompArgs a) {
+    __shared__ uint32_t tmp[kCompThreads / kWave + 1];
+    const int gc = blockIdx.x;
+    const int Ag = a.A / a.groups, taps = a.C * a.D;
+    int row_off = 0, col_off = 0;
+    for (int g = 0; g < gc; ++g) {
+        row_off += a.counts[4 * g + 0];
+        col_off += a.counts[4 * g + 1];
+    }
+    uint32_t running = 0;
+    const int64_t ncand = (int64_t)taps * a.B;
+    for (int64_t base = 0; base < ncand; base += kCompThreads) {
+        int64_t i = base + threadIdx.x;
+        bool keep = false;
+        int t = 0, b = 0;
+        if (i < ncand) {
+            t = (int)(i / a.B);
+            b = (int)(i - (int64_t)t * a.B);
+            keep = col_kept(a, gc, t, b);
+        }
+        uint32_t tot;
+        uint32_t pos = running + block_excl_scan(keep ? 1u : 0u, tmp, &tot);
+        if (keep) {
+            a.col_ch[col_off + pos] = gc * a.B + b;
+            a.col_tap[col_off + pos] = t;
+        }
+        running += tot;
+    }
+    running = 0;
+    for (int base = 0; base < Ag; base += kCompThreads) {
+        int r = base + threadIdx.x;
+        bool keep = r < Ag && (!a.row_mask || a.row_mask[gc * Ag + r]);
+        uint32_t tot;
+        uint32_t pos = running + block_excl_scan(keep ? 1u : 0u, tmp, &tot);
+        if (keep) a.row_idx[row_off + pos] = gc * Ag + r;
+        running += tot;
+    }
+}
+
+// Wc rows: block (m, gc) writes row m of group gc: bf16(Z[a, b, c, d]) per column, 0 padding.
+__global__ __launch_bounds__(256) void k_compact_gather(CompArgs a) {
+    const int m = blockIdx.x, gc = blockIdx.y;
+    const int M = a.counts[4 * gc + 0];
+    if (m >= M) return;
+    const int K = a.counts[4 * gc + 1];
+    const int ldk = (K + 7) / 8 * 8;
+    int64_t wc_off = 0;
+    int row_off = 0, col_off = 0;
+    for (int g = 0; g < gc; ++g) {
+        const int Mg = a.counts[4 * g + 0], Kg = a.counts[4 * g + 1];
+        wc_off += (int64_t)Mg * ((Kg + 7) / 8 * 8);
+        row_off += Mg;
+        col_off += Kg;
+    }
+    const int row = a.row_idx[row_off + m];
+    uint16_t *dst = a.Wc + wc_off + (int64_t)m * ldk;
+    for (int j = threadIdx.x; j < ldk; j += blockDim.x) {
+        uint16_t v = 0;
+        if (j < K) {
+            const int b = a.col_ch[col_off + j] - gc * a.B;
+            const int t = a.col_tap[col_off + j];
+            const int c = t / a.D, d = t - (t / a.D) * a.D;
+            v = f32_to_bf16_bits(a.Z[(((int64_t)row * a.B + b) * a.C + c) * a.D + d]);
+        }
+        dst[j] = v;
+    }
+}
+
+// Full input channel -> position in the channel-compacted input.
+__global__ __launch_bounds__(kCompThreads) void k_compact_inpos(CompArgs a, int total_cols) {
+    extern __shared__ int32_t pos[];  // [groups*B]
+    __shared__ uint32_t tmp[kCompThreads / kWave + 1];
+    const int nch = a.groups * a.B;
+    uint32_t running = 0;
+    for (int base = 0; base < nch; base += kCompThreads) {
+        int c = base + threadIdx.x;
+        uint32_t f = (c < nch && a.in_ch_mask[c]) ? 1u : 0u;
+        uint32_t tot;
+        uint32_t p = running + block_excl_scan(f, tmp, &tot);
+        if (c < nch) pos[c] = (int32_t)p;
+        running += tot;
+    }
+    __syncthreads();
+    for (int j = threadIdx.x; j < total_cols; j += kCompThreads) {
+        const int full = a.col_ch[j];
+        a.col_ch[j] = (full >= 0 && full < nch) ? pos[full] : 0;
+    }
+}
+
+// ---------------------------------------------------------------- pack
+constexpr int kPackTile = 64;
+
+// X binary32 NCHW -> Xp bfloat16 NHWC with kept channels in ascending order.
+// Workgroup = 64 channels x 64 pixels of one image, transposed through LDS.
+__global__ __launch_bounds__(256) void k_pack_nhwc(const float *__restrict__ X, const uint8_t *__restrict__ keep,
+                                                   uint16_t *__restrict__ Xp, int Cin, int HW, int Cx) {
+    __shared__ uint16_t tile[kPackTile][kPackTile + 2];
+    __shared__ int32_t cpos[kPackTile];
+    __shared__ int32_t s_base;
+    const int p0 = blockIdx.x * kPackTile, c0 = blockIdx.y * kPackTile, n = blockIdx.z;
+    const int tid = threadIdx.x;
+    if (tid < kWave) {
+        // position of channel c0 among kept channels, then ranks inside the tile
+        uint32_t cnt = 0;
+        if (keep)
+            for (int c = tid; c < c0; c += kWave) cnt += keep[c] != 0;
+        else
+            cnt = (tid == 0) ? (uint32_t)c0 : 0u;
+        cnt = wave_sum_u32(cnt);
+        const int c = c0 + tid;
+        uint32_t f = (c < Cin && (!keep || keep[c])) ? 1u : 0u;
+        uint32_t incl = wave_incl_scan(f);
+        cpos[tid] = f ? (int32_t)(cnt + incl - 1) : -1;
+        if (tid == 0) s_base = (int32_t)cnt;
+    }
+    for (int i = tid; i < kPackTile * kPackTile; i += 256) {
+        const int cl = i / kPackTile, pl = i % kPackTile;
+        const int c = c0 + cl, p = p0 + pl;
+        float v = (c < Cin && p < HW) ? X[((int64_t)n * Cin + c) * HW + p] : 0.0f;
+        tile[cl][pl] = f32_to_bf16_bits(v);
+    }
+    __syncthreads();
+    for (int i = tid; i < kPackTile * kPackTile; i += 256) {
+        const int pl = i / kPackTile, cl = i % kPackTile;
+        const int p = p0 + pl;
+        const int cp = cpos[cl];
+        if (p < HW && cp >= 0 && cp < Cx) Xp[((int64_t)n * HW + p) * Cx + cp] = tile[cl][pl];
+    }
+}
+
+}  // namespace
+}  // namespace sa
+
+using namespace sa;
+
+extern "C" int structadmm_compact(const sa_compact_desc *desc, sa_compact_sizes *sizes, hipStream_t stream) {
+    clear_error();
+    if (!desc || !sizes) return fail(SA_E_ARG, "compact: desc and sizes are required");
+    const sa_compact_desc &d = *desc;
+    if (int rc = validate_compact(d)) return rc;
+    if (d.in_compacted && (int64_t)d.groups * d.B > 16384)
+        return fail(SA_E_UNSUPPORTED, "compact: in_compacted supports at most 16384 input channels");
+    CompArgs a;
+    memset(&a, 0, sizeof a);
+    a.Z = d.Z;
+    a.row_mask = d.row_mask;
+    a.col_mask = d.col_mask;
+    a.chan_mask = d.chan_mask;
+    a.in_ch_mask = d.in_ch_mask;
+    a.Wc = d.Wc;
+    a.row_idx = d.row_idx;
+    a.col_ch = d.col_ch;
+    a.col_tap = d.col_tap;
+    a.counts = static_cast<int32_t *>(d.ws);
+    a.A = (int)d.A;
+    a.B = (int)d.B;
+    a.C = (int)d.C;
+    a.D = (int)d.D;
+    a.groups = d.groups;
+    a.in_compacted = d.in_compacted ? 1 : 0;
+    const int Ag = a.A / a.groups;
+    hipLaunchKernelGGL(k_compact_count, dim3(d.groups), dim3(kCompThreads), 0, stream, a);
+    if (int rc = check_hip(hipGetLastError(), "k_compact_count")) return rc;
+    hipLaunchKernelGGL(k_compact_tables, dim3(d.groups), dim3(kCompThreads), 0, stream, a);
+    if (int rc = check_hip(hipGetLastError(), "k_compact_tables")) return rc;
+    hipLaunchKernelGGL(k_compact_gather, dim3(Ag, d.groups), dim3(256), 0, stream, a);
+    if (int rc = check_hip(hipGetLastError(), "k_compact_gather")) return rc;
+    int32_t counts[4 * SA_MAX_CONV_GROUPS];
+    if (int rc = check_hip(hipMemcpyAsync(counts, d.ws, sizeof(int32_t) * 4 * d.groups, hipMemcpyDeviceToHost, stream),
+                           "compact: copy sizes"))
+        return rc;
+    if (int rc = check_hip(hipStreamSynchronize(stream), "compact: synchronize")) return rc;
+    int total_cols = 0;
+    for (int g = 0; g < d.groups; ++g) total_cols += counts[4 * g + 1];
+    if (d.in_compacted && total_cols > 0) {
+        size_t lds = sizeof(int32_t) * (size_t)d.groups * d.B;
+        hipLaunchKernelGGL(k_compact_inpos, dim3(1), dim3(kCompThreads), lds, stream, a, total_cols);
+        if (int rc = check_hip(hipGetLastError(), "k_compact_inpos")) return rc;
+        if (int rc = check_hip(hipStreamSynchronize(stream), "compact: synchronize")) return rc;
+    }
+    memset(sizes, 0, sizeof *sizes);
+    sizes->groups = d.groups;
+    int64_t wc_off = 0;
+    int32_t row_off = 0, col_off = 0;
+    for (int g = 0; g < d.groups; ++g) {
+        sizes->M[g] = counts[4 * g + 0];
+        sizes->K[g] = counts[4 * g + 1];
+        sizes->ldk[g] = (sizes->K[g] + 7) / 8 * 8;
+        sizes->run[g] = counts[4 * g + 2];
+        sizes->run_base[g] = counts[4 * g + 3];
+        sizes->wc_offset[g] = wc_off;
+        sizes->row_offset[g] = row_off;
+        sizes->col_offset[g] = col_off;
+        wc_off += (int64_t)sizes->M[g] * sizes->ldk[g];
+        row_off += sizes->M[g];
+        col_off += sizes->K[g];
+    }
+    return SA_OK;
+}
+
+extern "C" int structadmm_pack_nhwc(const float *X, int32_t N, int32_t Cin, int32_t H, int32_t W,
+                                    const uint8_t *keep, int32_t Cx, uint16_t *Xp, hipStream_t stream) {
+    clear_error();
+    if (!X || !Xp) return fail(SA_E_ARG, "pack: X and Xp are required");
+    if (N <= 0 || Cin <= 0 || H <= 0 || W <= 0 || Cx <= 0 || Cx > Cin)
+        return fail(SA_E_ARG, "pack: sizes must be positive and Cx <= Cin");
+    if (!keep && Cx != Cin) return fail(SA_E_ARG, "pack: Cx must equal Cin without a keep mask");
+    if ((int64_t)H * W > (int64_t(1) << 30) || (int64_t)Cin > 65535 || (int64_t)N > 65535)
+        return fail(SA_E_UNSUPPORTED, "pack: tensor too large");
+    const int HW = H * W;
+    dim3 grid((HW + kPackTile - 1) / kPackTile, (Cin + kPackTile - 1) / kPackTile, N);
+    hipLaunchKernelGGL(k_pack_nhwc, grid, dim3(256), 0, stream, X, keep, Xp, Cin, HW, Cx);
+    return check_hip(hipGetLastError(), "k_pack_nhwc");
+}

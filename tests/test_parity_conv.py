@@ -1,0 +1,252 @@
+"""GPU parity of structadmm_compact, structadmm_pack_nhwc and
+structadmm_conv_fwd against the oracle.
+
+Bar: compacted matrix, row / column tables and packed input bit-exact; CONV
+output (bf16, fp32 MFMA accumulation) within max|dY| / RMS(Y_ref) <= 2e-2 of
+the oracle's binary64 CONV over the same bf16 operands.  Small cases span
+several tiles with ragged tails in every dimension; workload cases run the
+benchmark's launch configuration at full batch and compare sampled images.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import paper_1807_11091_amd as sa
+from gpu_helpers import (DEV, GpuLayer, bf16_bits_to_f64, bitwise_equal, maxabs_over_rms, run_project,
+                         to_dev, torch)
+from workloads import WORKLOADS, input_nchw, layer_tensors
+
+pytestmark = pytest.mark.gpu
+
+TOL = 2e-2
+
+
+def strip_padding(Wc, sizes):
+    out = []
+    for g in range(sizes.groups):
+        M, K, ldk, off = sizes.M[g], sizes.K[g], sizes.ldk[g], sizes.wc_offset[g]
+        out.append(Wc[off: off + M * ldk].reshape(M, ldk)[:, :K].ravel())
+    return np.concatenate(out) if out else np.zeros(0, np.uint16)
+
+
+def gpu_compact(Z, groups, row_mask=None, col_mask=None, in_ch_mask=None, in_compacted=False):
+    t = torch()
+    Wc, row_idx, col_ch, col_tap, sizes = sa.compact(Z, groups, row_mask=row_mask, col_mask=col_mask,
+                                                     in_ch_mask=in_ch_mask, in_compacted=in_compacted)
+    t.cuda.synchronize()
+    return Wc, row_idx, col_ch, col_tap, sizes
+
+
+def check_compact(gpu, ref):
+    Wc, row_idx, col_ch, col_tap, sizes = gpu
+    assert list(sizes.M)[: sizes.groups] == list(ref["M"])
+    assert list(sizes.K)[: sizes.groups] == list(ref["K"])
+    nr, nc = int(ref["M"].sum()), int(ref["K"].sum())
+    assert np.array_equal(strip_padding(Wc.cpu().numpy(), sizes), ref["Wc"])
+    assert np.array_equal(row_idx.cpu().numpy()[:nr], ref["row_idx"])
+    assert np.array_equal(col_ch.cpu().numpy()[:nc], ref["col_ch"])
+    assert np.array_equal(col_tap.cpu().numpy()[:nc], ref["col_tap"])
+    # padding columns hold +0
+    full = Wc.cpu().numpy()
+    for g in range(sizes.groups):
+        M, K, ldk, off = sizes.M[g], sizes.K[g], sizes.ldk[g], sizes.wc_offset[g]
+        assert not np.any(full[off: off + M * ldk].reshape(M, ldk)[:, K:])
+
+
+def conv_case(N, Cin, H, Wd, A, C, D, stride, pad, groups, kind, keep, seed, dense_too=True):
+    rng = np.random.default_rng(seed)
+    B = Cin // groups
+    shape = (A, B, C, D)
+    W = (0.05 * rng.standard_normal(shape)).astype(np.float32)
+    U = (0.01 * rng.standard_normal(shape)).astype(np.float32)
+    G = {sa.FILTER: A, sa.CHANNEL: B, sa.SHAPE: B * C * D}[kind]
+    k = max(1, int(round(keep * G)))
+    # projection on both sides (bit-exact parity is checked elsewhere; here it feeds compaction)
+    ref = oracle.project(W, U, kind, k, groups)
+    L = GpuLayer(W, U, kind, k, groups)
+    got = run_project([L])[0]
+    assert np.array_equal(got["mask"], ref["mask"]) and bitwise_equal(got["Z"], ref["Z"])
+    rows = L.mask if kind == sa.FILTER else None
+    cols = L.mask if kind == sa.SHAPE else None
+    ch = L.mask if kind == sa.CHANNEL else None
+    Wc, row_idx, col_ch, col_tap, sizes = sa.compact(L.Z, groups, row_mask=rows, col_mask=cols, chan_mask=ch)
+    r_rows = ref["mask"] if kind == sa.FILTER else None
+    r_cols = ref["mask"] if kind == sa.SHAPE else None
+    r_ch = ref["mask"] if kind == sa.CHANNEL else None
+    rc = oracle.compact(ref["Z"], groups, row_mask=r_rows, col_mask=r_cols, chan_mask=r_ch)
+    check_compact((Wc, row_idx, col_ch, col_tap, sizes), rc)
+    X = rng.standard_normal((N, Cin, H, Wd)).astype(np.float32)
+    dX = to_dev(X)
+    Xp = sa.pack_nhwc(dX)
+    Xb = oracle.pack(X)
+    assert bitwise_equal(Xp.cpu().numpy(), Xb.transpose(0, 2, 3, 1))
+    Y = sa.conv_fwd(Xp, Wc, col_ch, col_tap, sizes, C, D, stride, pad)
+    Yr = oracle.conv(Xb, rc, C, D, stride, pad)
+    y = bf16_bits_to_f64(Y.cpu().numpy())
+    assert y.shape == Yr.shape
+    err = maxabs_over_rms(y, Yr)
+    assert err <= TOL, err
+    if dense_too:
+        Wd_, ri, cc, ct, sd = sa.compact(L.Z, groups)
+        Yd = sa.conv_fwd(Xp, Wd_, cc, ct, sd, C, D, stride, pad)
+        rd = oracle.compact(ref["Z"], groups)
+        Ydr = oracle.conv(Xb, rd, C, D, stride, pad)
+        yd = bf16_bits_to_f64(Yd.cpu().numpy())
+        kept = rc["row_idx"]
+        assert dense_masked_error(yd, Ydr, kept) <= TOL
+        # compacted and dense agree on the kept output channels
+        assert maxabs_over_rms(y, yd[..., kept]) <= TOL
+    return err
+
+
+def dense_masked_error(yd, ref, kept_rows):
+    """Dense CONV with masked weights: pruned output channels are exactly zero
+    on both sides; the kept ones are held to the tolerance (their RMS, not one
+    deflated by the zero channels, sets the scale)."""
+    A = ref.shape[-1]
+    pruned = np.setdiff1d(np.arange(A), kept_rows)
+    assert not np.any(ref[..., pruned]) and not np.any(yd[..., pruned])
+    return maxabs_over_rms(yd[..., kept_rows], ref[..., kept_rows])
+
+
+SMALL = [
+    # N, Cin, H,  W, A,  C, D, s, p, g, kind,        keep
+    (3, 16, 9, 9, 130, 3, 3, 1, 1, 1, sa.FILTER, 0.6),
+    (2, 32, 12, 11, 40, 3, 3, 1, 1, 1, sa.FILTER, 1.0),
+    (2, 24, 10, 10, 20, 3, 3, 2, 1, 1, sa.FILTER, 1.0),
+    (2, 3, 35, 35, 24, 11, 11, 4, 0, 1, sa.FILTER, 0.5),
+    (2, 32, 13, 13, 48, 3, 3, 1, 1, 2, sa.SHAPE, 0.3),
+    (2, 64, 7, 7, 96, 1, 1, 1, 0, 1, sa.FILTER, 0.6),
+    (2, 64, 14, 14, 64, 1, 1, 2, 0, 1, sa.CHANNEL, 0.5),
+    (1, 48, 8, 8, 300, 3, 3, 1, 1, 1, sa.SHAPE, 0.25),
+    (5, 8, 7, 9, 16, 3, 2, 1, 0, 1, sa.FILTER, 0.75),
+    (1, 256, 6, 6, 40, 3, 3, 1, 1, 2, sa.FILTER, 0.5),
+]
+
+
+@pytest.mark.parametrize("case", SMALL, ids=[f"c{i}" for i in range(len(SMALL))])
+def test_conv_small(case):
+    conv_case(*case, seed=hash(case) % 2**31)
+
+
+def test_compact_chain_input_positions():
+    """Channel-compacted input (the previous layer's kept filters): positions
+    in the compacted input, and the CONV over the gathered input."""
+    rng = np.random.default_rng(31)
+    groups, B, A, C, D = 2, 24, 32, 3, 3
+    W = (0.05 * rng.standard_normal((A, B, C, D))).astype(np.float32)
+    U = np.zeros_like(W)
+    prev = np.zeros(groups * B, np.uint8)
+    prev[rng.choice(groups * B, size=groups * B // 2, replace=False)] = 1
+    ref = oracle.project(W, U, sa.FILTER, 16, groups, in_ch_mask=prev)
+    L = GpuLayer(W, U, sa.FILTER, 16, groups, in_ch_mask=prev)
+    got = run_project([L])[0]
+    assert np.array_equal(got["mask"], ref["mask"])
+    dprev = L.in_ch_mask
+    gc = sa.compact(L.Z, groups, row_mask=L.mask, in_ch_mask=dprev, in_compacted=True)
+    rc = oracle.compact(ref["Z"], groups, row_mask=ref["mask"], in_ch_mask=prev, in_compacted=True)
+    check_compact(gc, rc)
+    X = rng.standard_normal((2, groups * B, 9, 9)).astype(np.float32)
+    Xp = sa.pack_nhwc(to_dev(X), keep=dprev)
+    Xb = oracle.pack(X, keep=prev)
+    assert bitwise_equal(Xp.cpu().numpy(), Xb.transpose(0, 2, 3, 1))
+    Wc, ri, cc, ct, sizes = gc
+    Y = sa.conv_fwd(Xp, Wc, cc, ct, sizes, C, D, 1, 1)
+    Yr = oracle.conv(Xb, rc, C, D, 1, 1)
+    assert maxabs_over_rms(bf16_bits_to_f64(Y.cpu().numpy()), Yr) <= TOL
+
+
+def sampled_images(N):
+    return sorted({0, N // 2, N - 1})
+
+
+def workload_conv(name, layer_ids=None, variant=0, chain=False):
+    """Full-batch GPU path of a workload (projection -> compaction -> pack ->
+    compacted and dense CONV); the oracle recomputes sampled images."""
+    t = torch()
+    wl = WORKLOADS[name]
+    kind, pct = wl.variants[variant]
+    ids = range(len(wl.layers)) if layer_ids is None else layer_ids
+    prev_gpu, prev_ref = None, None
+    worst = 0.0
+    for li in ids:
+        L = wl.layers[li]
+        W, U = layer_tensors(wl, li)
+        k = wl.k_for(li, kind, pct)
+        inm_gpu = prev_gpu if chain else None
+        inm_ref = prev_ref if chain else None
+        ref = oracle.project(W, U, kind, k, L.groups, in_ch_mask=inm_ref)
+        gl = GpuLayer(W, U, kind, k, L.groups, in_ch_mask=inm_gpu)
+        got = run_project([gl])[0]
+        assert np.array_equal(got["mask"], ref["mask"]) and bitwise_equal(got["Z"], ref["Z"])
+        rows = gl.mask if kind == sa.FILTER else None
+        cols = gl.mask if kind == sa.SHAPE else None
+        gc = sa.compact(gl.Z, L.groups, row_mask=rows, col_mask=cols, in_ch_mask=inm_gpu,
+                        in_compacted=inm_gpu is not None)
+        rc = oracle.compact(ref["Z"], L.groups, row_mask=ref["mask"] if kind == sa.FILTER else None,
+                            col_mask=ref["mask"] if kind == sa.SHAPE else None, in_ch_mask=inm_ref,
+                            in_compacted=inm_ref is not None)
+        check_compact(gc, rc)
+        X = input_nchw(wl, li)
+        dX = to_dev(X)
+        Xp = sa.pack_nhwc(dX, keep=inm_gpu)
+        Wc, ri, cc, ct, sizes = gc
+        Y = sa.conv_fwd(Xp, Wc, cc, ct, sizes, L.C, L.D, L.stride, L.pad)
+        Xf = sa.pack_nhwc(dX)
+        gd = sa.compact(gl.Z, L.groups)
+        Yd = sa.conv_fwd(Xf, gd[0], gd[2], gd[3], gd[4], L.C, L.D, L.stride, L.pad)
+        t.cuda.synchronize()
+        sel = sampled_images(wl.batch)
+        Xb = oracle.pack(X[sel], keep=inm_ref)
+        Yr = oracle.conv(Xb, rc, L.C, L.D, L.stride, L.pad)
+        y = bf16_bits_to_f64(Y.cpu().numpy()[sel])
+        err = maxabs_over_rms(y, Yr)
+        assert err <= TOL, ("compacted", name, li, err)
+        rd = oracle.compact(ref["Z"], L.groups)
+        Ydr = oracle.conv(oracle.pack(X[sel]), rd, L.C, L.D, L.stride, L.pad)
+        yd = bf16_bits_to_f64(Yd.cpu().numpy()[sel])
+        errd = dense_masked_error(yd, Ydr, rc["row_idx"])
+        assert errd <= TOL, ("dense", name, li, errd)
+        worst = max(worst, err, errd)
+        prev_gpu, prev_ref = gl.mask, ref["mask"]
+        del dX, Xp, Xf, Y, Yd
+    return worst
+
+
+def test_conv_workload_cifar():
+    workload_conv("cifar_conv64")
+
+
+def test_conv_workload_alexnet_shape30():
+    workload_conv("alexnet_shape30")
+
+
+def test_conv_workload_alexnet_chain():
+    workload_conv("alexnet_chain_f50c50", chain=True)
+
+
+def test_conv_workload_resnet50_sampled_layers():
+    wl = WORKLOADS["resnet50_filter60"]
+    names = {l.name: i for i, l in enumerate(wl.layers)}
+    pick = [names[n] for n in ("conv1", "layer1.0.conv1", "layer1.0.conv2", "layer2.0.conv2",
+                               "layer2.0.downsample", "layer3.3.conv2", "layer4.0.conv1",
+                               "layer4.2.conv2", "layer4.2.conv3")]
+    workload_conv("resnet50_filter60", pick)
+
+
+@pytest.mark.parametrize("variant", [0, 2, 3, 5, 6, 8])
+def test_conv_workload_sweep(variant):
+    workload_conv("resnet50_s3_sweep", variant=variant)
+
+
+def test_conv_is_deterministic():
+    t = torch()
+    rng = np.random.default_rng(4)
+    X = to_dev(rng.standard_normal((4, 64, 14, 14)).astype(np.float32))
+    Z = to_dev((0.05 * rng.standard_normal((96, 64, 3, 3))).astype(np.float32))
+    Wc, ri, cc, ct, sizes = sa.compact(Z, 1)
+    Xp = sa.pack_nhwc(X)
+    Y1 = sa.conv_fwd(Xp, Wc, cc, ct, sizes, 3, 3, 1, 1)
+    Y2 = sa.conv_fwd(Xp, Wc, cc, ct, sizes, 3, 3, 1, 1)
+    t.cuda.synchronize()
+    assert t.equal(Y1, Y2)

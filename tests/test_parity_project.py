@@ -1,0 +1,202 @@
+"""GPU parity of structadmm_project / structadmm_dual_update against the
+oracle on the same seeded inputs.
+
+Bar: masks and kept indices bit-exact; Z and U' bit-exact (both sides take
+the same binary32 operations); G within rel-L2 1e-5; scores (binary64 sums
+in a different order) within 1e-12 relative.  Structured inputs are drawn
+so that the k-th and (k+1)-th scores are apart by >= 1e-9 relative, far
+above the ~1e-13 difference between the two summation orders; exact ties
+are exercised separately with inputs whose sums are exact in binary64.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import paper_1807_11091_amd as sa
+from gpu_helpers import (GpuLayer, bitwise_equal, boundary_gap, n_groups, rel_l2, run_project,
+                         to_dev, torch)
+from workloads import WORKLOADS, layer_tensors
+
+pytestmark = pytest.mark.gpu
+
+KINDS = (sa.FILTER, sa.CHANNEL, sa.SHAPE, sa.ELEMENT)
+
+
+def check(got, ref, kind, k, fused, what=""):
+    assert np.array_equal(got["mask"], ref["mask"]), f"{what} mask"
+    assert np.array_equal(got["kept_idx"], ref["kept_idx"]), f"{what} kept_idx"
+    assert bitwise_equal(got["Z"], ref["Z"]), f"{what} Z"
+    if "scores" in got:
+        s, r = got["scores"], ref["scores"]
+        assert np.all(np.abs(s - r) <= 1e-12 * np.maximum(np.abs(r), 1e-300)), f"{what} scores"
+    if fused:
+        assert bitwise_equal(got["U"], ref["U"]), f"{what} U"
+        assert rel_l2(got["G"], ref["G"]) <= 1e-5, f"{what} G"
+
+
+def oracle_ref(W, U, kind, k, groups=1, in_ch_mask=None, rho=0.0, fused=False):
+    return oracle.project(W, U, kind, k, groups=groups, in_ch_mask=in_ch_mask, rho=rho, fused=fused)
+
+
+SMALL_SHAPES = [((16, 8, 3, 3), 1), ((24, 6, 5, 5), 2), ((12, 3, 11, 11), 1), ((70, 20, 1, 1), 1),
+                ((8, 3, 3, 3), 1), ((130, 33, 1, 3), 2), ((5, 7, 2, 2), 1)]
+
+
+@pytest.mark.parametrize("shape,groups", SMALL_SHAPES)
+@pytest.mark.parametrize("kind", KINDS)
+def test_project_small(shape, groups, kind):
+    rng = np.random.default_rng(abs(hash((shape, kind))) % 2**32)
+    W = (0.05 * rng.standard_normal(shape)).astype(np.float32)
+    U = (0.01 * rng.standard_normal(shape)).astype(np.float32)
+    G = n_groups(shape, kind)
+    for k in sorted({0, 1, G // 3, G // 2, G - 1, G}):
+        for fused in (False, True):
+            ref = oracle_ref(W, U, kind, k, groups, rho=1.5e-3, fused=fused)
+            if kind != sa.ELEMENT:
+                assert boundary_gap(ref["scores"], k) >= 1e-9
+            L = GpuLayer(W, U, kind, k, groups, rho=1.5e-3, fused=fused)
+            got = run_project([L])[0]
+            check(got, ref, kind, k, fused, f"{shape} k={k} fused={fused}")
+
+
+@pytest.mark.parametrize("kind", KINDS)
+def test_project_exact_ties(kind):
+    """Entries from {-1, -0.5, 0, 0.5, 1}: group sums are exact in binary64 on
+    both sides, so equal scores are equal bits and the lowest-index rule decides."""
+    rng = np.random.default_rng(77 + kind)
+    for shape in [(12, 4, 2, 2), (40, 6, 3, 3), (9, 5, 1, 1)]:
+        W = (rng.integers(-2, 3, size=shape) * 0.5).astype(np.float32)
+        U = np.zeros(shape, np.float32)
+        G = n_groups(shape, kind)
+        for k in sorted({1, G // 4, G // 2, G - 2}):
+            ref = oracle_ref(W, U, kind, k, rho=0.5, fused=True)
+            got = run_project([GpuLayer(W, U, kind, k, rho=0.5, fused=True)])[0]
+            check(got, ref, kind, k, True, f"ties {shape} k={k}")
+
+
+@pytest.mark.parametrize("kind", KINDS)
+def test_project_channel_support(kind):
+    rng = np.random.default_rng(5 + kind)
+    for shape, groups in [((32, 12, 3, 3), 2), ((20, 16, 1, 1), 1)]:
+        W = (0.05 * rng.standard_normal(shape)).astype(np.float32)
+        U = (0.01 * rng.standard_normal(shape)).astype(np.float32)
+        m = (rng.random(groups * shape[1]) < 0.5).astype(np.uint8)
+        G = n_groups(shape, kind)
+        for k in (1, G // 2, G):
+            ref = oracle_ref(W, U, kind, k, groups, in_ch_mask=m, rho=1e-3, fused=True)
+            got = run_project([GpuLayer(W, U, kind, k, groups, in_ch_mask=m, rho=1e-3, fused=True)])[0]
+            check(got, ref, kind, k, True, f"support {shape} k={k}")
+
+
+def test_project_mixed_multilayer_call():
+    rng = np.random.default_rng(123)
+    specs = [((64, 32, 3, 3), sa.FILTER, 20), ((48, 24, 3, 3), sa.CHANNEL, 7), ((32, 16, 3, 3), sa.SHAPE, 50),
+             ((16, 16, 3, 3), sa.ELEMENT, 1000), ((96, 3, 11, 11), sa.SHAPE, 109), ((64, 64, 1, 1), sa.FILTER, 38)]
+    specs = specs * 4  # 24 layers: more than one kernel-argument table
+    layers, refs = [], []
+    for i, (shape, kind, k) in enumerate(specs):
+        W = (0.05 * rng.standard_normal(shape)).astype(np.float32)
+        U = (0.01 * rng.standard_normal(shape)).astype(np.float32)
+        refs.append(oracle_ref(W, U, kind, k, rho=2e-3, fused=(i % 2 == 0)))
+        layers.append(GpuLayer(W, U, kind, k, rho=2e-3, fused=(i % 2 == 0)))
+    got = run_project(layers)
+    for i, (g, r) in enumerate(zip(got, refs)):
+        check(g, r, specs[i][1], specs[i][2], i % 2 == 0, f"layer {i}")
+
+
+def workload_layers(name, variant=0):
+    wl = WORKLOADS[name]
+    kind, pct = wl.variants[variant]
+    out = []
+    for li in range(len(wl.layers)):
+        W, U = layer_tensors(wl, li)
+        out.append((wl, li, W, U, kind, wl.k_for(li, kind, pct)))
+    return out
+
+
+@pytest.mark.parametrize("name", ["cifar_conv64", "alexnet_shape30", "resnet50_filter60"])
+def test_project_workload_one_call(name):
+    """All layers of a workload in one fused call, as the benchmark times it."""
+    layers, refs = [], []
+    for wl, li, W, U, kind, k in workload_layers(name):
+        L = wl.layers[li]
+        ref = oracle_ref(W, U, kind, k, L.groups, rho=wl.rho, fused=True)
+        assert boundary_gap(ref["scores"], k) >= 1e-9, f"{name} layer {li}: inputs not distinct"
+        refs.append(ref)
+        layers.append(GpuLayer(W, U, kind, k, L.groups, rho=wl.rho, fused=True))
+    got = run_project(layers)
+    for i, (g, r) in enumerate(zip(got, refs)):
+        check(g, r, layers[i].layer.kind, layers[i].k, True, f"{name} layer {i}")
+
+
+def test_project_alexnet_chain():
+    """Filter-wise 50% with each layer's input channels restricted to the
+    previous layer's kept filters, in one call (mask pointers chain the layers)."""
+    t = torch()
+    items = workload_layers("alexnet_chain_f50c50")
+    layers, refs = [], []
+    prev_gpu_mask, prev_ref_mask = None, None
+    for wl, li, W, U, kind, k in items:
+        L = wl.layers[li]
+        ref = oracle_ref(W, U, kind, k, L.groups, in_ch_mask=prev_ref_mask, rho=wl.rho, fused=True)
+        assert boundary_gap(ref["scores"], k) >= 1e-9
+        gl = GpuLayer(W, U, kind, k, L.groups, in_ch_mask=prev_gpu_mask, rho=wl.rho, fused=True)
+        layers.append(gl)
+        refs.append(ref)
+        prev_gpu_mask, prev_ref_mask = gl.mask, ref["mask"]
+    got = run_project(layers)
+    for i, (g, r) in enumerate(zip(got, refs)):
+        check(g, r, sa.FILTER, layers[i].k, True, f"chain layer {i}")
+        if i > 0:  # exactly the previous layer's kept channels carry weights
+            Z = g["Z"].reshape(g["Z"].shape[0], -1)
+            assert np.count_nonzero(Z) > 0
+
+
+@pytest.mark.parametrize("variant", range(9))
+def test_project_sweep_variants(variant):
+    (wl, li, W, U, kind, k), = workload_layers("resnet50_s3_sweep", variant)
+    ref = oracle_ref(W, U, kind, k, rho=wl.rho, fused=True)
+    if kind != sa.ELEMENT:
+        assert boundary_gap(ref["scores"], k) >= 1e-9
+    got = run_project([GpuLayer(W, U, kind, k, rho=wl.rho, fused=True)])[0]
+    check(got, ref, kind, k, True, f"sweep {variant}")
+
+
+def test_dual_update_parity():
+    t = torch()
+    rng = np.random.default_rng(9)
+    items, refs, devs = [], [], []
+    for n, upd, want_g in [(1000, True, True), (1001, True, True), (4099, False, True), (37, True, False),
+                           (3, True, True), (1 << 20, True, True)]:
+        W = rng.standard_normal(n).astype(np.float32)
+        Z = np.where(rng.random(n) < 0.5, W + 0.1, 0).astype(np.float32)
+        U = (0.1 * rng.standard_normal(n)).astype(np.float32)
+        Uo, Go = oracle.dual_update(W, Z, U, 0.25, update_dual=upd, want_grad=want_g)
+        dW, dZ, dU = to_dev(W), to_dev(Z), to_dev(U)
+        dG = t.full_like(dW, float("nan")) if want_g else None
+        items.append((dW, dZ, dU, 0.25, dG, upd))
+        refs.append((Uo, Go))
+        devs.append((dU, dG))
+    sa.dual_update(items)
+    t.cuda.synchronize()
+    for (dU, dG), (Uo, Go) in zip(devs, refs):
+        assert bitwise_equal(dU.cpu().numpy(), Uo)
+        if Go is not None:
+            g = dG.cpu().numpy()
+            assert rel_l2(g, Go) <= 1e-5
+            assert bitwise_equal(g, Go)
+
+
+def test_project_is_deterministic_across_streams():
+    t = torch()
+    items = workload_layers("alexnet_shape30")
+    outs = []
+    for rep in range(2):
+        s = t.cuda.Stream()
+        layers = [GpuLayer(W, U, kind, k, wl.layers[li].groups, rho=wl.rho, fused=True)
+                  for wl, li, W, U, kind, k in items]
+        with t.cuda.stream(s):
+            outs.append(run_project(layers, stream=s))
+    for a, b in zip(*outs):
+        for key in a:
+            assert bitwise_equal(a[key], b[key]), key
