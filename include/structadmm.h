@@ -150,8 +150,9 @@ int structadmm_dual_update(const sa_dual_desc *layers, int n_layers, hipStream_t
  *         nothing aside), in tap-major order: t ascending, then b ascending;
  *   entries: Wc[m][j] = Z[row m, column j] rounded to bfloat16 (nearest even).
  * Matrices are concatenated over conv groups, each row-major [M_g][ldk_g]
- * with ldk_g = K_g rounded up to a multiple of 8; the padding columns
- * j in [K_g, ldk_g) hold +0 (so every row starts 16-byte aligned).
+ * with ldk_g = K_g rounded up to a multiple of 64; the padding columns
+ * j in [K_g, ldk_g) hold +0 (rows start 128-byte aligned and the CONV reads
+ * whole 64-column slices without a bounds check).
  * Column tables: col_tap[j] = c*D + d, col_ch[j] = input channel of column j,
  * i.e. gc*B + b, or, when in_compacted is set, the position of channel
  * gc*B + b among the channels with in_ch_mask set (the input then holds only
@@ -169,7 +170,7 @@ typedef struct sa_compact_desc {
     const uint8_t *chan_mask;    /* [B] or NULL            */
     const uint8_t *in_ch_mask;   /* [groups*B] or NULL     */
     int32_t in_compacted;        /* requires in_ch_mask    */
-    uint16_t *Wc;                /* out, capacity A * roundup(B*C*D, 8) bfloat16 */
+    uint16_t *Wc;                /* out, capacity A * roundup(B*C*D, 64) bfloat16 */
     int32_t *row_idx;            /* out, capacity A                     */
     int32_t *col_ch;             /* out, capacity groups*B*C*D          */
     int32_t *col_tap;            /* out, capacity groups*B*C*D          */
@@ -191,6 +192,10 @@ typedef struct sa_compact_sizes {
      * channel block: filter / channel pruning); 0 for a general gather. */
     int32_t run[SA_MAX_CONV_GROUPS];
     int32_t run_base[SA_MAX_CONV_GROUPS];
+    /* Input channels the group's columns read lie in [ch_lo[gc], ch_lo[gc] + ch_span[gc])
+     * (ch_span = 0 when the group has no column). */
+    int32_t ch_lo[SA_MAX_CONV_GROUPS];
+    int32_t ch_span[SA_MAX_CONV_GROUPS];
 } sa_compact_sizes;
 
 int structadmm_compact(const sa_compact_desc *desc, sa_compact_sizes *sizes, hipStream_t stream);
@@ -211,7 +216,7 @@ int structadmm_pack_nhwc(const float *X, int32_t N, int32_t Cin, int32_t H, int3
  * (col_tap[j] / D, col_tap[j] % D); zero outside the image (cross-correlation,
  * no bias, no dilation).  bfloat16 inputs, binary32 accumulation on the
  * matrix cores, bfloat16 output (nearest even).
- * X: bfloat16 NHWC [N, H, W, Cx], 16-byte aligned.
+ * X: bfloat16 NHWC [N, H, W, Cx], 16-byte aligned, smaller than 2 GiB.
  * Y: bfloat16 NHWC [N, P, Q, sum_g M_g], P = (H + 2*pad - C)/stride + 1, same for Q.
  * sizes: host struct filled by structadmm_compact for the same Wc / tables.
  */
@@ -225,7 +230,18 @@ typedef struct sa_conv_desc {
     const int32_t *col_ch;
     const int32_t *col_tap;
     uint16_t *Y;
+    void *ws;                    /* device scratch of structadmm_conv_workspace() bytes,
+                                    256-byte aligned (NULL when that size is 0) */
+    size_t ws_bytes;
 } sa_conv_desc;
+
+/* Scratch bytes structadmm_conv_fwd needs.  Groups whose columns are every
+ * tap times one run of 8k input channels (dense, filter- or channel-pruned)
+ * need none; other groups (filter-shape pruning, inputs with few channels)
+ * first gather their compacted im2col rows, N*P*Q x ldk bfloat16, into the
+ * scratch (groups run one after another and share it).  Returns 0 for an
+ * invalid descriptor; structadmm_conv_fwd reports those. */
+size_t structadmm_conv_workspace(const sa_conv_desc *desc);
 
 int structadmm_conv_fwd(const sa_conv_desc *desc, hipStream_t stream);
 

@@ -58,19 +58,21 @@ class CompactSizes(ctypes.Structure):
     _fields_ = [("groups", ctypes.c_int32), ("M", ctypes.c_int32 * _G), ("K", ctypes.c_int32 * _G),
                 ("ldk", ctypes.c_int32 * _G), ("wc_offset", ctypes.c_int64 * _G),
                 ("row_offset", ctypes.c_int32 * _G), ("col_offset", ctypes.c_int32 * _G),
-                ("run", ctypes.c_int32 * _G), ("run_base", ctypes.c_int32 * _G)]
+                ("run", ctypes.c_int32 * _G), ("run_base", ctypes.c_int32 * _G),
+                ("ch_lo", ctypes.c_int32 * _G), ("ch_span", ctypes.c_int32 * _G)]
 
     def as_dict(self):
         g = self.groups
         return {k: list(getattr(self, k))[:g] for k in
-                ("M", "K", "ldk", "wc_offset", "row_offset", "col_offset", "run", "run_base")}
+                ("M", "K", "ldk", "wc_offset", "row_offset", "col_offset", "run", "run_base",
+                 "ch_lo", "ch_span")}
 
 
 class ConvDesc(ctypes.Structure):
     _fields_ = [("N", ctypes.c_int32), ("H", ctypes.c_int32), ("W", ctypes.c_int32), ("Cx", ctypes.c_int32),
                 ("C", ctypes.c_int32), ("D", ctypes.c_int32), ("stride", ctypes.c_int32), ("pad", ctypes.c_int32),
                 ("sizes", ctypes.POINTER(CompactSizes)), ("X", _vp), ("Wc", _vp), ("col_ch", _vp),
-                ("col_tap", _vp), ("Y", _vp)]
+                ("col_tap", _vp), ("Y", _vp), ("ws", _vp), ("ws_bytes", ctypes.c_size_t)]
 
 
 class StructAdmmError(RuntimeError):
@@ -100,6 +102,8 @@ def lib():
         L.structadmm_pack_nhwc.restype = ctypes.c_int
         L.structadmm_conv_fwd.argtypes = [ctypes.POINTER(ConvDesc), _vp]
         L.structadmm_conv_fwd.restype = ctypes.c_int
+        L.structadmm_conv_workspace.argtypes = [ctypes.POINTER(ConvDesc)]
+        L.structadmm_conv_workspace.restype = ctypes.c_size_t
         L.structadmm_last_error.argtypes = []
         L.structadmm_last_error.restype = ctypes.c_char_p
         L.structadmm_version.argtypes = []
@@ -188,7 +192,7 @@ def compact(Z, groups: int = 1, row_mask=None, col_mask=None, chan_mask=None, in
     dev = Z.device
     K = B * C * D
     if out is None:
-        Wc = torch.empty(A * ((K + 7) // 8 * 8), dtype=torch.uint16, device=dev)
+        Wc = torch.empty(A * ((K + 63) // 64 * 64), dtype=torch.uint16, device=dev)
         row_idx = torch.empty(A, dtype=torch.int32, device=dev)
         col_ch = torch.empty(groups * K, dtype=torch.int32, device=dev)
         col_tap = torch.empty(groups * K, dtype=torch.int32, device=dev)
@@ -222,22 +226,34 @@ def conv_out_shape(N, H, W, C, D, stride, pad, sizes: CompactSizes):
     return (N, P, Q, int(sum(sizes.M[g] for g in range(sizes.groups))))
 
 
-def conv_desc(Xp, Wc, col_ch, col_tap, sizes: CompactSizes, C, D, stride, pad, Y) -> ConvDesc:
+def conv_desc(Xp, Wc, col_ch, col_tap, sizes: CompactSizes, C, D, stride, pad, Y, ws=None) -> ConvDesc:
     N, H, W, Cx = Xp.shape
+    nbytes = 0 if ws is None else ws.numel() * ws.element_size()
     return ConvDesc(N, H, W, Cx, C, D, stride, pad, ctypes.pointer(sizes), _ptr(Xp), _ptr(Wc),
-                    _ptr(col_ch), _ptr(col_tap), _ptr(Y))
+                    _ptr(col_ch), _ptr(col_tap), _ptr(Y), _ptr(ws), nbytes)
+
+
+def conv_workspace(Xp, sizes: CompactSizes, C: int, D: int, stride: int, pad: int) -> int:
+    """Scratch bytes structadmm_conv_fwd needs for this input and compaction."""
+    N, H, W, Cx = Xp.shape
+    d = ConvDesc(N, H, W, Cx, C, D, stride, pad, ctypes.pointer(sizes), 16, 16, 16, 16, 16, None, 0)
+    return int(lib().structadmm_conv_workspace(ctypes.byref(d)))
 
 
 def conv_fwd(Xp, Wc, col_ch, col_tap, sizes: CompactSizes, C: int, D: int, stride: int, pad: int,
-             Y=None, stream=None, desc: Optional[ConvDesc] = None):
-    """structadmm_conv_fwd; Xp bf16 NHWC (uint16), returns Y bf16 NHWC (uint16)."""
+             Y=None, ws=None, stream=None, desc: Optional[ConvDesc] = None):
+    """structadmm_conv_fwd; Xp bf16 NHWC (uint16), returns Y bf16 NHWC (uint16).
+    ``ws``: uint8 device scratch of conv_workspace() bytes (allocated here when None)."""
     import torch
     if desc is None:
         N, H, W, Cx = Xp.shape
         if Y is None:
             Y = torch.empty(conv_out_shape(N, H, W, C, D, stride, pad, sizes), dtype=torch.uint16,
                             device=Xp.device)
-        desc = conv_desc(Xp, Wc, col_ch, col_tap, sizes, C, D, stride, pad, Y)
+        if ws is None:
+            need = conv_workspace(Xp, sizes, C, D, stride, pad)
+            ws = torch.empty(need, dtype=torch.uint8, device=Xp.device) if need else None
+        desc = conv_desc(Xp, Wc, col_ch, col_tap, sizes, C, D, stride, pad, Y, ws)
     _check(lib().structadmm_conv_fwd(ctypes.byref(desc), _stream(stream)), "structadmm_conv_fwd")
     return Y
 

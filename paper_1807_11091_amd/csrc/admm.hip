@@ -6,12 +6,12 @@
 //   k_expand_allowed  (layers with an input-channel support) per-column support bytes
 //   k_row_scores      filter sets: one wavefront per weight row, O_a in binary64
 //   k_col_partials    channel / shape sets: binary64 column sums per band of rows
-//   k_select          one workgroup per structured layer: final scores, LDS radix
-//                     select on the 64-bit score bits, lowest-index tie-break,
-//                     mask + ascending kept_idx, per-column keep bytes
+//   k_select          one workgroup per structured layer: final scores, bitonic
+//                     sort of (score bits, index) pairs in LDS, lowest-index
+//                     tie-break, mask + ascending kept_idx, per-column keep bytes
 //   k_elem_*          non-structured sets: 3 histogram passes over |v| bits, then an
 //                     order-preserving count / scan / apply
-//   k_apply           row-streaming Z (+ fused U', G) writer
+//   k_apply           flat streaming Z (+ fused U', G) writer over every layer
 // Every reduction has a fixed order; no floating-point atomics are used.
 #include <hip/hip_runtime.h>
 
@@ -30,7 +30,7 @@ namespace {
 constexpr int kTab = 16;           // layers per launch (kernel-argument table)
 constexpr int kRowThreads = 256;   // 4 wavefronts, one weight row each at a time
 constexpr int kColThreads = 256;
-constexpr int kColBand = 16;       // rows per band of column partial sums
+constexpr int kColBand = 32;       // rows per band of column partial sums
 constexpr int kSelThreads = 1024;
 constexpr int kElemThreads = 256;
 constexpr int kElemPerThread = 8;
@@ -221,123 +221,106 @@ __global__ __launch_bounds__(kColThreads) void k_col_partials(ColTab tab) {
 }
 
 // ---------------------------------------------------------------- select
-// One workgroup per structured layer.  Keeps exactly k groups: those whose
-// score exceeds the k-th largest score T, plus the lowest-index groups whose
-// score equals T.  Scores are non-negative binary64 values, so their bit
-// patterns order like unsigned integers; T is found by an 8-pass MSB-first
-// radix select (8-bit digits) over those bits in LDS.
+// One workgroup per structured layer.  Keeps exactly k groups: the first k
+// of the order (score descending, index ascending), i.e. every group whose
+// score exceeds the k-th largest score plus the lowest-index groups that tie
+// with it.  The (score bits, index) pairs are sorted in LDS by a bitonic
+// network (scores are non-negative binary64, so their bit patterns order
+// like unsigned integers); no atomics, so the result is reproducible.
+// s + p[0] + p[stride] + ... + p[(n-1)*stride], added in that order; the
+// loads of each group of 8 are issued together (latency, not bandwidth,
+// bounds this reduction).
+__device__ inline double sum_bands(const double *p, int stride, int n, double s) {
+    int b = 0;
+    for (; b + 8 <= n; b += 8) {
+        double v[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) v[q] = p[(int64_t)(b + q) * stride];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) s += v[q];
+    }
+    for (; b < n; ++b) s += p[(int64_t)b * stride];
+    return s;
+}
+
+__device__ inline bool sel_before(uint64_t ka, uint32_t ia, uint64_t kb, uint32_t ib) {
+    return ka > kb || (ka == kb && ia < ib);
+}
+
 __global__ __launch_bounds__(kSelThreads) void k_select(SelTab tab) {
     __shared__ uint64_t skey[SA_MAX_STRUCT_GROUPS];
+    __shared__ uint16_t sidx[SA_MAX_STRUCT_GROUPS];
     __shared__ uint8_t smask[SA_MAX_STRUCT_GROUPS];
-    __shared__ uint32_t hist[256];
     __shared__ uint32_t scan_tmp[kSelThreads / kWave + 1];
-    __shared__ uint64_t s_prefix;
-    __shared__ uint32_t s_kk;
 
     const SelLayer &L = tab.L[blockIdx.x];
     const int tid = threadIdx.x;
     const int G = L.G;
+    int Gp = 1;
+    while (Gp < G) Gp <<= 1;
 
-    // 1. final scores
-    for (int g = tid; g < G; g += kSelThreads) {
-        double s;
-        if (L.kind == SA_FILTER) {
-            s = L.scores[g];
-        } else if (L.kind == SA_SHAPE) {
-            s = 0.0;
-            for (int b = 0; b < L.nbands; ++b) s += L.partials[(int64_t)b * L.K + g];
-        } else {  // channel: sum over taps, then bands
-            s = 0.0;
-            for (int t = 0; t < L.CD; ++t)
-                for (int b = 0; b < L.nbands; ++b) s += L.partials[(int64_t)b * L.K + g * L.CD + t];
+    // 1. final scores (and padding that sorts after every real group)
+    for (int g = tid; g < Gp; g += kSelThreads) {
+        if (g < G) {
+            double s;
+            if (L.kind == SA_FILTER) {
+                s = L.scores[g];
+            } else if (L.kind == SA_SHAPE) {
+                s = sum_bands(L.partials + g, L.K, L.nbands, 0.0);
+            } else {  // channel: over taps, then bands
+                s = 0.0;
+                for (int t = 0; t < L.CD; ++t) s = sum_bands(L.partials + g * L.CD + t, L.K, L.nbands, s);
+            }
+            if (L.kind != SA_FILTER) L.scores[g] = s;
+            skey[g] = (uint64_t)__double_as_longlong(s);
+            sidx[g] = (uint16_t)g;
+        } else {
+            skey[g] = 0;
+            sidx[g] = 0xffffu;
         }
-        if (L.kind != SA_FILTER) L.scores[g] = s;
-        skey[g] = __double_as_longlong(s);
-    }
-    if (tid == 0) {
-        s_prefix = 0;
-        s_kk = (uint32_t)L.k;
+        smask[g] = 0;
     }
     __syncthreads();
 
-    // 2. T = k-th largest key (k >= 1)
-    if (L.k > 0) {
-        for (int pass = 0; pass < 8; ++pass) {
-            const int shift = 56 - 8 * pass;
-            if (tid < 256) hist[tid] = 0;
-            __syncthreads();
-            const uint64_t prefix = s_prefix;
-            for (int g = tid; g < G; g += kSelThreads) {
-                uint64_t key = skey[g];
-                bool match = pass == 0 || (key >> (shift + 8)) == prefix;
-                if (match) atomicAdd(&hist[(uint32_t)(key >> shift) & 255u], 1u);
-            }
-            __syncthreads();
-            if (tid < kWave) {
-                // lane l owns digits 255-4l .. 252-4l (descending)
-                uint32_t c[4];
-                uint32_t sum = 0;
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    c[q] = hist[255 - 4 * tid - q];
-                    sum += c[q];
-                }
-                uint32_t incl = wave_incl_scan(sum);
-                uint32_t excl = incl - sum;
-                const uint32_t kk = s_kk;
-                if (excl < kk && kk <= incl) {
-                    uint32_t above = excl;
-                    int d = 0;
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        if (above + c[q] >= kk) {
-                            d = 255 - 4 * tid - q;
-                            break;
-                        }
-                        above += c[q];
+    // 2. bitonic sort into (score desc, index asc) order
+    if (L.k > 0 && L.k < G) {
+        for (int size = 2; size <= Gp; size <<= 1) {
+            for (int stride = size >> 1; stride > 0; stride >>= 1) {
+                for (int t = tid; t < (Gp >> 1); t += kSelThreads) {
+                    const int i = 2 * t - (t & (stride - 1));
+                    const int j = i + stride;
+                    const bool up = (i & size) == 0;
+                    const uint64_t ka = skey[i], kb = skey[j];
+                    const uint32_t ia = sidx[i], ib = sidx[j];
+                    const bool swap = up ? sel_before(kb, ib, ka, ia) : sel_before(ka, ia, kb, ib);
+                    if (swap) {
+                        skey[i] = kb;
+                        skey[j] = ka;
+                        sidx[i] = (uint16_t)ib;
+                        sidx[j] = (uint16_t)ia;
                     }
-                    s_prefix = (prefix << 8) | (uint64_t)d;
-                    s_kk = kk - above;
                 }
+                __syncthreads();
             }
-            __syncthreads();
         }
+        for (int r = tid; r < L.k; r += kSelThreads) smask[sidx[r]] = 1;
+    } else if (L.k == G) {
+        for (int g = tid; g < G; g += kSelThreads) smask[g] = 1;
     }
-    const uint64_t T = s_prefix;
-    const uint32_t need = L.k > 0 ? s_kk : 0u;  // ties at T to keep
+    __syncthreads();
 
-    // 3. ordered scans: tie ranks, then kept positions
+    // 3. mask and ascending kept list (ordered workgroup scan)
     const int per = (G + kSelThreads - 1) / kSelThreads;
     const int g0 = min(G, tid * per), g1 = min(G, g0 + per);
-    uint32_t eq_local = 0;
-    if (L.k > 0)
-        for (int g = g0; g < g1; ++g) eq_local += skey[g] == T;
-    uint32_t total;
-    uint32_t eq_before = block_excl_scan(eq_local, scan_tmp, &total);
     uint32_t kept_local = 0;
-    {
-        uint32_t r = eq_before;
-        for (int g = g0; g < g1; ++g) {
-            bool keep = false;
-            if (L.k > 0) {
-                uint64_t key = skey[g];
-                if (key > T) keep = true;
-                else if (key == T) keep = (r++ < need);
-            }
-            smask[g] = keep ? 1 : 0;
-            kept_local += keep;
-        }
+    for (int g = g0; g < g1; ++g) kept_local += smask[g];
+    uint32_t total;
+    uint32_t pos = block_excl_scan(kept_local, scan_tmp, &total);
+    for (int g = g0; g < g1; ++g) {
+        L.mask[g] = smask[g];
+        if (smask[g] && pos < (uint32_t)L.k) L.kept_idx[pos] = g;
+        pos += smask[g];
     }
-    uint32_t kept_before = block_excl_scan(kept_local, scan_tmp, &total);
-    {
-        uint32_t pos = kept_before;
-        for (int g = g0; g < g1; ++g) {
-            L.mask[g] = smask[g];
-            if (smask[g] && pos < (uint32_t)L.k) L.kept_idx[pos] = g;
-            pos += smask[g];
-        }
-    }
-    __syncthreads();
 
     // 4. per-column keep bytes for the apply pass
     if (L.colkeep) {
@@ -356,75 +339,90 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelTab tab) {
 
 // ---------------------------------------------------------------- apply
 // Z = v on kept entries, +0 elsewhere; fused: U' = v - Z, G = rho * ((W - Z) + U').
-__global__ __launch_bounds__(kRowThreads) void k_apply(RowTab tab) {
+// Flat float4 stream over the layer; entry e sits at row e / K, column e % K.
+struct ApplyLayer {
+    const float *W;
+    float *U;
+    float *Z;
+    float *G;
+    const uint8_t *rowkeep;  // [A] or null
+    const uint8_t *colkeep;  // [groups*K] or null
+    FastDiv divK, divAg;
+    int32_t n, K;
+    float rho;
+};
+struct ApplyTab {
+    ApplyLayer L[kTab];
+    int32_t begin[kTab + 1];
+    int32_t nl;
+};
+
+constexpr int kApplyThreads = 256;
+constexpr int kApplyVec = 4;  // float4 per thread
+constexpr int kApplyChunk = kApplyThreads * kApplyVec * 4;
+
+__device__ inline void apply_one(const ApplyLayer &L, float w, float u, uint32_t row, uint32_t col, bool fused,
+                                 float &z, float &un, float &g) {
+    bool keep = true;
+    if (L.rowkeep) keep = L.rowkeep[row] != 0;
+    if (keep && L.colkeep) keep = L.colkeep[(int64_t)fdiv(row, L.divAg) * L.K + col] != 0;
+    const float v = w + u;
+    z = keep ? v : 0.0f;
+    if (fused) {
+        un = v - z;
+        const float wz = w - z;
+        const float s = wz + un;
+        g = L.rho * s;
+    }
+}
+
+__global__ __launch_bounds__(kApplyThreads) void k_apply(ApplyTab tab) {
     const int li = find_layer(tab.begin, tab.nl, blockIdx.x);
-    const RowLayer &L = tab.L[li];
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    const int r0 = (blockIdx.x - tab.begin[li]) * L.rpb;
-    const int r1 = min(L.A, r0 + L.rpb);
+    const ApplyLayer &L = tab.L[li];
     const bool fused = L.G != nullptr;
-    for (int a = r0 + wave; a < r1; a += kRowThreads / kWave) {
-        const int64_t base = (int64_t)a * L.K;
-        const bool rk = L.rowkeep ? (L.rowkeep[a] != 0) : true;
-        const uint8_t *ck = L.colkeep ? L.colkeep + (int64_t)(a / L.Ag) * L.K : nullptr;
-        if (L.vec) {
-            const int K4 = L.K >> 2;
-            float4 *z4 = reinterpret_cast<float4 *>(L.Z + base);
-            if (!rk && !fused) {
-                // pruned row, projection only: Z = 0 without touching W, U
-                for (int i = lane; i < K4; i += kWave) z4[i] = make_float4(0.f, 0.f, 0.f, 0.f);
-                continue;
+    const int64_t c0 = (int64_t)(blockIdx.x - tab.begin[li]) * kApplyChunk;
+    float4 xw[kApplyVec], xu[kApplyVec];
+#pragma unroll
+    for (int q = 0; q < kApplyVec; ++q) {
+        const int64_t e = c0 + ((int64_t)q * kApplyThreads + threadIdx.x) * 4;
+        if (e + 4 <= L.n) {
+            xw[q] = *reinterpret_cast<const float4 *>(L.W + e);
+            xu[q] = *reinterpret_cast<const float4 *>(L.U + e);
+        }
+    }
+#pragma unroll
+    for (int q = 0; q < kApplyVec; ++q) {
+        const int64_t e = c0 + ((int64_t)q * kApplyThreads + threadIdx.x) * 4;
+        if (e >= L.n) continue;
+        if (e + 4 <= L.n) {
+            uint32_t row = fdiv((uint32_t)e, L.divK);
+            uint32_t col = (uint32_t)e - row * (uint32_t)L.K;
+            float w[4] = {xw[q].x, xw[q].y, xw[q].z, xw[q].w};
+            float u[4] = {xu[q].x, xu[q].y, xu[q].z, xu[q].w};
+            float z[4], un[4], g[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                apply_one(L, w[i], u[i], row, col, fused, z[i], un[i], g[i]);
+                if (++col == (uint32_t)L.K) {
+                    col = 0;
+                    ++row;
+                }
             }
-            const float4 *w4 = reinterpret_cast<const float4 *>(L.W + base);
-            float4 *u4 = reinterpret_cast<float4 *>(L.U + base);
-            float4 *g4 = fused ? reinterpret_cast<float4 *>(L.G + base) : nullptr;
-            const uchar4 *c4 = reinterpret_cast<const uchar4 *>(ck);
-            for (int i0 = 0; i0 < K4; i0 += 4 * kWave) {
-                float4 x[4], y[4];
-#pragma unroll
-                for (int u = 0; u < 4; ++u) {
-                    int i = i0 + u * kWave + lane;
-                    if (i < K4) {
-                        x[u] = w4[i];
-                        y[u] = u4[i];
-                    }
-                }
-#pragma unroll
-                for (int u = 0; u < 4; ++u) {
-                    int i = i0 + u * kWave + lane;
-                    if (i >= K4) continue;
-                    uchar4 m = c4 ? c4[i] : make_uchar4(1, 1, 1, 1);
-                    float v[4] = {x[u].x + y[u].x, x[u].y + y[u].y, x[u].z + y[u].z, x[u].w + y[u].w};
-                    float w[4] = {x[u].x, x[u].y, x[u].z, x[u].w};
-                    uint8_t mk[4] = {m.x, m.y, m.z, m.w};
-                    float z[4], un[4], gg[4];
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        z[e] = (rk && mk[e]) ? v[e] : 0.0f;
-                        un[e] = v[e] - z[e];
-                        float wz = w[e] - z[e];
-                        float s = wz + un[e];
-                        gg[e] = L.rho * s;
-                    }
-                    z4[i] = make_float4(z[0], z[1], z[2], z[3]);
-                    if (fused) {
-                        u4[i] = make_float4(un[0], un[1], un[2], un[3]);
-                        g4[i] = make_float4(gg[0], gg[1], gg[2], gg[3]);
-                    }
-                }
+            *reinterpret_cast<float4 *>(L.Z + e) = make_float4(z[0], z[1], z[2], z[3]);
+            if (fused) {
+                *reinterpret_cast<float4 *>(L.U + e) = make_float4(un[0], un[1], un[2], un[3]);
+                *reinterpret_cast<float4 *>(L.G + e) = make_float4(g[0], g[1], g[2], g[3]);
             }
         } else {
-            for (int i = lane; i < L.K; i += kWave) {
-                float w = L.W[base + i];
-                float v = w + L.U[base + i];
-                float z = (rk && (!ck || ck[i])) ? v : 0.0f;
-                L.Z[base + i] = z;
+            for (int64_t f = e; f < L.n; ++f) {
+                uint32_t row = fdiv((uint32_t)f, L.divK);
+                uint32_t col = (uint32_t)f - row * (uint32_t)L.K;
+                float z, un = 0.f, g = 0.f;
+                apply_one(L, L.W[f], L.U[f], row, col, fused, z, un, g);
+                L.Z[f] = z;
                 if (fused) {
-                    float un = v - z;
-                    float wz = w - z;
-                    float s = wz + un;
-                    L.U[base + i] = un;
-                    L.G[base + i] = L.rho * s;
+                    L.U[f] = un;
+                    L.G[f] = g;
                 }
             }
         }
@@ -1004,17 +1002,31 @@ extern "C" int structadmm_project(const sa_project_desc *layers, int n_layers, v
             for (int i : ids)
                 if (layers[i].kind != SA_ELEMENT) sl.push_back(i);
             for (size_t s = 0; s < sl.size(); s += kTab) {
-                RowTab tab;
+                ApplyTab tab;
                 memset(&tab, 0, sizeof tab);
                 int blocks = 0;
                 tab.nl = (int)std::min<size_t>(kTab, sl.size() - s);
                 for (int t = 0; t < tab.nl; ++t) {
-                    fill_row(sl[s + t], tab.L[t]);
+                    RowLayer R;
+                    fill_row(sl[s + t], R);
+                    const sa_project_desc &d = layers[sl[s + t]];
+                    ApplyLayer &L = tab.L[t];
+                    L.W = R.W;
+                    L.U = R.U;
+                    L.Z = R.Z;
+                    L.G = R.G;
+                    L.rowkeep = R.rowkeep;
+                    L.colkeep = R.colkeep;
+                    L.divK = make_fastdiv((uint32_t)R.K);
+                    L.divAg = make_fastdiv((uint32_t)R.Ag);
+                    L.n = (int32_t)(d.A * d.B * d.C * d.D);
+                    L.K = R.K;
+                    L.rho = R.rho;
                     tab.begin[t] = blocks;
-                    blocks += (tab.L[t].A + tab.L[t].rpb - 1) / tab.L[t].rpb;
+                    blocks += (int)((L.n + kApplyChunk - 1) / kApplyChunk);
                 }
                 tab.begin[tab.nl] = blocks;
-                hipLaunchKernelGGL(k_apply, dim3(blocks), dim3(kRowThreads), 0, stream, tab);
+                hipLaunchKernelGGL(k_apply, dim3(blocks), dim3(kApplyThreads), 0, stream, tab);
                 if (int rc = launch_check("k_apply")) return rc;
             }
         }

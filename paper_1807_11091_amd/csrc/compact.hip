@@ -19,13 +19,14 @@ namespace sa {
 namespace {
 
 constexpr int kCompThreads = 1024;
+constexpr int kCS = 8;  // ints per conv group in the size record
 
 struct CompArgs {
     const float *Z;
     const uint8_t *row_mask, *col_mask, *chan_mask, *in_ch_mask;
     uint16_t *Wc;
     int32_t *row_idx, *col_ch, *col_tap;
-    int32_t *counts;  // ws: [groups][4] = M, K, run, run_base
+    int32_t *counts;  // ws: [groups][kCS] = M, K, run, run_base, ch_lo, ch_span
     int32_t A, B, C, D, groups, in_compacted;
 };
 
@@ -46,30 +47,37 @@ __device__ inline int in_position(const CompArgs &a, int full) {
     return pos;
 }
 
-// Per conv group: M (kept rows), K (kept columns) and, when every tap keeps
-// the same channels and their input positions are consecutive, the channel run.
+// Per conv group: M (kept rows), K (kept columns), the span of input channels
+// the kept columns read and, when every tap keeps the same channels and their
+// input positions are consecutive, that channel run.
 __global__ __launch_bounds__(kCompThreads) void k_compact_count(CompArgs a) {
     __shared__ uint32_t tmp[kCompThreads / kWave + 1];
-    __shared__ int s_first, s_last;
+    __shared__ int s_first, s_last, s_cfirst, s_clast;
     const int gc = blockIdx.x;
     const int Ag = a.A / a.groups, taps = a.C * a.D;
+    if (threadIdx.x == 0) {
+        s_first = -1;
+        s_last = -1;
+        s_cfirst = -1;
+        s_clast = -1;
+    }
+    __syncthreads();
     uint32_t m = 0, kc = 0, nb = 0;
     for (int r = threadIdx.x; r < Ag; r += kCompThreads) m += (!a.row_mask || a.row_mask[gc * Ag + r]) ? 1 : 0;
     for (int64_t i = threadIdx.x; i < (int64_t)taps * a.B; i += kCompThreads) {
         int t = (int)(i / a.B), b = (int)(i - (int64_t)t * a.B);
-        kc += col_kept(a, gc, t, b) ? 1 : 0;
+        if (col_kept(a, gc, t, b)) {
+            ++kc;
+            atomicMin(reinterpret_cast<unsigned *>(&s_cfirst), (unsigned)b);  // -1 is the largest unsigned
+            atomicMax(&s_clast, b);
+        }
     }
-    if (threadIdx.x == 0) {
-        s_first = -1;
-        s_last = -1;
-    }
-    __syncthreads();
     // kept channels ignoring the shape mask (defines the run when there is no shape mask)
     for (int b = threadIdx.x; b < a.B; b += kCompThreads) {
         bool keep = (!a.chan_mask || a.chan_mask[b]) && (!a.in_ch_mask || a.in_ch_mask[gc * a.B + b]);
         nb += keep ? 1 : 0;
         if (keep) {
-            atomicMin(reinterpret_cast<unsigned *>(&s_first), (unsigned)b);  // -1 is the largest unsigned
+            atomicMin(reinterpret_cast<unsigned *>(&s_first), (unsigned)b);
             atomicMax(&s_last, b);
         }
     }
@@ -87,10 +95,17 @@ __global__ __launch_bounds__(kCompThreads) void k_compact_count(CompArgs a) {
                 base = p0;
             }
         }
-        a.counts[4 * gc + 0] = (int)tot_m;
-        a.counts[4 * gc + 1] = (int)tot_k;
-        a.counts[4 * gc + 2] = run;
-        a.counts[4 * gc + 3] = base;
+        int clo = 0, cspan = 0;
+        if (tot_k > 0) {
+            clo = in_position(a, gc * a.B + s_cfirst);
+            cspan = in_position(a, gc * a.B + s_clast) - clo + 1;
+        }
+        a.counts[kCS * gc + 0] = (int)tot_m;
+        a.counts[kCS * gc + 1] = (int)tot_k;
+        a.counts[kCS * gc + 2] = run;
+        a.counts[kCS * gc + 3] = base;
+        a.counts[kCS * gc + 4] = clo;
+        a.counts[kCS * gc + 5] = cspan;
     }
 }
 
@@ -101,8 +116,8 @@ __global__ __launch_bounds__(kCompThreads) void k_compact_tables(CompArgs a) {
     const int Ag = a.A / a.groups, taps = a.C * a.D;
     int row_off = 0, col_off = 0;
     for (int g = 0; g < gc; ++g) {
-        row_off += a.counts[4 * g + 0];
-        col_off += a.counts[4 * g + 1];
+        row_off += a.counts[kCS * g + 0];
+        col_off += a.counts[kCS * g + 1];
     }
     uint32_t running = 0;
     const int64_t ncand = (int64_t)taps * a.B;
@@ -137,15 +152,15 @@ __global__ __launch_bounds__(kCompThreads) void k_compact_tables(CompArgs a) {
 // Wc rows: block (m, gc) writes row m of group gc: bf16(Z[a, b, c, d]) per column, 0 padding.
 __global__ __launch_bounds__(256) void k_compact_gather(CompArgs a) {
     const int m = blockIdx.x, gc = blockIdx.y;
-    const int M = a.counts[4 * gc + 0];
+    const int M = a.counts[kCS * gc + 0];
     if (m >= M) return;
-    const int K = a.counts[4 * gc + 1];
-    const int ldk = (K + 7) / 8 * 8;
+    const int K = a.counts[kCS * gc + 1];
+    const int ldk = (K + 63) / 64 * 64;
     int64_t wc_off = 0;
     int row_off = 0, col_off = 0;
     for (int g = 0; g < gc; ++g) {
-        const int Mg = a.counts[4 * g + 0], Kg = a.counts[4 * g + 1];
-        wc_off += (int64_t)Mg * ((Kg + 7) / 8 * 8);
+        const int Mg = a.counts[kCS * g + 0], Kg = a.counts[kCS * g + 1];
+        wc_off += (int64_t)Mg * ((Kg + 63) / 64 * 64);
         row_off += Mg;
         col_off += Kg;
     }
@@ -188,16 +203,18 @@ __global__ __launch_bounds__(kCompThreads) void k_compact_inpos(CompArgs a, int 
 constexpr int kPackTile = 64;
 
 // X binary32 NCHW -> Xp bfloat16 NHWC with kept channels in ascending order.
-// Workgroup = 64 channels x 64 pixels of one image, transposed through LDS.
+// Workgroup = 64 channels x 64 pixels of one image: float4 loads along the
+// pixels, bf16 conversion, transpose through LDS with every kept channel at
+// its output rank, 16-byte stores along the channels when aligned.
 __global__ __launch_bounds__(256) void k_pack_nhwc(const float *__restrict__ X, const uint8_t *__restrict__ keep,
                                                    uint16_t *__restrict__ Xp, int Cin, int HW, int Cx) {
-    __shared__ uint16_t tile[kPackTile][kPackTile + 2];
-    __shared__ int32_t cpos[kPackTile];
-    __shared__ int32_t s_base;
+    __shared__ __attribute__((aligned(16))) uint16_t tile[kPackTile][kPackTile + 8];  // [pixel][rank]
+    __shared__ int32_t crank[kPackTile];
+    __shared__ int32_t s_base, s_nkept;
     const int p0 = blockIdx.x * kPackTile, c0 = blockIdx.y * kPackTile, n = blockIdx.z;
     const int tid = threadIdx.x;
     if (tid < kWave) {
-        // position of channel c0 among kept channels, then ranks inside the tile
+        // rank of channel c0 among the kept channels, then ranks inside the tile
         uint32_t cnt = 0;
         if (keep)
             for (int c = tid; c < c0; c += kWave) cnt += keep[c] != 0;
@@ -205,23 +222,66 @@ __global__ __launch_bounds__(256) void k_pack_nhwc(const float *__restrict__ X, 
             cnt = (tid == 0) ? (uint32_t)c0 : 0u;
         cnt = wave_sum_u32(cnt);
         const int c = c0 + tid;
-        uint32_t f = (c < Cin && (!keep || keep[c])) ? 1u : 0u;
-        uint32_t incl = wave_incl_scan(f);
-        cpos[tid] = f ? (int32_t)(cnt + incl - 1) : -1;
+        const uint32_t f = (c < Cin && (!keep || keep[c])) ? 1u : 0u;
+        const uint32_t incl = wave_incl_scan(f);
+        crank[tid] = f ? (int32_t)(incl - 1) : -1;
         if (tid == 0) s_base = (int32_t)cnt;
-    }
-    for (int i = tid; i < kPackTile * kPackTile; i += 256) {
-        const int cl = i / kPackTile, pl = i % kPackTile;
-        const int c = c0 + cl, p = p0 + pl;
-        float v = (c < Cin && p < HW) ? X[((int64_t)n * Cin + c) * HW + p] : 0.0f;
-        tile[cl][pl] = f32_to_bf16_bits(v);
+        if (tid == kWave - 1) s_nkept = (int32_t)incl;
     }
     __syncthreads();
-    for (int i = tid; i < kPackTile * kPackTile; i += 256) {
-        const int pl = i / kPackTile, cl = i % kPackTile;
-        const int p = p0 + pl;
-        const int cp = cpos[cl];
-        if (p < HW && cp >= 0 && cp < Cx) Xp[((int64_t)n * HW + p) * Cx + cp] = tile[cl][pl];
+    const int nk = s_nkept, base = s_base;
+    if (nk == 0) return;
+    const bool vec_in = (HW % 4) == 0;
+    for (int i = tid; i < kPackTile * (kPackTile / 4); i += 256) {
+        const int cl = i / (kPackTile / 4), pq = i % (kPackTile / 4);
+        const int r = crank[cl];
+        if (r < 0) continue;
+        const int p = p0 + pq * 4;
+        const float *src = X + ((int64_t)n * Cin + c0 + cl) * HW + p;
+        float v[4] = {0.f, 0.f, 0.f, 0.f};
+        if (vec_in && p + 4 <= HW) {
+            const float4 t = *reinterpret_cast<const float4 *>(src);
+            v[0] = t.x;
+            v[1] = t.y;
+            v[2] = t.z;
+            v[3] = t.w;
+        } else {
+            for (int e = 0; e < 4; ++e)
+                if (p + e < HW) v[e] = src[e];
+        }
+#pragma unroll
+        for (int e = 0; e < 4; ++e) tile[pq * 4 + e][r] = f32_to_bf16_bits(v[e]);
+    }
+    __syncthreads();
+    if ((Cx % 8) == 0 && (base % 8) == 0) {
+        const int chunks = (nk + 7) / 8;
+        for (int i = tid; i < kPackTile * chunks; i += 256) {
+            const int pl = i / chunks, ch = i % chunks;
+            const int p = p0 + pl;
+            if (p >= HW) continue;
+            uint16_t *dst = Xp + ((int64_t)n * HW + p) * Cx + base;
+            if (ch * 8 + 8 <= nk && base + ch * 8 + 8 <= Cx) {
+                *reinterpret_cast<uint4 *>(dst + ch * 8) = *reinterpret_cast<const uint4 *>(&tile[pl][ch * 8]);
+            } else {
+                for (int e = ch * 8; e < nk && e < ch * 8 + 8; ++e)
+                    if (base + e < Cx) dst[e] = tile[pl][e];
+            }
+        }
+    } else {
+        for (int i = tid; i < kPackTile * nk; i += 256) {
+            const int pl = i / nk, e = i % nk;
+            const int p = p0 + pl;
+            if (p < HW && base + e < Cx) Xp[((int64_t)n * HW + p) * Cx + base + e] = tile[pl][e];
+        }
+    }
+}
+
+// Few input channels and no channel gather: one thread per pixel.
+__global__ __launch_bounds__(256) void k_pack_small(const float *__restrict__ X, uint16_t *__restrict__ Xp, int Cin,
+                                                    int HW, int64_t pixels) {
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < pixels; i += (int64_t)gridDim.x * 256) {
+        const int64_t n = i / HW, p = i - n * HW;
+        for (int c = 0; c < Cin; ++c) Xp[i * Cin + c] = f32_to_bf16_bits(X[(n * Cin + c) * HW + p]);
     }
 }
 
@@ -262,13 +322,13 @@ extern "C" int structadmm_compact(const sa_compact_desc *desc, sa_compact_sizes 
     if (int rc = check_hip(hipGetLastError(), "k_compact_tables")) return rc;
     hipLaunchKernelGGL(k_compact_gather, dim3(Ag, d.groups), dim3(256), 0, stream, a);
     if (int rc = check_hip(hipGetLastError(), "k_compact_gather")) return rc;
-    int32_t counts[4 * SA_MAX_CONV_GROUPS];
-    if (int rc = check_hip(hipMemcpyAsync(counts, d.ws, sizeof(int32_t) * 4 * d.groups, hipMemcpyDeviceToHost, stream),
+    int32_t counts[kCS * SA_MAX_CONV_GROUPS];
+    if (int rc = check_hip(hipMemcpyAsync(counts, d.ws, sizeof(int32_t) * kCS * d.groups, hipMemcpyDeviceToHost, stream),
                            "compact: copy sizes"))
         return rc;
     if (int rc = check_hip(hipStreamSynchronize(stream), "compact: synchronize")) return rc;
     int total_cols = 0;
-    for (int g = 0; g < d.groups; ++g) total_cols += counts[4 * g + 1];
+    for (int g = 0; g < d.groups; ++g) total_cols += counts[kCS * g + 1];
     if (d.in_compacted && total_cols > 0) {
         size_t lds = sizeof(int32_t) * (size_t)d.groups * d.B;
         hipLaunchKernelGGL(k_compact_inpos, dim3(1), dim3(kCompThreads), lds, stream, a, total_cols);
@@ -280,11 +340,13 @@ extern "C" int structadmm_compact(const sa_compact_desc *desc, sa_compact_sizes 
     int64_t wc_off = 0;
     int32_t row_off = 0, col_off = 0;
     for (int g = 0; g < d.groups; ++g) {
-        sizes->M[g] = counts[4 * g + 0];
-        sizes->K[g] = counts[4 * g + 1];
-        sizes->ldk[g] = (sizes->K[g] + 7) / 8 * 8;
-        sizes->run[g] = counts[4 * g + 2];
-        sizes->run_base[g] = counts[4 * g + 3];
+        sizes->M[g] = counts[kCS * g + 0];
+        sizes->K[g] = counts[kCS * g + 1];
+        sizes->ldk[g] = (sizes->K[g] + 63) / 64 * 64;
+        sizes->run[g] = counts[kCS * g + 2];
+        sizes->run_base[g] = counts[kCS * g + 3];
+        sizes->ch_lo[g] = counts[kCS * g + 4];
+        sizes->ch_span[g] = counts[kCS * g + 5];
         sizes->wc_offset[g] = wc_off;
         sizes->row_offset[g] = row_off;
         sizes->col_offset[g] = col_off;
@@ -305,6 +367,12 @@ extern "C" int structadmm_pack_nhwc(const float *X, int32_t N, int32_t Cin, int3
     if ((int64_t)H * W > (int64_t(1) << 30) || (int64_t)Cin > 65535 || (int64_t)N > 65535)
         return fail(SA_E_UNSUPPORTED, "pack: tensor too large");
     const int HW = H * W;
+    if (!keep && Cin <= 8) {
+        const int64_t pixels = (int64_t)N * HW;
+        const int blocks = (int)std::min<int64_t>(8192, (pixels + 255) / 256);
+        hipLaunchKernelGGL(k_pack_small, dim3(blocks), dim3(256), 0, stream, X, Xp, Cin, HW, pixels);
+        return check_hip(hipGetLastError(), "k_pack_small");
+    }
     dim3 grid((HW + kPackTile - 1) / kPackTile, (Cin + kPackTile - 1) / kPackTile, N);
     hipLaunchKernelGGL(k_pack_nhwc, grid, dim3(256), 0, stream, X, keep, Xp, Cin, HW, Cx);
     return check_hip(hipGetLastError(), "k_pack_nhwc");

@@ -42,8 +42,9 @@ def _c_layout():
         "sa_project_desc": ("ProjectDesc", ["A", "groups", "kind", "k", "W", "in_ch_mask", "scores", "rho", "G"]),
         "sa_dual_desc": ("DualDesc", ["n", "W", "U", "rho", "G", "update_dual"]),
         "sa_compact_desc": ("CompactDesc", ["groups", "Z", "in_compacted", "Wc", "ws"]),
-        "sa_compact_sizes": ("CompactSizes", ["M", "K", "ldk", "wc_offset", "row_offset", "run", "run_base"]),
-        "sa_conv_desc": ("ConvDesc", ["N", "pad", "sizes", "X", "Y"]),
+        "sa_compact_sizes": ("CompactSizes", ["M", "K", "ldk", "wc_offset", "row_offset", "run", "run_base",
+                                              "ch_lo", "ch_span"]),
+        "sa_conv_desc": ("ConvDesc", ["N", "pad", "sizes", "X", "Y", "ws", "ws_bytes"]),
     }
     lines = ["#include <stdio.h>", "#include <stddef.h>", '#include "structadmm.h"', "int main(void){"]
     for st, (_, fs) in fields.items():
@@ -148,7 +149,7 @@ def test_compact_and_conv_validation():
 
     s = sa.CompactSizes()
     s.groups = 1
-    s.M[0], s.K[0], s.ldk[0] = 4, 18, 24
+    s.M[0], s.K[0], s.ldk[0] = 4, 18, 64
     def conv(**kw):
         d = dict(N=1, H=8, W=8, Cx=2, C=3, D=3, stride=1, pad=1, sizes=ctypes.pointer(s), X=FAKE,
                  Wc=FAKE + 256, col_ch=FAKE + 512, col_tap=FAKE + 768, Y=FAKE + 1024)
@@ -164,6 +165,17 @@ def test_compact_and_conv_validation():
     s.run[0] = 0
     s.ldk[0] = 18  # not the padded stride that compaction produces
     assert conv() == -1
+    # a gathered group (run 0) needs scratch for its compacted im2col rows
+    s.ldk[0] = 64
+    s.ch_lo[0], s.ch_span[0] = 0, 2
+    need = L.structadmm_conv_workspace(ctypes.byref(sa.ConvDesc(1, 8, 8, 2, 3, 3, 1, 1, ctypes.pointer(s),
+                                                                FAKE, FAKE, FAKE, FAKE, FAKE, None, 0)))
+    assert need == 8 * 8 * 64 * 2
+    assert conv() == -3
+    assert conv(ws=FAKE + 2048, ws_bytes=need - 1) == -3
+    assert conv(ws=FAKE + 2048 + 16, ws_bytes=need) == -2
+    s.ch_span[0] = 3  # channels past the input
+    assert conv(ws=FAKE + 2048, ws_bytes=need) == -1
 
 
 def test_pack_validation():
