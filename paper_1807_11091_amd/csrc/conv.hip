@@ -43,6 +43,7 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef unsigned short u16x8 __attribute__((ext_vector_type(8)));
 
 constexpr int kBK = 64;            // K slice per stage (= compacted row padding)
 constexpr int kRow = kBK + 8;      // LDS row of a staged operand tile (bf16 elements)
@@ -59,6 +60,15 @@ __device__ inline __amdgpu_buffer_rsrc_t rsrc(const void *base, uint32_t bytes) 
 __device__ inline uint4 bload16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
     auto v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
     return make_uint4(v[0], v[1], v[2], v[3]);
+}
+
+// Workgroups are dispatched to the 8 XCDs round-robin (id mod 8); each XCD has
+// its own L2.  Remap ids so that every XCD walks one contiguous range of tiles
+// (neighbouring tiles share input rows and weight slices): XCD x gets the
+// range of q+1 tiles when x < r, of q tiles otherwise (n = 8q + r).
+__device__ inline int xcd_remap(int bid, int n) {
+    const int xcd = bid & 7, local = bid >> 3, q = n >> 3, r = n & 7;
+    return xcd < r ? xcd * (q + 1) + local : r * (q + 1) + (xcd - r) * q + local;
 }
 
 // ---------------------------------------------------------------- k_conv
@@ -106,7 +116,7 @@ __global__ __launch_bounds__(64 * WN * WM) void k_conv(ConvArgs a) {
     const int wn = wave % WN, wm = wave / WN;
 
     int bid = blockIdx.x;
-    if ((a.nblocks & 7) == 0) bid = (bid & 7) * (a.nblocks >> 3) + (bid >> 3);
+    bid = xcd_remap(bid, a.nblocks);
     int gi = 0;
     while (gi + 1 < a.ngroups && bid >= a.g[gi + 1].begin) ++gi;
     const ConvGroup &G = a.g[gi];
@@ -411,6 +421,294 @@ __global__ __launch_bounds__(256) void k_im2col_global(GatherArgs a) {
     }
 }
 
+// ---------------------------------------------------------------- k_conv_patch
+// Gathered groups without a scratch pass.  A workgroup owns the output tile
+// (32*TM filters) x (128*TN pixels) of one conv group:
+//   1. the input footprint of its pixels (the group's channel span, zero
+//      halo) is copied once into LDS; for stride s > 1 the padded columns are
+//      stored de-interleaved (column w at (w mod s) * Ws + w div s), so the
+//      pixels of an output row read consecutive LDS words at every tap;
+//   2. a per-column table holds the byte offset of (tap, channel) relative to
+//      a pixel's base in that copy;
+//   3. each wavefront owns 32*TN pixels and gathers its MFMA B fragments
+//      straight from the copy into registers (lane = pixel, 8 columns per
+//      lane), while the weight slices (A) are staged through LDS, two
+//      buffers of 32 columns, shared by the four wavefronts.
+// Only ceil(K/16) column steps are run; columns past K in the last step are
+// zeroed in registers, so padding never multiplies a value from the input.
+constexpr int kPatchSlice = 32;                // columns per staged weight slice
+constexpr int kPatchRowA = kPatchSlice + 8;    // LDS row of a weight slice (80 B)
+
+struct PatchGroup {
+    const uint16_t *Wc;      // group base, rows of ldk columns
+    const int32_t *col_ch;   // group base
+    const int32_t *col_tap;  // group base
+    int32_t M, K, ldk, o_off, ch_lo, nch, pix_bytes, mtiles, begin;
+    FastDiv divNch, divRow;  // 16-byte chunks per pixel, chunks per padded input row
+};
+struct PatchArgs {
+    const uint16_t *X;
+    uint16_t *Y;
+    uint32_t x_bytes;
+    int32_t N, H, W, Cx, C, D, stride, pad, P, Q, NPQ, Cy;
+    int32_t Hp, Wp, Ws, Wpp;
+    int32_t ngroups, nblocks, patch_bytes, tab_bytes;
+    FastDiv divQ, divP, divHp, divD, divS;
+    PatchGroup g[SA_MAX_CONV_GROUPS];
+};
+
+template <int TM, int TN>
+struct PatchCfg {
+    static constexpr int NT = 256;
+    static constexpr int BNB = 32 * TM;   // filters per tile
+    static constexpr int BMB = 128 * TN;  // pixels per tile
+    static constexpr int AR = (BNB * (kPatchSlice / 8) + NT - 1) / NT;  // 16-B weight chunks per thread
+    static constexpr int a_bytes = 2 * BNB * kPatchRowA * 2;
+    static constexpr int c_bytes = BMB * (BNB + 8) * 2;
+};
+
+template <int TM, int TN>
+__global__ __launch_bounds__(256) void k_conv_patch(PatchArgs a) {
+    using Cfg = PatchCfg<TM, TN>;
+    constexpr int NT = Cfg::NT, BNB = Cfg::BNB, BMB = Cfg::BMB, AR = Cfg::AR;
+    constexpr int CPS = kPatchSlice / 8;  // 16-B chunks per weight row of a slice
+
+    extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+    uint8_t *patch = smem;
+    int32_t *tab = reinterpret_cast<int32_t *>(smem + a.patch_bytes);
+    uint16_t *sA = reinterpret_cast<uint16_t *>(smem + a.patch_bytes + a.tab_bytes);  // [2][BNB][kPatchRowA]
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+
+    int bid = blockIdx.x;
+    bid = xcd_remap(bid, a.nblocks);
+    int gi = 0;
+    while (gi + 1 < a.ngroups && bid >= a.g[gi + 1].begin) ++gi;
+    const PatchGroup &G = a.g[gi];
+    const int lb = bid - G.begin;
+    const int mt = lb % G.mtiles, nt = lb / G.mtiles;
+    const int m0 = mt * BNB, n0 = nt * BMB;
+
+    // weight slices: issued first, they do not depend on the copy
+    const __amdgpu_buffer_rsrc_t wrs = rsrc(G.Wc, (uint32_t)G.M * (uint32_t)G.ldk * 2u);
+    uint32_t aoff[AR];
+#pragma unroll
+    for (int i = 0; i < AR; ++i) {
+        const int c = tid + i * NT;
+        aoff[i] = ((uint32_t)(m0 + c / CPS) * (uint32_t)G.ldk + (c % CPS) * 8) * 2u;
+    }
+    uint4 wreg[AR];
+    auto load_a = [&](int s) {
+#pragma unroll
+        for (int i = 0; i < AR; ++i) wreg[i] = bload16(wrs, aoff[i] + (uint32_t)s * (kPatchSlice * 2));
+    };
+    auto store_a = [&](int buf) {
+        uint16_t *A = sA + buf * BNB * kPatchRowA;
+#pragma unroll
+        for (int i = 0; i < AR; ++i) {
+            const int c = tid + i * NT;
+            if (BNB * CPS % NT == 0 || c < BNB * CPS)
+                *reinterpret_cast<uint4 *>(&A[(c / CPS) * kPatchRowA + (c % CPS) * 8]) = wreg[i];
+        }
+    };
+    // 32-column slices of two MFMA steps; the table covers two slices more,
+    // so the offsets and B fragments ahead of the last step are read unconditionally
+    const int nsl = (G.K + kPatchSlice - 1) / kPatchSlice;
+    load_a(0);
+
+    // 1. input footprint: padded rows [g0, g1) of the stacked padded images
+    const int r0 = (int)fdiv((uint32_t)n0, a.divQ);
+    const int r1 = (int)fdiv((uint32_t)(min(n0 + BMB, a.NPQ) - 1), a.divQ);
+    const int i0 = (int)fdiv((uint32_t)r0, a.divP), i1 = (int)fdiv((uint32_t)r1, a.divP);
+    const int g0 = i0 * a.Hp + (r0 - i0 * a.P) * a.stride;
+    const int g1 = i1 * a.Hp + (r1 - i1 * a.P) * a.stride + a.C;  // exclusive
+    const int nch = G.nch, pixb = G.pix_bytes;
+    // source order (padded row, padded column, chunk): consecutive threads read
+    // consecutive input bytes; columns land at their de-interleaved position
+    const int rowchunks = a.Wp * nch;
+    const int total = (g1 - g0) * rowchunks;
+    const __amdgpu_buffer_rsrc_t xrs = rsrc(a.X, a.x_bytes);
+    // fill item idx = one 16-byte chunk of 8 channels: its LDS destination and
+    // source element (-1 for the zero halo)
+    auto locate = [&](int idx, int *dst, int *src) {
+        const int pr = (int)fdiv((uint32_t)idx, G.divRow);
+        const int rem = idx - pr * rowchunks;
+        const int wpad = (int)fdiv((uint32_t)rem, G.divNch);
+        const int ch = rem - wpad * nch;
+        const int j = (int)fdiv((uint32_t)wpad, a.divS);
+        const int cp = (wpad - j * a.stride) * a.Ws + j;
+        const int gr = g0 + pr;
+        const int img = (int)fdiv((uint32_t)gr, a.divHp);
+        const int h = gr - img * a.Hp - a.pad, w = wpad - a.pad;
+        const bool in = img < a.N && (unsigned)h < (unsigned)a.H && (unsigned)w < (unsigned)a.W;
+        const int pos = ((img * a.H + h) * a.W + w) * a.Cx + G.ch_lo;  // element index
+        *dst = (pr * a.Wpp + cp) * pixb + ch * 16;
+        *src = in ? pos + ch * 8 : -1;
+    };
+    constexpr int kFill = 16;  // 16-byte loads in flight per thread
+    for (int base = tid; base < total; base += NT * kFill) {
+        uint4 v[kFill];
+        int dst[kFill];
+#pragma unroll
+        for (int u = 0; u < kFill; ++u) {
+            const int idx = base + u * NT;
+            dst[u] = -1;
+            v[u] = make_uint4(0, 0, 0, 0);
+            if (idx >= total) continue;
+            int src;
+            locate(idx, &dst[u], &src);
+            if (src >= 0) v[u] = bload16(xrs, (uint32_t)src * 2u);
+        }
+#pragma unroll
+        for (int u = 0; u < kFill; ++u) {
+            if (dst[u] < 0) continue;
+            uint32_t *d32 = reinterpret_cast<uint32_t *>(patch + dst[u]);
+            d32[0] = v[u].x;
+            d32[1] = v[u].y;
+            d32[2] = v[u].z;
+            d32[3] = v[u].w;
+        }
+    }
+    // 2. column table: (kernel row, kernel column, channel) -> byte offset
+    for (int k = tid; k < (nsl + 2) * kPatchSlice; k += NT) {
+        int32_t off = 0;  // columns past K: zeroed after the gather
+        if (k < G.K) {
+            const int t = G.col_tap[k];
+            const int c = (int)fdiv((uint32_t)t, a.divD), d = t - c * a.D;
+            const int dph = (int)fdiv((uint32_t)d, a.divS);
+            off = (c * a.Wpp + (d - dph * a.stride) * a.Ws + dph) * pixb + (G.col_ch[k] - G.ch_lo) * 2;
+        }
+        tab[k] = off;
+    }
+    store_a(0);
+    if (nsl > 1) load_a(1);
+
+    // byte offset of each owned pixel's window corner in the copy
+    int pbase[TN];
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+        const int px = n0 + wave * 32 * TN + j * 32 + (lane & 31);
+        pbase[j] = 0;  // pixels past the output read the copy's first word; never stored
+        if (px < a.NPQ) {
+            const int r = (int)fdiv((uint32_t)px, a.divQ);
+            const int img = (int)fdiv((uint32_t)r, a.divP);
+            const int gr = img * a.Hp + (r - img * a.P) * a.stride;
+            pbase[j] = ((gr - g0) * a.Wpp + (px - r * a.Q)) * pixb;
+        }
+    }
+    __syncthreads();
+
+    f32x16 acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+    const int frow = lane & 31, fk = (lane >> 5) * 8;
+    // B fragments of the 16 columns from k0: lane = pixel, 8 columns per lane;
+    // the column offsets are read one step before the gather that uses them
+    struct Offs {
+        int4 lo, hi;
+    };
+    auto offsets = [&](int k0) {
+        Offs o;
+        o.lo = *reinterpret_cast<const int4 *>(tab + k0 + fk);
+        o.hi = *reinterpret_cast<const int4 *>(tab + k0 + fk + 4);
+        return o;
+    };
+    auto gather = [&](int k0, const Offs &o, bf16x8 (&b)[TN]) {
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+            const uint8_t *pp = patch + pbase[j];
+            u16x8 v;
+            v[0] = *reinterpret_cast<const uint16_t *>(pp + o.lo.x);
+            v[1] = *reinterpret_cast<const uint16_t *>(pp + o.lo.y);
+            v[2] = *reinterpret_cast<const uint16_t *>(pp + o.lo.z);
+            v[3] = *reinterpret_cast<const uint16_t *>(pp + o.lo.w);
+            v[4] = *reinterpret_cast<const uint16_t *>(pp + o.hi.x);
+            v[5] = *reinterpret_cast<const uint16_t *>(pp + o.hi.y);
+            v[6] = *reinterpret_cast<const uint16_t *>(pp + o.hi.z);
+            v[7] = *reinterpret_cast<const uint16_t *>(pp + o.hi.w);
+            if (k0 + 16 > G.K) {
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    if (k0 + fk + e >= G.K) v[e] = 0;
+            }
+            b[j] = __builtin_bit_cast(bf16x8, v);
+        }
+    };
+    auto mma = [&](const bf16x8 (&af)[TM], const bf16x8 (&b)[TN]) {
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], b[j], acc[i][j], 0, 0, 0);
+    };
+    auto afrag = [&](const uint16_t *A, int kk, bf16x8 (&af)[TM]) {
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+            af[i] = *reinterpret_cast<const bf16x8 *>(&A[(i * 32 + frow) * kPatchRowA + kk + fk]);
+    };
+    // software pipeline over 16-column steps t: the weight fragments of t are
+    // read first, then the offsets of t+2 and the gather of t+1 are issued,
+    // and the MFMAs of t run while those reads are in flight
+    bf16x8 b0[TN], b1[TN], af[TM];
+    Offs o1 = offsets(0);
+    gather(0, o1, b0);
+    o1 = offsets(16);
+    for (int s = 0; s < nsl; ++s) {
+        if (s + 1 < nsl) store_a((s + 1) & 1);
+        if (s + 2 < nsl) load_a(s + 2);
+        const uint16_t *A = sA + (s & 1) * BNB * kPatchRowA;
+        const int k0 = s * kPatchSlice;
+        afrag(A, 0, af);
+        Offs o2 = offsets(k0 + 32);
+        gather(k0 + 16, o1, b1);
+        mma(af, b0);
+        afrag(A, 16, af);
+        o1 = offsets(k0 + 48);
+        gather(k0 + 32, o2, b0);
+        mma(af, b1);
+        __syncthreads();
+    }
+
+    // epilogue: accumulator (i, j, r): m = i*32 + (r/4)*8 + (lane/32)*4 + r%4,
+    // px = wave*32*TN + j*32 + lane%32; staged through LDS as [px][m]
+    uint16_t *sC = reinterpret_cast<uint16_t *>(smem);  // [BMB][BNB + 8]
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int r4 = 0; r4 < 4; ++r4) {
+                const int ml = i * 32 + r4 * 8 + (lane >> 5) * 4;
+                const int pl = wave * 32 * TN + j * 32 + (lane & 31);
+                const uint32_t lo = (uint32_t)f32_to_bf16_bits(acc[i][j][r4 * 4 + 0]) |
+                                    ((uint32_t)f32_to_bf16_bits(acc[i][j][r4 * 4 + 1]) << 16);
+                const uint32_t hi = (uint32_t)f32_to_bf16_bits(acc[i][j][r4 * 4 + 2]) |
+                                    ((uint32_t)f32_to_bf16_bits(acc[i][j][r4 * 4 + 3]) << 16);
+                *reinterpret_cast<uint2 *>(&sC[pl * (BNB + 8) + ml]) = make_uint2(lo, hi);
+            }
+    __syncthreads();
+    const bool vec_out = (a.Cy % 8 == 0) && ((G.o_off + m0) % 8 == 0) && ((uintptr_t)a.Y % 16 == 0);
+    constexpr int CPR = BNB / 8;
+    for (int c = tid; c < BMB * CPR; c += NT) {
+        const int pl = c / CPR, mc = c - pl * CPR;
+        const int px = n0 + pl, m = m0 + mc * 8;
+        if (px >= a.NPQ || m >= G.M) continue;
+        uint16_t *dst = a.Y + (int64_t)px * a.Cy + G.o_off + m;
+        const uint16_t *srcp = &sC[pl * (BNB + 8) + mc * 8];
+        if (vec_out && m + 8 <= G.M) {
+            *reinterpret_cast<uint4 *>(dst) = *reinterpret_cast<const uint4 *>(srcp);
+        } else {
+            for (int e = 0; e < 8 && m + e < G.M; ++e) dst[e] = srcp[e];
+        }
+    }
+}
+
 // ---------------------------------------------------------------- host side
 template <int BM, int BN, int WN, int WM>
 int launch_conv(ConvArgs a, hipStream_t stream) {
@@ -511,8 +809,50 @@ int gather_group(GatherArgs g, int ch_span, hipStream_t stream) {
     return check_hip(hipGetLastError(), "k_im2col_global");
 }
 
-// Validates the descriptor (beyond validate_conv) and returns the scratch size.
-int conv_plan(const sa_conv_desc &d, size_t *ws_need) {
+// ---------------------------------------------------------------- planning
+enum GroupPath { kSkip, kDirect, kPatch, kGather };
+
+template <int TM, int TN>
+int launch_patch(PatchArgs a, int lds, hipStream_t stream) {
+    using Cfg = PatchCfg<TM, TN>;
+    const int ntiles = (a.NPQ + Cfg::BMB - 1) / Cfg::BMB;
+    int begin = 0;
+    for (int i = 0; i < a.ngroups; ++i) {
+        a.g[i].mtiles = (a.g[i].M + Cfg::BNB - 1) / Cfg::BNB;
+        a.g[i].begin = begin;
+        begin += a.g[i].mtiles * ntiles;
+    }
+    a.nblocks = begin;
+    auto kern = k_conv_patch<TM, TN>;
+    if (int rc = check_hip(hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
+                                               hipFuncAttributeMaxDynamicSharedMemorySize, lds),
+                           "conv: set LDS size"))
+        return rc;
+    hipLaunchKernelGGL(kern, dim3(a.nblocks), dim3(Cfg::NT), (size_t)lds, stream, a);
+    return check_hip(hipGetLastError(), "k_conv_patch");
+}
+
+struct ConvPlan {
+    int P, Q, NPQ, Cy;
+    int path[SA_MAX_CONV_GROUPS];
+    int pix_bytes[SA_MAX_CONV_GROUPS], nch[SA_MAX_CONV_GROUPS], ch_lo8[SA_MAX_CONV_GROUPS];
+    int TM, TN, patch_bytes, tab_bytes, lds;  // k_conv_patch launch (when any group takes it)
+    size_t ws_need;                           // scratch of the two-phase groups
+};
+
+constexpr int kPatchTMs[4] = {4, 3, 2, 1};
+
+int patch_lds(int TM, int TN, int patch_bytes, int tab_bytes) {
+    const int a_bytes = 2 * 32 * TM * kPatchRowA * 2;
+    const int c_bytes = 128 * TN * (32 * TM + 8) * 2;
+    return std::max(patch_bytes + tab_bytes + a_bytes, c_bytes);
+}
+
+// Validates the descriptor (beyond validate_conv) and chooses, per conv group,
+// the direct kernel (columns are every tap of one run of channels), the
+// LDS-footprint kernel, or the two-phase gather when the footprint of even the
+// smallest pixel tile does not fit in LDS.
+int conv_plan(const sa_conv_desc &d, ConvPlan *pl) {
     if (int rc = validate_conv(d)) return rc;
     const sa_compact_sizes &s = *d.sizes;
     const int64_t P = ((int64_t)d.H + 2 * d.pad - d.C) / d.stride + 1;
@@ -521,7 +861,12 @@ int conv_plan(const sa_conv_desc &d, size_t *ws_need) {
     if (d.Cx > 65535) return fail(SA_E_UNSUPPORTED, "conv: Cx > 65535");
     if ((int64_t)d.N * d.H * d.W * d.Cx * 2 >= (int64_t(1) << 31))
         return fail(SA_E_UNSUPPORTED, "conv: input of 2 GiB or more");
-    size_t need = 0;
+    ConvPlan &p = *pl;
+    memset(&p, 0, sizeof p);
+    p.P = (int)P;
+    p.Q = (int)Q;
+    p.NPQ = (int)NPQ;
+    int max_ldk = 0, ngath = 0;
     for (int g = 0; g < s.groups; ++g) {
         if (s.ldk[g] != (s.K[g] + kBK - 1) / kBK * kBK || s.wc_offset[g] % 8 != 0)
             return fail(SA_E_ARG, "conv: sizes->ldk / wc_offset of group %d are not those of structadmm_compact", g);
@@ -529,14 +874,83 @@ int conv_plan(const sa_conv_desc &d, size_t *ws_need) {
             return fail(SA_E_UNSUPPORTED, "conv: compacted matrix of group %d of 2 GiB or more", g);
         if (s.K[g] > 0 && (s.ch_lo[g] < 0 || s.ch_span[g] <= 0 || s.ch_lo[g] + s.ch_span[g] > d.Cx))
             return fail(SA_E_ARG, "conv: channel span of group %d outside the input's %d channels", g, d.Cx);
-        if (s.M[g] > 0 && !is_vec(s, g, d.Cx)) {
-            const int64_t bytes = NPQ * s.ldk[g] * 2;
-            if (bytes >= (int64_t(1) << 31))
-                return fail(SA_E_UNSUPPORTED, "conv: gathered rows of group %d need 2 GiB or more", g);
-            need += ((size_t)bytes + 255) / 256 * 256;  // each gathered group has its own rows
+        p.Cy += s.M[g];
+        if (s.M[g] == 0) {
+            p.path[g] = kSkip;  // no output channels in this group
+        } else if (is_vec(s, g, d.Cx)) {
+            p.path[g] = kDirect;
+        } else {
+            // the LDS copy is filled with 16-byte loads of 8 channels from an
+            // 8-aligned channel window; inputs whose pixels are not a whole
+            // number of such chunks (few input channels) gather their rows in a
+            // separate pass instead
+            p.path[g] = d.Cx % 8 == 0 ? kPatch : kGather;
+            if (p.path[g] == kGather) continue;
+            const int lo = s.K[g] > 0 ? s.ch_lo[g] : 0;
+            const int hi = s.K[g] > 0 ? s.ch_lo[g] + s.ch_span[g] : 1;
+            p.ch_lo8[g] = lo / 8 * 8;
+            p.nch[g] = (hi - p.ch_lo8[g] + 7) / 8;
+            // 16 bytes per chunk plus one word: an odd number of words per pixel,
+            // so the lanes of an output row hit distinct banks
+            const int bytes = p.nch[g] * 16 + 4;
+            p.pix_bytes[g] = bytes;
+            max_ldk = std::max(max_ldk, s.ldk[g]);
+            ++ngath;
         }
     }
-    *ws_need = need;
+    if (ngath > 0) {
+        // tile shape: least padded filter work, then the larger tile
+        int best_tm = 4;
+        int64_t best_cost = -1;
+        for (int tm : kPatchTMs) {
+            int64_t cost = 0;
+            for (int g = 0; g < s.groups; ++g)
+                if (p.path[g] == kPatch) cost += (s.M[g] + 32 * tm - 1) / (32 * tm) * (32 * tm);
+            if (best_cost < 0 || cost < best_cost) best_cost = cost, best_tm = tm;
+        }
+        const int Hp = d.H + 2 * d.pad, Wp = d.W + 2 * d.pad;
+        const int Ws = (Wp + d.stride - 1) / d.stride, Wpp = Ws * d.stride;
+        p.TM = best_tm;
+        p.tab_bytes = ((max_ldk + 2 * kPatchSlice) * 4 + 15) / 16 * 16;  // two slices past the last
+        auto fits = [&](int tn, int *patch_bytes) {
+            const int rows = patch_rows(p.NPQ, p.P, p.Q, Hp, d.stride, d.C, 128 * tn);
+            int64_t pb = 0;
+            for (int g = 0; g < s.groups; ++g)
+                if (p.path[g] == kPatch) pb = std::max<int64_t>(pb, ((int64_t)rows * Wpp * p.pix_bytes[g] + 15) / 16 * 16);
+            if (pb > kLdsBytes) return false;
+            *patch_bytes = (int)pb;
+            return patch_lds(p.TM, tn, (int)pb, p.tab_bytes) <= kLdsBytes;
+        };
+        int64_t mt = 0;
+        for (int g = 0; g < s.groups; ++g)
+            if (p.path[g] == kPatch) mt += (s.M[g] + 32 * p.TM - 1) / (32 * p.TM);
+        int pb2 = 0, pb1 = 0;
+        const bool f2 = fits(2, &pb2), f1 = fits(1, &pb1);
+        // two pixel fragments per wavefront halve the weight reads per MFMA, as
+        // long as the launch still has two tiles per compute unit
+        if (f2 && (!f1 || mt * ((p.NPQ + 255) / 256) >= 512)) {
+            p.TN = 2;
+            p.patch_bytes = pb2;
+        } else if (f1) {
+            p.TN = 1;
+            p.patch_bytes = pb1;
+        } else {
+            p.TN = 0;
+        }
+        if (p.TN > 0) {
+            p.lds = patch_lds(p.TM, p.TN, p.patch_bytes, p.tab_bytes);
+        } else {
+            for (int g = 0; g < s.groups; ++g)
+                if (p.path[g] == kPatch) p.path[g] = kGather;
+        }
+    }
+    for (int g = 0; g < s.groups; ++g) {
+        if (p.path[g] != kGather) continue;
+        const int64_t bytes = NPQ * s.ldk[g] * 2;
+        if (bytes >= (int64_t(1) << 31))
+            return fail(SA_E_UNSUPPORTED, "conv: gathered rows of group %d need 2 GiB or more", g);
+        p.ws_need += ((size_t)bytes + 255) / 256 * 256;  // each gathered group has its own rows
+    }
     return SA_OK;
 }
 
@@ -547,41 +961,41 @@ using namespace sa;
 
 extern "C" size_t structadmm_conv_workspace(const sa_conv_desc *desc) {
     if (!desc) return 0;
-    size_t need = 0;
-    if (conv_plan(*desc, &need) != SA_OK) {
+    ConvPlan p;
+    if (conv_plan(*desc, &p) != SA_OK) {
         clear_error();
         return 0;
     }
-    return need;
+    return p.ws_need;
 }
 
 extern "C" int structadmm_conv_fwd(const sa_conv_desc *desc, hipStream_t stream) {
     clear_error();
     if (!desc) return fail(SA_E_ARG, "conv: desc is required");
     const sa_conv_desc &d = *desc;
-    size_t need = 0;
-    if (int rc = conv_plan(d, &need)) return rc;
-    if (need > 0) {
-        if (!d.ws || d.ws_bytes < need)
-            return fail(SA_E_WORKSPACE, "conv: scratch of %zu bytes required (%zu given)", need, d.ws ? d.ws_bytes : 0);
+    ConvPlan p;
+    if (int rc = conv_plan(d, &p)) return rc;
+    if (p.ws_need > 0) {
+        if (!d.ws || d.ws_bytes < p.ws_need)
+            return fail(SA_E_WORKSPACE, "conv: scratch of %zu bytes required (%zu given)", p.ws_need,
+                        d.ws ? d.ws_bytes : 0);
         if (!aligned(d.ws, 256)) return fail(SA_E_ALIGN, "conv: scratch must be 256-byte aligned");
     }
     const sa_compact_sizes &s = *d.sizes;
-    const int P = (d.H + 2 * d.pad - d.C) / d.stride + 1;
-    const int Q = (d.W + 2 * d.pad - d.D) / d.stride + 1;
-    const int NPQ = d.N * P * Q;
+    const int P = p.P, Q = p.Q, NPQ = p.NPQ;
     const uint32_t x_bytes = (uint32_t)((int64_t)d.N * d.H * d.W * d.Cx * 2);
-    int Cy = 0;
-    for (int g = 0; g < s.groups; ++g) Cy += s.M[g];
 
-    // groups read straight from the NHWC input share one launch; groups with
-    // arbitrary columns are gathered first and share a second, 1x1 launch
+    // groups read straight from the NHWC input share one launch, groups with
+    // arbitrary columns a second (LDS footprint) and, when their footprint is
+    // too large, a gather pass plus a third, 1x1 launch
     ConvArgs direct, gathered;
+    PatchArgs pa;
     memset(&direct, 0, sizeof direct);
     memset(&gathered, 0, sizeof gathered);
-    direct.Y = gathered.Y = d.Y;
-    direct.Cy = gathered.Cy = Cy;
-    direct.NPQ = gathered.NPQ = NPQ;
+    memset(&pa, 0, sizeof pa);
+    direct.Y = gathered.Y = pa.Y = d.Y;
+    direct.Cy = gathered.Cy = pa.Cy = p.Cy;
+    direct.NPQ = gathered.NPQ = pa.NPQ = NPQ;
     direct.H = d.H;
     direct.W = d.W;
     direct.D = d.D;
@@ -591,10 +1005,49 @@ extern "C" int structadmm_conv_fwd(const sa_conv_desc *desc, hipStream_t stream)
     direct.Q = Q;
     gathered.H = gathered.W = gathered.D = gathered.stride = gathered.P = gathered.Q = 1;
     gathered.pad = 0;
+    pa.X = d.X;
+    pa.x_bytes = x_bytes;
+    pa.N = d.N;
+    pa.H = d.H;
+    pa.W = d.W;
+    pa.Cx = d.Cx;
+    pa.C = d.C;
+    pa.D = d.D;
+    pa.stride = d.stride;
+    pa.pad = d.pad;
+    pa.P = P;
+    pa.Q = Q;
+    pa.Hp = d.H + 2 * d.pad;
+    pa.Wp = d.W + 2 * d.pad;
+    pa.Ws = (d.W + 2 * d.pad + d.stride - 1) / d.stride;
+    pa.Wpp = pa.Ws * d.stride;
+    pa.patch_bytes = p.patch_bytes;
+    pa.tab_bytes = p.tab_bytes;
+    pa.divQ = make_fastdiv((uint32_t)Q);
+    pa.divP = make_fastdiv((uint32_t)P);
+    pa.divHp = make_fastdiv((uint32_t)pa.Hp);
+    pa.divD = make_fastdiv((uint32_t)d.D);
+    pa.divS = make_fastdiv((uint32_t)d.stride);
     size_t ws_off = 0;
     for (int g = 0; g < s.groups; ++g) {
-        if (s.M[g] == 0) continue;  // no output channels in this group
-        const bool vec = is_vec(s, g, d.Cx);
+        if (p.path[g] == kSkip) continue;
+        if (p.path[g] == kPatch) {
+            PatchGroup &G = pa.g[pa.ngroups++];
+            G.Wc = d.Wc + s.wc_offset[g];
+            G.col_ch = d.col_ch + s.col_offset[g];
+            G.col_tap = d.col_tap + s.col_offset[g];
+            G.M = s.M[g];
+            G.K = s.K[g];
+            G.ldk = s.ldk[g];
+            G.o_off = s.row_offset[g];
+            G.ch_lo = p.ch_lo8[g];
+            G.nch = p.nch[g];
+            G.pix_bytes = p.pix_bytes[g];
+            G.divNch = make_fastdiv((uint32_t)G.nch);
+            G.divRow = make_fastdiv((uint32_t)(pa.Wp * G.nch));
+            continue;
+        }
+        const bool vec = p.path[g] == kDirect;
         ConvArgs &a = vec ? direct : gathered;
         ConvGroup &G = a.g[a.ngroups++];
         G.Wc = d.Wc + s.wc_offset[g];
@@ -646,5 +1099,20 @@ extern "C" int structadmm_conv_fwd(const sa_conv_desc *desc, hipStream_t stream)
         G.run_base = 0;
     }
     if (int rc = run_conv(direct, stream)) return rc;
+    if (pa.ngroups > 0) {
+        int rc = SA_OK;
+        switch (p.TM * 10 + p.TN) {
+            case 41: rc = launch_patch<4, 1>(pa, p.lds, stream); break;
+            case 42: rc = launch_patch<4, 2>(pa, p.lds, stream); break;
+            case 31: rc = launch_patch<3, 1>(pa, p.lds, stream); break;
+            case 32: rc = launch_patch<3, 2>(pa, p.lds, stream); break;
+            case 21: rc = launch_patch<2, 1>(pa, p.lds, stream); break;
+            case 22: rc = launch_patch<2, 2>(pa, p.lds, stream); break;
+            case 11: rc = launch_patch<1, 1>(pa, p.lds, stream); break;
+            case 12: rc = launch_patch<1, 2>(pa, p.lds, stream); break;
+            default: return fail(SA_E_ARG, "conv: no tile shape for the gathered groups");
+        }
+        if (rc) return rc;
+    }
     return run_conv(gathered, stream);
 }

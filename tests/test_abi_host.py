@@ -165,17 +165,27 @@ def test_compact_and_conv_validation():
     s.run[0] = 0
     s.ldk[0] = 18  # not the padded stride that compaction produces
     assert conv() == -1
-    # a gathered group (run 0) needs scratch for its compacted im2col rows
+    # arbitrary columns over 8-aligned channels are gathered from an LDS copy of
+    # each tile's input footprint: no scratch
     s.ldk[0] = 64
     s.ch_lo[0], s.ch_span[0] = 0, 2
-    need = L.structadmm_conv_workspace(ctypes.byref(sa.ConvDesc(1, 8, 8, 2, 3, 3, 1, 1, ctypes.pointer(s),
-                                                                FAKE, FAKE, FAKE, FAKE, FAKE, None, 0)))
+    desc = lambda **kw: sa.ConvDesc(**{**dict(N=1, H=8, W=8, Cx=2, C=3, D=3, stride=1, pad=1,
+                                             sizes=ctypes.pointer(s), X=FAKE, Wc=FAKE, col_ch=FAKE,
+                                             col_tap=FAKE, Y=FAKE, ws=None, ws_bytes=0), **kw})
+    assert L.structadmm_conv_workspace(ctypes.byref(desc(Cx=8))) == 0
+    # channels not 8-aligned: the compacted im2col rows go through caller scratch
+    need = L.structadmm_conv_workspace(ctypes.byref(desc()))
     assert need == 8 * 8 * 64 * 2
     assert conv() == -3
     assert conv(ws=FAKE + 2048, ws_bytes=need - 1) == -3
     assert conv(ws=FAKE + 2048 + 16, ws_bytes=need) == -2
     s.ch_span[0] = 3  # channels past the input
     assert conv(ws=FAKE + 2048, ws_bytes=need) == -1
+    assert L.structadmm_conv_workspace(ctypes.byref(desc())) == 0
+    # so do footprints too wide for LDS
+    s.ch_span[0] = 16
+    wide = dict(W=4000, Cx=16)
+    assert L.structadmm_conv_workspace(ctypes.byref(desc(**wide))) == 8 * 4000 * 64 * 2
 
 
 def test_pack_validation():

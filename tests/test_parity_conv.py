@@ -53,12 +53,15 @@ def check_compact(gpu, ref):
         assert not np.any(full[off: off + M * ldk].reshape(M, ldk)[:, K:])
 
 
-def conv_case(N, Cin, H, Wd, A, C, D, stride, pad, groups, kind, keep, seed, dense_too=True):
+def conv_case(N, Cin, H, Wd, A, C, D, stride, pad, groups, kind, keep, seed, dense_too=True, dead_lo=0):
     rng = np.random.default_rng(seed)
     B = Cin // groups
     shape = (A, B, C, D)
     W = (0.05 * rng.standard_normal(shape)).astype(np.float32)
     U = (0.01 * rng.standard_normal(shape)).astype(np.float32)
+    # the first dead_lo input channels of every group score 0 and are pruned
+    W[:, :dead_lo] = 0
+    U[:, :dead_lo] = 0
     G = {sa.FILTER: A, sa.CHANNEL: B, sa.SHAPE: B * C * D}[kind]
     k = max(1, int(round(keep * G)))
     # projection on both sides (bit-exact parity is checked elsewhere; here it feeds compaction)
@@ -121,12 +124,25 @@ SMALL = [
     (1, 48, 8, 8, 300, 3, 3, 1, 1, 1, sa.SHAPE, 0.25),
     (5, 8, 7, 9, 16, 3, 2, 1, 0, 1, sa.FILTER, 0.75),
     (1, 256, 6, 6, 40, 3, 3, 1, 1, 2, sa.FILTER, 0.5),
+    (2, 20, 15, 13, 70, 3, 3, 2, 1, 1, sa.SHAPE, 0.3),
+    (2, 6, 23, 23, 34, 5, 5, 3, 2, 2, sa.SHAPE, 0.4),
+    (3, 16, 11, 11, 200, 3, 3, 1, 1, 1, sa.SHAPE, 0.5),
+    (2, 16, 17, 15, 40, 3, 3, 2, 1, 1, sa.SHAPE, 0.4),
+    (2, 24, 23, 23, 36, 5, 5, 3, 2, 3, sa.SHAPE, 0.4),
+    # input rows too wide for an LDS copy of the footprint: two-phase gather
+    (1, 64, 3, 2100, 40, 3, 3, 1, 1, 1, sa.SHAPE, 0.3),
 ]
 
 
 @pytest.mark.parametrize("case", SMALL, ids=[f"c{i}" for i in range(len(SMALL))])
 def test_conv_small(case):
     conv_case(*case, seed=hash(case) % 2**31)
+
+
+def test_conv_unaligned_channel_window():
+    # kept columns start at channel 3 (of 32 per group): the LDS copy starts at
+    # the 8-aligned channel below
+    assert conv_case(2, 64, 13, 13, 48, 3, 3, 1, 1, 2, sa.SHAPE, 0.3, seed=7, dead_lo=3) <= TOL
 
 
 def test_compact_chain_input_positions():
