@@ -8,14 +8,17 @@ the paper's AlexNet shapes; no dataset, no trained weights).
 One step = one pass of the whole path over one batch:
   1. structadmm_project     fused Z-update + dual update + regulariser gradient, 5 layers in one call
   2. structadmm_dual_update per-SGD-step gradient rho (W - Z + U) of the 5 layers
-  3. per layer: structadmm_compact (pruned and dense matrices), structadmm_pack_nhwc,
-     structadmm_conv_fwd over the compacted matrix and over the dense one
+  3. per layer: structadmm_compact (pruned and dense matrices) and structadmm_pack_nhwc
+  4. structadmm_conv_fwd of every layer over its compacted matrix, then over the dense one
 Inputs are resident in HBM before the timed region.
 
 Output: one JSON line.  value = compacted-CONV TFLOP/s over the step's five
 compacted convolutions (algorithmic flops 2*N*P*Q*sum_g M_g*K_g / their
 HIP-event time); speedup_vs_dense = dense CONV time / compacted CONV time;
-admm_gbps = algorithmic bytes of steps 1-2 / their time.
+admm_gbps = algorithmic bytes of steps 1-2 / their time.  Each CONV is bracketed
+by HIP events on the stream it runs on; the CONVs are enqueued back to back
+(the compactions, which return sizes to the host, come first), so the events
+measure the kernels rather than host gaps.
 """
 from __future__ import annotations
 
@@ -99,14 +102,17 @@ def run_step(torch, sa, wl, layers, ws, cws, ev, record):
     sa.project([o.proj for o in layers], ws, descs=ev["pdescs"])
     sa.dual_update(None, descs=ev["ddescs"])
     mark("admm1")
+    # compaction synchronises with the host (it returns the sizes), so every
+    # layer is compacted first and the CONVs are then enqueued back to back
+    comp = []
     for i, o in enumerate(layers):
         L = o.cfg
         cols = o.mask if o.kind == sa.SHAPE else None
         rows = o.mask if o.kind == sa.FILTER else None
-        Wc, ri, cc, ct, sizes = sa.compact(o.Z, L.groups, row_mask=rows, col_mask=cols, ws=cws,
-                                           out=o.comp_out)
-        Wd, rid, ccd, ctd, sized = sa.compact(o.Z, L.groups, ws=cws, out=o.dense_out)
+        c = sa.compact(o.Z, L.groups, row_mask=rows, col_mask=cols, ws=cws, out=o.comp_out)
+        d = sa.compact(o.Z, L.groups, ws=cws, out=o.dense_out)
         sa.pack_nhwc(o.X, out=o.Xp)
+        sizes, sized = c[4], d[4]
         if o.Yc is None:
             o.Yc = torch.empty(sa.conv_out_shape(*o.Xp.shape[:3], L.C, L.D, L.stride, L.pad, sizes),
                                dtype=torch.uint16, device="cuda")
@@ -119,11 +125,17 @@ def run_step(torch, sa, wl, layers, ws, cws, ev, record):
                    sa.conv_workspace(o.Xp, sized, L.C, L.D, L.stride, L.pad), 256)
         if o.cvws is None or o.cvws.numel() < need:
             o.cvws = torch.empty(need, dtype=torch.uint8, device="cuda")
+        comp.append((c, d))
+    for i, (o, (c, d)) in enumerate(zip(layers, comp)):
+        L = o.cfg
         mark(f"c{i}a")
-        sa.conv_fwd(o.Xp, Wc, cc, ct, sizes, L.C, L.D, L.stride, L.pad, Y=o.Yc, ws=o.cvws)
+        sa.conv_fwd(o.Xp, c[0], c[2], c[3], c[4], L.C, L.D, L.stride, L.pad, Y=o.Yc, ws=o.cvws)
         mark(f"c{i}b")
-        sa.conv_fwd(o.Xp, Wd, ccd, ctd, sized, L.C, L.D, L.stride, L.pad, Y=o.Yd, ws=o.cvws)
-        mark(f"c{i}c")
+    for i, (o, (c, d)) in enumerate(zip(layers, comp)):
+        L = o.cfg
+        mark(f"d{i}a")
+        sa.conv_fwd(o.Xp, d[0], d[2], d[3], d[4], L.C, L.D, L.stride, L.pad, Y=o.Yd, ws=o.cvws)
+        mark(f"d{i}b")
     return marks
 
 
@@ -205,7 +217,7 @@ def main():
 
     t_admm = sum(span(m, "admm0", "admm1") for m in all_marks) / args.steps
     t_c = [sum(span(m, f"c{i}a", f"c{i}b") for m in all_marks) / args.steps for i in range(len(layers))]
-    t_d = [sum(span(m, f"c{i}b", f"c{i}c") for m in all_marks) / args.steps for i in range(len(layers))]
+    t_d = [sum(span(m, f"d{i}a", f"d{i}b") for m in all_marks) / args.steps for i in range(len(layers))]
     flops_c = sum(o.flops_c for o in layers)
     flops_d = sum(o.flops_d for o in layers)
     n_el = sum(o.cfg.n for o in layers)

@@ -33,6 +33,9 @@
 #include <algorithm>
 #include <cstdint>
 #include <cstring>
+#include <mutex>
+#include <set>
+#include <utility>
 
 #include "sa_device.h"
 #include "sa_host.h"
@@ -710,6 +713,21 @@ __global__ __launch_bounds__(256) void k_conv_patch(PatchArgs a) {
 }
 
 // ---------------------------------------------------------------- host side
+// Raises a kernel's dynamic LDS limit to the full 160 KB, once per device.
+int allow_full_lds(const void *kern) {
+    static std::mutex mu;
+    static std::set<std::pair<const void *, int>> done;
+    int dev = 0;
+    if (int rc = check_hip(hipGetDevice(&dev), "conv: current device")) return rc;
+    std::lock_guard<std::mutex> lock(mu);
+    if (done.count({kern, dev})) return SA_OK;
+    if (int rc = check_hip(hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, kLdsBytes),
+                           "conv: set LDS size"))
+        return rc;
+    done.insert({kern, dev});
+    return SA_OK;
+}
+
 template <int BM, int BN, int WN, int WM>
 int launch_conv(ConvArgs a, hipStream_t stream) {
     using Cfg = ConvCfg<BM, BN, WN, WM>;
@@ -723,10 +741,7 @@ int launch_conv(ConvArgs a, hipStream_t stream) {
     }
     a.nblocks = begin;
     auto kern = k_conv<BM, BN, WN, WM>;
-    if (int rc = check_hip(hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
-                                               hipFuncAttributeMaxDynamicSharedMemorySize, Cfg::lds),
-                           "conv: set LDS size"))
-        return rc;
+    if (int rc = allow_full_lds(reinterpret_cast<const void *>(kern))) return rc;
     hipLaunchKernelGGL(kern, dim3(a.nblocks), dim3(Cfg::NT), Cfg::lds, stream, a);
     return check_hip(hipGetLastError(), "k_conv");
 }
@@ -791,19 +806,13 @@ int gather_group(GatherArgs g, int ch_span, hipStream_t stream) {
         g.divHp = make_fastdiv((uint32_t)g.Hp);
         g.divWpN = make_fastdiv((uint32_t)(g.Wp * g.nch));
         g.divNch = make_fastdiv((uint32_t)g.nch);
-        if (int rc = check_hip(hipFuncSetAttribute(reinterpret_cast<const void *>(k_im2col),
-                                                   hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds),
-                               "conv: set LDS size"))
-            return rc;
+        if (int rc = allow_full_lds(reinterpret_cast<const void *>(k_im2col))) return rc;
         hipLaunchKernelGGL(k_im2col, dim3(blocks), dim3(kGatherThreads), (size_t)lds, stream, g);
         return check_hip(hipGetLastError(), "k_im2col");
     }
     const int64_t chunks = (int64_t)g.NPQ * (g.ldk / 8);
     const size_t tab = (size_t)g.ldk * 4;
-    if (int rc = check_hip(hipFuncSetAttribute(reinterpret_cast<const void *>(k_im2col_global),
-                                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)tab),
-                           "conv: set LDS size"))
-        return rc;
+    if (int rc = allow_full_lds(reinterpret_cast<const void *>(k_im2col_global))) return rc;
     hipLaunchKernelGGL(k_im2col_global, dim3((unsigned)std::min<int64_t>(8192, (chunks + 255) / 256)), dim3(256), tab,
                        stream, g);
     return check_hip(hipGetLastError(), "k_im2col_global");
@@ -824,10 +833,7 @@ int launch_patch(PatchArgs a, int lds, hipStream_t stream) {
     }
     a.nblocks = begin;
     auto kern = k_conv_patch<TM, TN>;
-    if (int rc = check_hip(hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
-                                               hipFuncAttributeMaxDynamicSharedMemorySize, lds),
-                           "conv: set LDS size"))
-        return rc;
+    if (int rc = allow_full_lds(reinterpret_cast<const void *>(kern))) return rc;
     hipLaunchKernelGGL(kern, dim3(a.nblocks), dim3(Cfg::NT), (size_t)lds, stream, a);
     return check_hip(hipGetLastError(), "k_conv_patch");
 }
