@@ -6,8 +6,8 @@
 //   k_expand_allowed  (layers with an input-channel support) per-column support bytes
 //   k_row_scores      filter sets: one wavefront per weight row, O_a in binary64
 //   k_col_partials    channel / shape sets: binary64 column sums per band of rows
-//   k_select          one workgroup per structured layer: final scores, bitonic
-//                     sort of (score bits, index) pairs in LDS, lowest-index
+//   k_select          one workgroup per structured layer: final scores, radix
+//                     select of the k-th largest score bits in LDS, lowest-index
 //                     tie-break, mask + ascending kept_idx, per-column keep bytes
 //   k_elem_*          non-structured sets: 3 histogram passes over |v| bits, then an
 //                     order-preserving count / scan / apply
@@ -27,10 +27,11 @@
 namespace sa {
 namespace {
 
-constexpr int kTab = 16;           // layers per launch (kernel-argument table)
+constexpr int kTab = 32;           // layers per launch (kernel-argument table, < 4 KiB)
 constexpr int kRowThreads = 256;   // 4 wavefronts, one weight row each at a time
 constexpr int kColThreads = 256;
 constexpr int kColBand = 32;       // rows per band of column partial sums
+constexpr int kColSlices = 4;      // row slices of a band (one wavefront each)
 constexpr int kSelThreads = 1024;
 constexpr int kElemThreads = 256;
 constexpr int kElemPerThread = 8;
@@ -121,112 +122,155 @@ __global__ void k_expand_allowed(const uint8_t *__restrict__ in_ch_mask, uint8_t
 __device__ inline float masked(float v, uint8_t keep) { return keep ? v : 0.0f; }
 
 // O_a = sum_j (double)v_aj^2 for each filter a (Section 4, filter-wise set).
+// A wavefront reduces R rows per pass with all their loads issued together:
+// R = 4 when a row has at most 64 float4 (one per lane), 2 up to 128, else 1
+// row looped in slices of 256 float4.
+__device__ inline float4 row_v(const RowLayer &L, const uint8_t *al, int64_t base, int i) {
+    float4 x = *reinterpret_cast<const float4 *>(L.W + base + 4 * (int64_t)i);
+    float4 y = *reinterpret_cast<const float4 *>(L.U + base + 4 * (int64_t)i);
+    float4 v = make_float4(x.x + y.x, x.y + y.y, x.z + y.z, x.w + y.w);
+    if (al) {
+        uchar4 m = reinterpret_cast<const uchar4 *>(al)[i];
+        v.x = masked(v.x, m.x); v.y = masked(v.y, m.y);
+        v.z = masked(v.z, m.z); v.w = masked(v.w, m.w);
+    }
+    return v;
+}
+__device__ inline double sq4(float4 v) {
+    double acc = (double)v.x * (double)v.x;
+    acc += (double)v.y * (double)v.y;
+    acc += (double)v.z * (double)v.z;
+    acc += (double)v.w * (double)v.w;
+    return acc;
+}
+
 __global__ __launch_bounds__(kRowThreads) void k_row_scores(RowTab tab) {
     const int li = find_layer(tab.begin, tab.nl, blockIdx.x);
     const RowLayer &L = tab.L[li];
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const int r0 = (blockIdx.x - tab.begin[li]) * L.rpb;
     const int r1 = min(L.A, r0 + L.rpb);
-    for (int a = r0 + wave; a < r1; a += kRowThreads / kWave) {
-        const int64_t base = (int64_t)a * L.K;
-        const uint8_t *al = L.allowed ? L.allowed + (int64_t)(a / L.Ag) * L.K : nullptr;
-        double acc = 0.0;
-        if (L.vec) {
-            const float4 *w4 = reinterpret_cast<const float4 *>(L.W + base);
-            const float4 *u4 = reinterpret_cast<const float4 *>(L.U + base);
-            const uchar4 *a4 = reinterpret_cast<const uchar4 *>(al);
-            const int K4 = L.K >> 2;
-            for (int i0 = 0; i0 < K4; i0 += 4 * kWave) {
-                float4 x[4], y[4];
-#pragma unroll
-                for (int u = 0; u < 4; ++u) {
-                    int i = i0 + u * kWave + lane;
-                    if (i < K4) {
-                        x[u] = w4[i];
-                        y[u] = u4[i];
-                    } else {
-                        x[u] = make_float4(0.f, 0.f, 0.f, 0.f);
-                        y[u] = x[u];
-                    }
-                }
-#pragma unroll
-                for (int u = 0; u < 4; ++u) {
-                    int i = i0 + u * kWave + lane;
-                    float v0 = x[u].x + y[u].x, v1 = x[u].y + y[u].y;
-                    float v2 = x[u].z + y[u].z, v3 = x[u].w + y[u].w;
-                    if (a4 && i < K4) {
-                        uchar4 m = a4[i];
-                        v0 = masked(v0, m.x); v1 = masked(v1, m.y);
-                        v2 = masked(v2, m.z); v3 = masked(v3, m.w);
-                    }
-                    acc += (double)v0 * (double)v0;
-                    acc += (double)v1 * (double)v1;
-                    acc += (double)v2 * (double)v2;
-                    acc += (double)v3 * (double)v3;
-                }
-            }
-        } else {
+    constexpr int kWaves = kRowThreads / kWave;
+    if (!L.vec) {
+        for (int a = r0 + wave; a < r1; a += kWaves) {
+            const int64_t base = (int64_t)a * L.K;
+            const uint8_t *al = L.allowed ? L.allowed + (int64_t)(a / L.Ag) * L.K : nullptr;
+            double acc = 0.0;
             for (int i = lane; i < L.K; i += kWave) {
                 float v = L.W[base + i] + L.U[base + i];
                 if (al) v = masked(v, al[i]);
                 acc += (double)v * (double)v;
             }
+            acc = wave_sum(acc);
+            if (lane == 0) L.scores[a] = acc;
         }
-        acc = wave_sum(acc);
-        if (lane == 0) L.scores[a] = acc;
+        return;
+    }
+    const int K4 = L.K >> 2;
+    const int R = K4 <= kWave ? 4 : (K4 <= 2 * kWave ? 2 : 1);
+    for (int a0 = r0 + wave * R; a0 < r1; a0 += kWaves * R) {
+        double acc[4] = {0.0, 0.0, 0.0, 0.0};
+        if (R > 1) {
+            // slot u: row a0 + u / (4 / R), float4 lane + 64 * (u % (4 / R))
+            float4 v[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int a = a0 + u / (4 / R), i = lane + kWave * (u % (4 / R));
+                v[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+                if (a < r1 && i < K4) {
+                    const uint8_t *al = L.allowed ? L.allowed + (int64_t)(a / L.Ag) * L.K : nullptr;
+                    v[u] = row_v(L, al, (int64_t)a * L.K, i);
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u) acc[u / (4 / R)] += sq4(v[u]);
+        } else {
+            const uint8_t *al = L.allowed ? L.allowed + (int64_t)(a0 / L.Ag) * L.K : nullptr;
+            const int64_t base = (int64_t)a0 * L.K;
+            for (int i0 = 0; i0 < K4; i0 += 4 * kWave) {
+                float4 v[4];
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    const int i = i0 + u * kWave + lane;
+                    v[u] = i < K4 ? row_v(L, al, base, i) : make_float4(0.f, 0.f, 0.f, 0.f);
+                }
+#pragma unroll
+                for (int u = 0; u < 4; ++u) acc[0] += sq4(v[u]);
+            }
+        }
+        for (int r = 0; r < R; ++r) {
+            const double t = wave_sum(acc[r]);
+            if (lane == 0 && a0 + r < r1) L.scores[a0 + r] = t;
+        }
     }
 }
 
 // partials[band][j] = sum over rows a of the band of (double)v_aj^2
-// (column sums; channel and shape scores are finished in k_select).
+// (column sums; channel and shape scores are finished in k_select).  The four
+// wavefronts of a workgroup take 8-row slices of the 32-row band; the slice
+// sums are added in slice order.
 __global__ __launch_bounds__(kColThreads) void k_col_partials(ColTab tab) {
+    constexpr int kLanes = kColThreads / kColSlices;
+    __shared__ double red[kColSlices - 1][kLanes * 4];
     const int li = find_layer(tab.begin, tab.nl, blockIdx.x);
     const ColLayer &L = tab.L[li];
     const int lb = blockIdx.x - tab.begin[li];
     const int band = lb / L.ctiles, ct = lb - band * L.ctiles;
-    const int a0 = band * kColBand, a1 = min(L.A, a0 + kColBand);
-    if (L.vec) {
-        const int j = (ct * kColThreads + threadIdx.x) * 4;
-        if (j >= L.K) return;
-        double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
-        for (int a = a0; a < a1; ++a) {
-            const int64_t off = (int64_t)a * L.K + j;
-            float4 x = *reinterpret_cast<const float4 *>(L.W + off);
-            float4 y = *reinterpret_cast<const float4 *>(L.U + off);
-            float v0 = x.x + y.x, v1 = x.y + y.y, v2 = x.z + y.z, v3 = x.w + y.w;
-            if (L.allowed) {
-                uchar4 m = *reinterpret_cast<const uchar4 *>(L.allowed + (int64_t)(a / L.Ag) * L.K + j);
-                v0 = masked(v0, m.x); v1 = masked(v1, m.y);
-                v2 = masked(v2, m.z); v3 = masked(v3, m.w);
+    const int lane = threadIdx.x % kLanes, slice = threadIdx.x / kLanes;
+    const int a0 = min(L.A, band * kColBand + slice * (kColBand / kColSlices));
+    const int a1 = min(L.A, a0 + kColBand / kColSlices);
+    const int cw = L.vec ? 4 : 1;  // columns per lane
+    const int j = (ct * kLanes + lane) * cw;
+    double s[4] = {0.0, 0.0, 0.0, 0.0};
+    if (j < L.K) {
+        if (L.vec) {
+            for (int a = a0; a < a1; ++a) {
+                const int64_t off = (int64_t)a * L.K + j;
+                float4 x = *reinterpret_cast<const float4 *>(L.W + off);
+                float4 y = *reinterpret_cast<const float4 *>(L.U + off);
+                float v0 = x.x + y.x, v1 = x.y + y.y, v2 = x.z + y.z, v3 = x.w + y.w;
+                if (L.allowed) {
+                    uchar4 m = *reinterpret_cast<const uchar4 *>(L.allowed + (int64_t)(a / L.Ag) * L.K + j);
+                    v0 = masked(v0, m.x); v1 = masked(v1, m.y);
+                    v2 = masked(v2, m.z); v3 = masked(v3, m.w);
+                }
+                s[0] += (double)v0 * (double)v0;
+                s[1] += (double)v1 * (double)v1;
+                s[2] += (double)v2 * (double)v2;
+                s[3] += (double)v3 * (double)v3;
             }
-            s0 += (double)v0 * (double)v0;
-            s1 += (double)v1 * (double)v1;
-            s2 += (double)v2 * (double)v2;
-            s3 += (double)v3 * (double)v3;
+        } else {
+            for (int a = a0; a < a1; ++a) {
+                const int64_t off = (int64_t)a * L.K + j;
+                float v = L.W[off] + L.U[off];
+                if (L.allowed) v = masked(v, L.allowed[(int64_t)(a / L.Ag) * L.K + j]);
+                s[0] += (double)v * (double)v;
+            }
         }
+    }
+    if (slice > 0)
+        for (int c = 0; c < 4; ++c) red[slice - 1][lane * 4 + c] = s[c];
+    __syncthreads();
+    if (slice == 0 && j < L.K) {
         double *p = L.partials + (int64_t)band * L.K + j;
-        p[0] = s0; p[1] = s1; p[2] = s2; p[3] = s3;
-    } else {
-        const int j = ct * kColThreads + threadIdx.x;
-        if (j >= L.K) return;
-        double s = 0.0;
-        for (int a = a0; a < a1; ++a) {
-            const int64_t off = (int64_t)a * L.K + j;
-            float v = L.W[off] + L.U[off];
-            if (L.allowed) v = masked(v, L.allowed[(int64_t)(a / L.Ag) * L.K + j]);
-            s += (double)v * (double)v;
+        for (int c = 0; c < cw; ++c) {
+            double t = s[c];
+#pragma unroll
+            for (int q = 0; q < kColSlices - 1; ++q) t += red[q][lane * 4 + c];
+            p[c] = t;
         }
-        L.partials[(int64_t)band * L.K + j] = s;
     }
 }
 
 // ---------------------------------------------------------------- select
 // One workgroup per structured layer.  Keeps exactly k groups: the first k
 // of the order (score descending, index ascending), i.e. every group whose
-// score exceeds the k-th largest score plus the lowest-index groups that tie
-// with it.  The (score bits, index) pairs are sorted in LDS by a bitonic
-// network (scores are non-negative binary64, so their bit patterns order
-// like unsigned integers); no atomics, so the result is reproducible.
+// score exceeds the k-th largest score T plus the lowest-index groups that
+// tie with it.  Scores are non-negative binary64, so their bit patterns order
+// like unsigned integers: T is found by an MSB-first radix select over the
+// 64-bit keys (eight 8-bit digits, one LDS histogram per digit), and the ties
+// are ranked by an ordered scan in index order.  Counting is order-free and
+// the scans have a fixed order, so the result is reproducible.
 // s + p[0] + p[stride] + ... + p[(n-1)*stride], added in that order; the
 // loads of each group of 8 are issued together (latency, not bandwidth,
 // bounds this reduction).
@@ -243,75 +287,94 @@ __device__ inline double sum_bands(const double *p, int stride, int n, double s)
     return s;
 }
 
-__device__ inline bool sel_before(uint64_t ka, uint32_t ia, uint64_t kb, uint32_t ib) {
-    return ka > kb || (ka == kb && ia < ib);
-}
-
 __global__ __launch_bounds__(kSelThreads) void k_select(SelTab tab) {
     __shared__ uint64_t skey[SA_MAX_STRUCT_GROUPS];
-    __shared__ uint16_t sidx[SA_MAX_STRUCT_GROUPS];
     __shared__ uint8_t smask[SA_MAX_STRUCT_GROUPS];
+    __shared__ uint32_t hist[256];
     __shared__ uint32_t scan_tmp[kSelThreads / kWave + 1];
+    __shared__ uint64_t s_prefix;
+    __shared__ uint32_t s_need, s_class;
 
     const SelLayer &L = tab.L[blockIdx.x];
-    const int tid = threadIdx.x;
+    const int tid = threadIdx.x, lane = tid & 63;
     const int G = L.G;
-    int Gp = 1;
-    while (Gp < G) Gp <<= 1;
 
-    // 1. final scores (and padding that sorts after every real group)
-    for (int g = tid; g < Gp; g += kSelThreads) {
-        if (g < G) {
-            double s;
-            if (L.kind == SA_FILTER) {
-                s = L.scores[g];
-            } else if (L.kind == SA_SHAPE) {
-                s = sum_bands(L.partials + g, L.K, L.nbands, 0.0);
-            } else {  // channel: over taps, then bands
-                s = 0.0;
-                for (int t = 0; t < L.CD; ++t) s = sum_bands(L.partials + g * L.CD + t, L.K, L.nbands, s);
-            }
-            if (L.kind != SA_FILTER) L.scores[g] = s;
-            skey[g] = (uint64_t)__double_as_longlong(s);
-            sidx[g] = (uint16_t)g;
-        } else {
-            skey[g] = 0;
-            sidx[g] = 0xffffu;
+    // 1. final scores
+    for (int g = tid; g < G; g += kSelThreads) {
+        double s;
+        if (L.kind == SA_FILTER) {
+            s = L.scores[g];
+        } else if (L.kind == SA_SHAPE) {
+            s = sum_bands(L.partials + g, L.K, L.nbands, 0.0);
+        } else {  // channel: over taps, then bands
+            s = 0.0;
+            for (int t = 0; t < L.CD; ++t) s = sum_bands(L.partials + g * L.CD + t, L.K, L.nbands, s);
         }
+        if (L.kind != SA_FILTER) L.scores[g] = s;
+        skey[g] = (uint64_t)__double_as_longlong(s);
         smask[g] = 0;
     }
     __syncthreads();
 
-    // 2. bitonic sort into (score desc, index asc) order
+    // 2. k-th largest key T, and how many of the keys equal to T are kept
+    const int per = (G + kSelThreads - 1) / kSelThreads;
+    const int g0 = min(G, tid * per), g1 = min(G, g0 + per);
     if (L.k > 0 && L.k < G) {
-        for (int size = 2; size <= Gp; size <<= 1) {
-            for (int stride = size >> 1; stride > 0; stride >>= 1) {
-                for (int t = tid; t < (Gp >> 1); t += kSelThreads) {
-                    const int i = 2 * t - (t & (stride - 1));
-                    const int j = i + stride;
-                    const bool up = (i & size) == 0;
-                    const uint64_t ka = skey[i], kb = skey[j];
-                    const uint32_t ia = sidx[i], ib = sidx[j];
-                    const bool swap = up ? sel_before(kb, ib, ka, ia) : sel_before(ka, ia, kb, ib);
-                    if (swap) {
-                        skey[i] = kb;
-                        skey[j] = ka;
-                        sidx[i] = (uint16_t)ib;
-                        sidx[j] = (uint16_t)ia;
+        uint64_t prefix = 0, pmask = 0;
+        uint32_t need = (uint32_t)L.k;  // rank of T among the keys matching prefix
+        for (int shift = 56; shift >= 0; shift -= 8) {
+            if (tid < 256) hist[tid] = 0;
+            __syncthreads();
+            for (int g = tid; g < G; g += kSelThreads) {
+                const uint64_t key = skey[g];
+                if ((key & pmask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
+            }
+            __syncthreads();
+            if (tid < kWave) {
+                // lane l owns digits 255-4l .. 252-4l (descending)
+                uint32_t c[4], tot = 0;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) tot += (c[q] = hist[255 - 4 * lane - q]);
+                const uint32_t incl = wave_incl_scan(tot), excl = incl - tot;
+                if (excl < need && need <= incl) {
+                    uint32_t cum = excl;
+                    for (int q = 0; q < 4; ++q) {
+                        if (cum + c[q] >= need) {
+                            s_prefix = prefix | ((uint64_t)(255 - 4 * lane - q) << shift);
+                            s_need = need - cum;
+                            s_class = c[q];
+                            break;
+                        }
+                        cum += c[q];
                     }
                 }
-                __syncthreads();
             }
+            __syncthreads();
+            prefix = s_prefix;
+            need = s_need;
+            pmask |= (uint64_t)255 << shift;
+            // every key of the class is kept: no finer digit matters (s_* are
+            // rewritten only after the next pass's two barriers)
+            if (s_class == need) break;
         }
-        for (int r = tid; r < L.k; r += kSelThreads) smask[sidx[r]] = 1;
+        // keys whose leading digits exceed the class are kept; keys of the class
+        // (all equal when every digit was resolved) are kept in index order
+        uint32_t ties = 0;
+        for (int g = g0; g < g1; ++g) ties += (skey[g] & pmask) == prefix;
+        uint32_t total;
+        uint32_t rank = block_excl_scan(ties, scan_tmp, &total);
+        for (int g = g0; g < g1; ++g) {
+            const uint64_t key = skey[g] & pmask;
+            uint8_t keep = key > prefix;
+            if (key == prefix) keep = rank++ < need;
+            smask[g] = keep;
+        }
     } else if (L.k == G) {
         for (int g = tid; g < G; g += kSelThreads) smask[g] = 1;
     }
     __syncthreads();
 
     // 3. mask and ascending kept list (ordered workgroup scan)
-    const int per = (G + kSelThreads - 1) / kSelThreads;
-    const int g0 = min(G, tid * per), g1 = min(G, g0 + per);
     uint32_t kept_local = 0;
     for (int g = g0; g < g1; ++g) kept_local += smask[g];
     uint32_t total;
@@ -356,6 +419,10 @@ struct ApplyTab {
     int32_t begin[kTab + 1];
     int32_t nl;
 };
+
+static_assert(sizeof(RowTab) < 4096 && sizeof(ColTab) < 4096 && sizeof(SelTab) < 4096 &&
+                  sizeof(DualTab) < 4096 && sizeof(ApplyTab) < 4096,
+              "layer tables must fit the kernel-argument segment");
 
 constexpr int kApplyThreads = 256;
 constexpr int kApplyVec = 4;  // float4 per thread
@@ -743,7 +810,7 @@ void plan_layer(const sa_project_desc &d, size_t start, LayerPlan &p) {
     int rpb = (int)std::max<int64_t>(4, std::min<int64_t>(64, 16384 / std::max(1, p.K)));
     p.rpb = rpb / 4 * 4;
     p.nbands = (int)((d.A + kColBand - 1) / kColBand);
-    const int cols_per_block = p.vec ? kColThreads * 4 : kColThreads;
+    const int cols_per_block = (kColThreads / kColSlices) * (p.vec ? 4 : 1);
     p.ctiles = (p.K + cols_per_block - 1) / cols_per_block;
     const int64_t n = d.A * d.B * d.C * d.D;
     p.nchunks = (int)((n + kElemChunk - 1) / kElemChunk);
