@@ -3,31 +3,28 @@
 //
 // Per conv group g the GEMM is  Y^T[m, px] = sum_k Wc_g[m, k] * Xcol[px, k]
 // with px = (n, p, q) an output pixel and k a kept (tap, channel) column.
+// structadmm_conv_fwd takes one of three paths per group, all on MFMA
+// v_mfma_f32_32x32x16_bf16 (A = Wc rows, B = output pixels, fp32 accumulate):
 //
-// k_conv (the contraction, MFMA v_mfma_f32_32x32x16_bf16):
-//   - A operand = Wc rows (kept filters), B operand = Xcol rows (output
-//     pixels), fp32 accumulators; the two 64-wide K-slice tiles are staged
-//     through LDS with two buffers: the loads of slice s+2 are issued while
-//     slice s is multiplied, one barrier per slice; LDS rows are padded by
-//     16 bytes so fragment reads spread over the banks;
-//   - global reads are raw buffer loads: 32-bit offsets, and rows past the
-//     end of the compacted matrix read as zero in hardware (no branches);
-//     compacted rows are padded to 64 columns, so no K check on the A side;
-//   - B rows are read as 16-byte vectors of 8 channels straight from the NHWC
-//     input when the group's columns are every tap times one run of input
-//     channels (dense, filter- or channel-pruned layers): Xcol is never
-//     materialised;
-//   - the output tile is staged through LDS and written as 16-byte rows;
-//   - workgroup ids are remapped so that each XCD (8 per MI355X, each with
-//     its own L2) walks a contiguous range of output tiles.
-// k_im2col (filter-shape pruning: arbitrary (tap, channel) columns, or inputs
-// with few channels): writes the compacted Xcol rows [N*P*Q][ldk] to scratch
-// first, then k_conv runs on them as a 1x1 convolution.  Each workgroup copies
-// the input footprint of 64 output pixels (the channels the group reads,
-// zero-padded halo) into LDS and gathers every kept column from there through
-// a per-column byte-offset table, one lane per output pixel (consecutive
-// pixels fall in consecutive LDS banks); k_im2col_global gathers straight
-// from global memory when the footprint does not fit in LDS.
+// k_conv (direct): the group's columns are every tap times one run of 8k
+//   input channels (dense, filter- or channel-pruned layers).  B rows are read
+//   as 16-byte vectors straight from the NHWC input; both operand tiles are
+//   staged through LDS in two buffers of 64 columns (loads of slice s+2 in
+//   flight while slice s is multiplied); raw buffer loads with 32-bit offsets
+//   read rows past the matrix as zero, without branches.
+// k_conv_patch (fused gather): arbitrary (tap, channel) columns over inputs
+//   whose channels are 8-aligned (filter-shape pruning).  Each workgroup copies
+//   the input footprint of its pixels into LDS once and its wavefronts gather
+//   their B fragments from that copy through a per-column offset table.
+// k_im2col / k_im2col_global + k_conv (two-phase): inputs with few channels
+//   or footprints too large for LDS; the compacted im2col rows [N*P*Q][ldk]
+//   go to caller scratch first, then k_conv runs on them as a 1x1 convolution.
+//   k_im2col gathers from an LDS copy of the footprint of 64 output pixels,
+//   k_im2col_global straight from global memory.
+// Every path launches once per layer for all of its conv groups, stages the
+// output tile through LDS for 16-byte stores, and remaps workgroup ids so that
+// each XCD (8 per MI355X, each with its own L2) walks a contiguous range of
+// tiles.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
