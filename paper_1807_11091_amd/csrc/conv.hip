@@ -44,6 +44,7 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef unsigned short u16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kBK = 64;            // K slice per stage (= compacted row padding)
 constexpr int kRow = kBK + 8;      // LDS row of a staged operand tile (bf16 elements)
@@ -236,11 +237,10 @@ __global__ __launch_bounds__(64 * WN * WM) void k_conv(ConvArgs a) {
             for (int r4 = 0; r4 < 4; ++r4) {
                 const int ml = wm * WTM + i * 32 + r4 * 8 + (lane >> 5) * 4;
                 const int pl = wn * WTN + j * 32 + (lane & 31);
-                const uint32_t lo = (uint32_t)f32_to_bf16_bits(acc[i][j][r4 * 4 + 0]) |
-                                    ((uint32_t)f32_to_bf16_bits(acc[i][j][r4 * 4 + 1]) << 16);
-                const uint32_t hi = (uint32_t)f32_to_bf16_bits(acc[i][j][r4 * 4 + 2]) |
-                                    ((uint32_t)f32_to_bf16_bits(acc[i][j][r4 * 4 + 3]) << 16);
-                *reinterpret_cast<uint2 *>(&sC[pl * (BN + 8) + ml]) = make_uint2(lo, hi);
+                bf16x4 o;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) o[e] = (__bf16)acc[i][j][r4 * 4 + e];  // round to nearest even
+                *reinterpret_cast<bf16x4 *>(&sC[pl * (BN + 8) + ml]) = o;
             }
     __syncthreads();
     const bool vec_out = (a.Cy % 8 == 0) && ((G.o_off + m0) % 8 == 0) && ((uintptr_t)a.Y % 16 == 0);
@@ -444,6 +444,7 @@ struct PatchGroup {
     const int32_t *col_ch;   // group base
     const int32_t *col_tap;  // group base
     int32_t M, K, ldk, o_off, ch_lo, nch, pix_bytes, mtiles, begin;
+    int32_t dch, dw, dpr;    // fill item step of one workgroup (256 chunks) in (channel chunk, column, row)
     FastDiv divNch, divRow;  // 16-byte chunks per pixel, chunks per padded input row
 };
 struct PatchArgs {
@@ -529,45 +530,47 @@ __global__ __launch_bounds__(256) void k_conv_patch(PatchArgs a) {
     const int rowchunks = a.Wp * nch;
     const int total = (g1 - g0) * rowchunks;
     const __amdgpu_buffer_rsrc_t xrs = rsrc(a.X, a.x_bytes);
-    // fill item idx = one 16-byte chunk of 8 channels: its LDS destination and
-    // source element (-1 for the zero halo)
-    auto locate = [&](int idx, int *dst, int *src) {
-        const int pr = (int)fdiv((uint32_t)idx, G.divRow);
-        const int rem = idx - pr * rowchunks;
-        const int wpad = (int)fdiv((uint32_t)rem, G.divNch);
-        const int ch = rem - wpad * nch;
-        const int j = (int)fdiv((uint32_t)wpad, a.divS);
-        const int cp = (wpad - j * a.stride) * a.Ws + j;
-        const int gr = g0 + pr;
-        const int img = (int)fdiv((uint32_t)gr, a.divHp);
-        const int h = gr - img * a.Hp - a.pad, w = wpad - a.pad;
-        const bool in = img < a.N && (unsigned)h < (unsigned)a.H && (unsigned)w < (unsigned)a.W;
-        const int pos = ((img * a.H + h) * a.W + w) * a.Cx + G.ch_lo;  // element index
-        *dst = (pr * a.Wpp + cp) * pixb + ch * 16;
-        *src = in ? pos + ch * 8 : -1;
-    };
-    constexpr int kFill = 16;  // 16-byte loads in flight per thread
-    for (int base = tid; base < total; base += NT * kFill) {
-        uint4 v[kFill];
-        int dst[kFill];
+    {
+        // item tid, then steps of NT items: one carry at most per coordinate
+        int pr = (int)fdiv((uint32_t)tid, G.divRow);
+        const int rem = tid - pr * rowchunks;
+        int wpad = (int)fdiv((uint32_t)rem, G.divNch);
+        int ch = rem - wpad * nch;
+        constexpr int kFill = 16;  // 16-byte loads in flight per thread
+        for (int base = tid; base < total; base += NT * kFill) {
+            uint4 v[kFill];
+            int dst[kFill];
 #pragma unroll
-        for (int u = 0; u < kFill; ++u) {
-            const int idx = base + u * NT;
-            dst[u] = -1;
-            v[u] = make_uint4(0, 0, 0, 0);
-            if (idx >= total) continue;
-            int src;
-            locate(idx, &dst[u], &src);
-            if (src >= 0) v[u] = bload16(xrs, (uint32_t)src * 2u);
-        }
+            for (int u = 0; u < kFill; ++u) {
+                dst[u] = -1;
+                v[u] = make_uint4(0, 0, 0, 0);
+                if (base + u * NT < total) {
+                    const int jw = a.stride == 1 ? wpad : (int)fdiv((uint32_t)wpad, a.divS);
+                    const int cp = (wpad - jw * a.stride) * a.Ws + jw;
+                    const int gr = g0 + pr;
+                    const int img = (int)fdiv((uint32_t)gr, a.divHp);
+                    const int h = gr - img * a.Hp - a.pad, w = wpad - a.pad;
+                    dst[u] = (pr * a.Wpp + cp) * pixb + ch * 16;
+                    if (img < a.N && (unsigned)h < (unsigned)a.H && (unsigned)w < (unsigned)a.W)
+                        v[u] = bload16(xrs, ((((uint32_t)(img * a.H + h) * a.W + w) * a.Cx + G.ch_lo) + ch * 8) * 2u);
+                }
+                ch += G.dch;
+                const int c1 = ch >= nch;
+                ch -= c1 ? nch : 0;
+                wpad += G.dw + c1;
+                const int c2 = wpad >= a.Wp;
+                wpad -= c2 ? a.Wp : 0;
+                pr += G.dpr + c2;
+            }
 #pragma unroll
-        for (int u = 0; u < kFill; ++u) {
-            if (dst[u] < 0) continue;
-            uint32_t *d32 = reinterpret_cast<uint32_t *>(patch + dst[u]);
-            d32[0] = v[u].x;
-            d32[1] = v[u].y;
-            d32[2] = v[u].z;
-            d32[3] = v[u].w;
+            for (int u = 0; u < kFill; ++u) {
+                if (dst[u] < 0) continue;
+                uint32_t *d32 = reinterpret_cast<uint32_t *>(patch + dst[u]);
+                d32[0] = v[u].x;
+                d32[1] = v[u].y;
+                d32[2] = v[u].z;
+                d32[3] = v[u].w;
+            }
         }
     }
     // 2. column table: (kernel row, kernel column, channel) -> byte offset
@@ -686,11 +689,10 @@ __global__ __launch_bounds__(256) void k_conv_patch(PatchArgs a) {
             for (int r4 = 0; r4 < 4; ++r4) {
                 const int ml = i * 32 + r4 * 8 + (lane >> 5) * 4;
                 const int pl = wave * 32 * TN + j * 32 + (lane & 31);
-                const uint32_t lo = (uint32_t)f32_to_bf16_bits(acc[i][j][r4 * 4 + 0]) |
-                                    ((uint32_t)f32_to_bf16_bits(acc[i][j][r4 * 4 + 1]) << 16);
-                const uint32_t hi = (uint32_t)f32_to_bf16_bits(acc[i][j][r4 * 4 + 2]) |
-                                    ((uint32_t)f32_to_bf16_bits(acc[i][j][r4 * 4 + 3]) << 16);
-                *reinterpret_cast<uint2 *>(&sC[pl * (BNB + 8) + ml]) = make_uint2(lo, hi);
+                bf16x4 o;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) o[e] = (__bf16)acc[i][j][r4 * 4 + e];  // round to nearest even
+                *reinterpret_cast<bf16x4 *>(&sC[pl * (BNB + 8) + ml]) = o;
             }
     __syncthreads();
     const bool vec_out = (a.Cy % 8 == 0) && ((G.o_off + m0) % 8 == 0) && ((uintptr_t)a.Y % 16 == 0);
@@ -1048,6 +1050,9 @@ extern "C" int structadmm_conv_fwd(const sa_conv_desc *desc, hipStream_t stream)
             G.pix_bytes = p.pix_bytes[g];
             G.divNch = make_fastdiv((uint32_t)G.nch);
             G.divRow = make_fastdiv((uint32_t)(pa.Wp * G.nch));
+            G.dch = 256 % G.nch;  // k_conv_patch runs 256 threads
+            G.dw = 256 / G.nch % pa.Wp;
+            G.dpr = 256 / G.nch / pa.Wp;
             continue;
         }
         const bool vec = p.path[g] == kDirect;
