@@ -454,7 +454,11 @@ struct PatchArgs {
     int32_t N, H, W, Cx, C, D, stride, pad, P, Q, NPQ, Cy;
     int32_t Hp, Wp, Ws, Wpp;
     int32_t ngroups, nblocks, patch_bytes, tab_bytes;
-    FastDiv divQ, divP, divHp, divD, divS;
+    // space-to-depth input (s2d > 1): X holds s x s blocks of the padded input
+    // as s*s*Cxo channels; column (kh, kw, c) of the compacted matrix reads
+    // tap (kh / s, kw / s), channel ((kh % s) * s + kw % s) * Cxo + c
+    int32_t s2d, Do, Cxo;
+    FastDiv divQ, divP, divHp, divD, divS, divDo, divS2d;
     PatchGroup g[SA_MAX_CONV_GROUPS];
 };
 
@@ -578,9 +582,18 @@ __global__ __launch_bounds__(256) void k_conv_patch(PatchArgs a) {
         int32_t off = 0;  // columns past K: zeroed after the gather
         if (k < G.K) {
             const int t = G.col_tap[k];
-            const int c = (int)fdiv((uint32_t)t, a.divD), d = t - c * a.D;
+            int c, d, ch = G.col_ch[k];
+            if (a.s2d > 1) {
+                const int kh = (int)fdiv((uint32_t)t, a.divDo), kw = t - kh * a.Do;
+                c = (int)fdiv((uint32_t)kh, a.divS2d);
+                d = (int)fdiv((uint32_t)kw, a.divS2d);
+                ch += ((kh - c * a.s2d) * a.s2d + (kw - d * a.s2d)) * a.Cxo;
+            } else {
+                c = (int)fdiv((uint32_t)t, a.divD);
+                d = t - c * a.D;
+            }
             const int dph = (int)fdiv((uint32_t)d, a.divS);
-            off = (c * a.Wpp + (d - dph * a.stride) * a.Ws + dph) * pixb + (G.col_ch[k] - G.ch_lo) * 2;
+            off = (c * a.Wpp + (d - dph * a.stride) * a.Ws + dph) * pixb + (ch - G.ch_lo) * 2;
         }
         tab[k] = off;
     }
@@ -708,6 +721,45 @@ __global__ __launch_bounds__(256) void k_conv_patch(PatchArgs a) {
         } else {
             for (int e = 0; e < 8 && m + e < G.M; ++e) dst[e] = srcp[e];
         }
+    }
+}
+
+// ---------------------------------------------------------------- k_s2d
+// Space-to-depth image of the zero-padded input for strided layers with few
+// channels: Xs[n][i][j][(a*s + b)*Cx + c] = Xpad[n][i*s + a][j*s + b][c].  The
+// strided CONV over X is then a stride-1 CONV over Xs with ceil(C/s) x
+// ceil(D/s) taps and s*s*Cx channels (8-aligned), which k_conv_patch runs.
+struct S2dArgs {
+    const uint16_t *X;
+    uint16_t *Xs;
+    int32_t N, H, W, Cx, s, pad, Hs, Ws, Cs;  // Cs = s*s*Cx
+    int64_t chunks;                           // N*Hs*Ws*Cs / 8
+    FastDiv divCx, divS;
+};
+
+__global__ __launch_bounds__(256) void k_s2d(S2dArgs a) {
+    const int cs8 = a.Cs / 8;
+    for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < a.chunks; e += (int64_t)gridDim.x * 256) {
+        const int64_t pix = e / cs8;  // (n, i, j)
+        const int c0 = (int)(e - pix * cs8) * 8;
+        const int j = (int)(pix % a.Ws);
+        const int64_t ni = pix / a.Ws;
+        const int i = (int)(ni % a.Hs);
+        const int n = (int)(ni / a.Hs);
+        uint16_t v[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            const int cc = c0 + q;
+            const int blk = (int)fdiv((uint32_t)cc, a.divCx), c = cc - blk * a.Cx;
+            const int ra = (int)fdiv((uint32_t)blk, a.divS), rb = blk - ra * a.s;
+            const int h = i * a.s + ra - a.pad, w = j * a.s + rb - a.pad;
+            v[q] = ((unsigned)h < (unsigned)a.H && (unsigned)w < (unsigned)a.W)
+                       ? a.X[(((int64_t)n * a.H + h) * a.W + w) * a.Cx + c]
+                       : (uint16_t)0;
+        }
+        *reinterpret_cast<uint4 *>(a.Xs + e * 8) =
+            make_uint4(v[0] | ((uint32_t)v[1] << 16), v[2] | ((uint32_t)v[3] << 16), v[4] | ((uint32_t)v[5] << 16),
+                       v[6] | ((uint32_t)v[7] << 16));
     }
 }
 
@@ -842,7 +894,11 @@ struct ConvPlan {
     int path[SA_MAX_CONV_GROUPS];
     int pix_bytes[SA_MAX_CONV_GROUPS], nch[SA_MAX_CONV_GROUPS], ch_lo8[SA_MAX_CONV_GROUPS];
     int TM, TN, patch_bytes, tab_bytes, lds;  // k_conv_patch launch (when any group takes it)
-    size_t ws_need;                           // scratch of the two-phase groups
+    // geometry the footprint kernel sees: the input itself, or (s2d > 1) its
+    // space-to-depth image, which then takes the first s2d_bytes of the scratch
+    int s2d, gH, gW, gCx, gC, gD, gs, gpad;
+    size_t s2d_bytes;
+    size_t ws_need;  // scratch: space-to-depth image, then the two-phase groups' rows
 };
 
 constexpr int kPatchTMs[4] = {4, 3, 2, 1};
@@ -871,6 +927,31 @@ int conv_plan(const sa_conv_desc &d, ConvPlan *pl) {
     p.P = (int)P;
     p.Q = (int)Q;
     p.NPQ = (int)NPQ;
+    // a strided layer whose pixels are not whole 16-byte chunks (few input
+    // channels) runs on its space-to-depth image when that one's are
+    const int st = d.stride;
+    p.s2d = (d.Cx % 8 != 0 && st > 1 && (d.Cx * st * st) % 8 == 0) ? st : 1;
+    if (p.s2d > 1) {
+        p.gH = (d.H + 2 * d.pad + st - 1) / st;
+        p.gW = (d.W + 2 * d.pad + st - 1) / st;
+        p.gCx = d.Cx * st * st;
+        p.gC = (d.C + st - 1) / st;
+        p.gD = (d.D + st - 1) / st;
+        p.gs = 1;
+        p.gpad = 0;
+        p.s2d_bytes = (size_t)d.N * p.gH * p.gW * p.gCx * 2;
+        if (p.s2d_bytes >= (size_t(1) << 31)) p.s2d = 1;  // too large for 32-bit offsets: two-phase
+    }
+    if (p.s2d == 1) {
+        p.gH = d.H;
+        p.gW = d.W;
+        p.gCx = d.Cx;
+        p.gC = d.C;
+        p.gD = d.D;
+        p.gs = st;
+        p.gpad = d.pad;
+        p.s2d_bytes = 0;
+    }
     int max_ldk = 0, ngath = 0;
     for (int g = 0; g < s.groups; ++g) {
         if (s.ldk[g] != (s.K[g] + kBK - 1) / kBK * kBK || s.wc_offset[g] % 8 != 0)
@@ -889,12 +970,17 @@ int conv_plan(const sa_conv_desc &d, ConvPlan *pl) {
             // 8-aligned channel window; inputs whose pixels are not a whole
             // number of such chunks (few input channels) gather their rows in a
             // separate pass instead
-            p.path[g] = d.Cx % 8 == 0 ? kPatch : kGather;
+            p.path[g] = p.gCx % 8 == 0 ? kPatch : kGather;
             if (p.path[g] == kGather) continue;
-            const int lo = s.K[g] > 0 ? s.ch_lo[g] : 0;
-            const int hi = s.K[g] > 0 ? s.ch_lo[g] + s.ch_span[g] : 1;
-            p.ch_lo8[g] = lo / 8 * 8;
-            p.nch[g] = (hi - p.ch_lo8[g] + 7) / 8;
+            if (p.s2d > 1) {  // every channel of the space-to-depth pixel
+                p.ch_lo8[g] = 0;
+                p.nch[g] = p.gCx / 8;
+            } else {
+                const int lo = s.K[g] > 0 ? s.ch_lo[g] : 0;
+                const int hi = s.K[g] > 0 ? s.ch_lo[g] + s.ch_span[g] : 1;
+                p.ch_lo8[g] = lo / 8 * 8;
+                p.nch[g] = (hi - p.ch_lo8[g] + 7) / 8;
+            }
             // 16 bytes per chunk plus one word: an odd number of words per pixel,
             // so the lanes of an output row hit distinct banks
             const int bytes = p.nch[g] * 16 + 4;
@@ -913,12 +999,12 @@ int conv_plan(const sa_conv_desc &d, ConvPlan *pl) {
                 if (p.path[g] == kPatch) cost += (s.M[g] + 32 * tm - 1) / (32 * tm) * (32 * tm);
             if (best_cost < 0 || cost < best_cost) best_cost = cost, best_tm = tm;
         }
-        const int Hp = d.H + 2 * d.pad, Wp = d.W + 2 * d.pad;
-        const int Ws = (Wp + d.stride - 1) / d.stride, Wpp = Ws * d.stride;
+        const int Hp = p.gH + 2 * p.gpad, Wp = p.gW + 2 * p.gpad;
+        const int Ws = (Wp + p.gs - 1) / p.gs, Wpp = Ws * p.gs;
         p.TM = best_tm;
         p.tab_bytes = ((max_ldk + 2 * kPatchSlice) * 4 + 15) / 16 * 16;  // two slices past the last
         auto fits = [&](int tn, int *patch_bytes) {
-            const int rows = patch_rows(p.NPQ, p.P, p.Q, Hp, d.stride, d.C, 128 * tn);
+            const int rows = patch_rows(p.NPQ, p.P, p.Q, Hp, p.gs, p.gC, 128 * tn);
             int64_t pb = 0;
             for (int g = 0; g < s.groups; ++g)
                 if (p.path[g] == kPatch) pb = std::max<int64_t>(pb, ((int64_t)rows * Wpp * p.pix_bytes[g] + 15) / 16 * 16);
@@ -949,6 +1035,10 @@ int conv_plan(const sa_conv_desc &d, ConvPlan *pl) {
                 if (p.path[g] == kPatch) p.path[g] = kGather;
         }
     }
+    bool any_patch = false;
+    for (int g = 0; g < s.groups; ++g) any_patch = any_patch || p.path[g] == kPatch;
+    if (!any_patch) p.s2d_bytes = 0;
+    p.ws_need = (p.s2d_bytes + 255) / 256 * 256;
     for (int g = 0; g < s.groups; ++g) {
         if (p.path[g] != kGather) continue;
         const int64_t bytes = NPQ * s.ldk[g] * 2;
@@ -1012,28 +1102,56 @@ extern "C" int structadmm_conv_fwd(const sa_conv_desc *desc, hipStream_t stream)
     gathered.pad = 0;
     pa.X = d.X;
     pa.x_bytes = x_bytes;
+    if (p.s2d_bytes > 0) {  // the footprint kernel reads the space-to-depth image
+        S2dArgs sa2;
+        memset(&sa2, 0, sizeof sa2);
+        sa2.X = d.X;
+        sa2.Xs = static_cast<uint16_t *>(d.ws);
+        sa2.N = d.N;
+        sa2.H = d.H;
+        sa2.W = d.W;
+        sa2.Cx = d.Cx;
+        sa2.s = p.s2d;
+        sa2.pad = d.pad;
+        sa2.Hs = p.gH;
+        sa2.Ws = p.gW;
+        sa2.Cs = p.gCx;
+        sa2.chunks = (int64_t)d.N * p.gH * p.gW * p.gCx / 8;
+        sa2.divCx = make_fastdiv((uint32_t)d.Cx);
+        sa2.divS = make_fastdiv((uint32_t)p.s2d);
+        hipLaunchKernelGGL(k_s2d, dim3((unsigned)std::min<int64_t>(16384, (sa2.chunks + 255) / 256)), dim3(256), 0,
+                           stream, sa2);
+        if (int rc = check_hip(hipGetLastError(), "k_s2d")) return rc;
+        pa.X = sa2.Xs;
+        pa.x_bytes = (uint32_t)p.s2d_bytes;
+    }
     pa.N = d.N;
-    pa.H = d.H;
-    pa.W = d.W;
-    pa.Cx = d.Cx;
-    pa.C = d.C;
-    pa.D = d.D;
-    pa.stride = d.stride;
-    pa.pad = d.pad;
+    pa.H = p.gH;
+    pa.W = p.gW;
+    pa.Cx = p.gCx;
+    pa.C = p.gC;
+    pa.D = p.gD;
+    pa.stride = p.gs;
+    pa.pad = p.gpad;
     pa.P = P;
     pa.Q = Q;
-    pa.Hp = d.H + 2 * d.pad;
-    pa.Wp = d.W + 2 * d.pad;
-    pa.Ws = (d.W + 2 * d.pad + d.stride - 1) / d.stride;
-    pa.Wpp = pa.Ws * d.stride;
+    pa.Hp = p.gH + 2 * p.gpad;
+    pa.Wp = p.gW + 2 * p.gpad;
+    pa.Ws = (pa.Wp + p.gs - 1) / p.gs;
+    pa.Wpp = pa.Ws * p.gs;
     pa.patch_bytes = p.patch_bytes;
     pa.tab_bytes = p.tab_bytes;
+    pa.s2d = p.s2d;
+    pa.Do = d.D;
+    pa.Cxo = d.Cx;
     pa.divQ = make_fastdiv((uint32_t)Q);
     pa.divP = make_fastdiv((uint32_t)P);
     pa.divHp = make_fastdiv((uint32_t)pa.Hp);
-    pa.divD = make_fastdiv((uint32_t)d.D);
-    pa.divS = make_fastdiv((uint32_t)d.stride);
-    size_t ws_off = 0;
+    pa.divD = make_fastdiv((uint32_t)p.gD);
+    pa.divS = make_fastdiv((uint32_t)p.gs);
+    pa.divDo = make_fastdiv((uint32_t)d.D);
+    pa.divS2d = make_fastdiv((uint32_t)p.s2d);
+    size_t ws_off = (p.s2d_bytes + 255) / 256 * 256;
     for (int g = 0; g < s.groups; ++g) {
         if (p.path[g] == kSkip) continue;
         if (p.path[g] == kPatch) {

@@ -129,6 +129,9 @@ SMALL = [
     (3, 16, 11, 11, 200, 3, 3, 1, 1, 1, sa.SHAPE, 0.5),
     (2, 16, 17, 15, 40, 3, 3, 2, 1, 1, sa.SHAPE, 0.4),
     (2, 24, 23, 23, 36, 5, 5, 3, 2, 3, sa.SHAPE, 0.4),
+    # strided, few channels: space-to-depth image of the input, then the footprint kernel
+    (2, 2, 19, 17, 40, 5, 5, 2, 2, 1, sa.SHAPE, 0.4),
+    (2, 4, 16, 16, 24, 3, 3, 2, 1, 2, sa.SHAPE, 0.5),
     # input rows too wide for an LDS copy of the footprint: two-phase gather
     (1, 64, 3, 2100, 40, 3, 3, 1, 1, 1, sa.SHAPE, 0.3),
 ]
