@@ -473,7 +473,7 @@ struct PatchCfg {
 };
 
 template <int TM, int TN>
-__global__ __launch_bounds__(256) void k_conv_patch(PatchArgs a) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k_conv_patch(PatchArgs a) {
     using Cfg = PatchCfg<TM, TN>;
     constexpr int NT = Cfg::NT, BNB = Cfg::BNB, BMB = Cfg::BMB, AR = Cfg::AR;
     constexpr int CPS = kPatchSlice / 8;  // 16-B chunks per weight row of a slice
@@ -733,33 +733,43 @@ struct S2dArgs {
     const uint16_t *X;
     uint16_t *Xs;
     int32_t N, H, W, Cx, s, pad, Hs, Ws, Cs;  // Cs = s*s*Cx
-    int64_t chunks;                           // N*Hs*Ws*Cs / 8
-    FastDiv divCx, divS;
+    int32_t chunks;                           // N*Hs*Ws*Cs / 8 (< 2^27: the image is below 2 GiB)
+    FastDiv divCs8, divWs, divHs, divCx, divS;
 };
 
+// One thread per 8 consecutive channels (16 bytes) of the output image.
 __global__ __launch_bounds__(256) void k_s2d(S2dArgs a) {
     const int cs8 = a.Cs / 8;
-    for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < a.chunks; e += (int64_t)gridDim.x * 256) {
-        const int64_t pix = e / cs8;  // (n, i, j)
-        const int c0 = (int)(e - pix * cs8) * 8;
-        const int j = (int)(pix % a.Ws);
-        const int64_t ni = pix / a.Ws;
-        const int i = (int)(ni % a.Hs);
-        const int n = (int)(ni / a.Hs);
-        uint16_t v[8];
+    for (int e = blockIdx.x * 256 + threadIdx.x; e < a.chunks; e += gridDim.x * 256) {
+        const int pix = (int)fdiv((uint32_t)e, a.divCs8);  // (n, i, j)
+        const int c0 = (e - pix * cs8) * 8;
+        const int ni = (int)fdiv((uint32_t)pix, a.divWs);
+        const int j = pix - ni * a.Ws;
+        const int n = (int)fdiv((uint32_t)ni, a.divHs);
+        const int i = ni - n * a.Hs;
+        // channel c0 = (ra * s + rb) * Cx + c, advanced one channel at a time
+        int blk = (int)fdiv((uint32_t)c0, a.divCx);
+        int c = c0 - blk * a.Cx;
+        int ra = (int)fdiv((uint32_t)blk, a.divS);
+        int rb = blk - ra * a.s;
+        const int64_t img = (int64_t)n * a.H * a.W;
+        uint32_t v[8];
 #pragma unroll
         for (int q = 0; q < 8; ++q) {
-            const int cc = c0 + q;
-            const int blk = (int)fdiv((uint32_t)cc, a.divCx), c = cc - blk * a.Cx;
-            const int ra = (int)fdiv((uint32_t)blk, a.divS), rb = blk - ra * a.s;
             const int h = i * a.s + ra - a.pad, w = j * a.s + rb - a.pad;
             v[q] = ((unsigned)h < (unsigned)a.H && (unsigned)w < (unsigned)a.W)
-                       ? a.X[(((int64_t)n * a.H + h) * a.W + w) * a.Cx + c]
-                       : (uint16_t)0;
+                       ? a.X[(img + (int64_t)h * a.W + w) * a.Cx + c]
+                       : 0u;
+            if (++c == a.Cx) {
+                c = 0;
+                if (++rb == a.s) {
+                    rb = 0;
+                    ++ra;
+                }
+            }
         }
-        *reinterpret_cast<uint4 *>(a.Xs + e * 8) =
-            make_uint4(v[0] | ((uint32_t)v[1] << 16), v[2] | ((uint32_t)v[3] << 16), v[4] | ((uint32_t)v[5] << 16),
-                       v[6] | ((uint32_t)v[7] << 16));
+        *reinterpret_cast<uint4 *>(a.Xs + (int64_t)e * 8) =
+            make_uint4(v[0] | (v[1] << 16), v[2] | (v[3] << 16), v[4] | (v[5] << 16), v[6] | (v[7] << 16));
     }
 }
 
@@ -1116,11 +1126,13 @@ extern "C" int structadmm_conv_fwd(const sa_conv_desc *desc, hipStream_t stream)
         sa2.Hs = p.gH;
         sa2.Ws = p.gW;
         sa2.Cs = p.gCx;
-        sa2.chunks = (int64_t)d.N * p.gH * p.gW * p.gCx / 8;
+        sa2.chunks = (int32_t)(p.s2d_bytes / 16);
+        sa2.divCs8 = make_fastdiv((uint32_t)(p.gCx / 8));
+        sa2.divWs = make_fastdiv((uint32_t)p.gW);
+        sa2.divHs = make_fastdiv((uint32_t)p.gH);
         sa2.divCx = make_fastdiv((uint32_t)d.Cx);
         sa2.divS = make_fastdiv((uint32_t)p.s2d);
-        hipLaunchKernelGGL(k_s2d, dim3((unsigned)std::min<int64_t>(16384, (sa2.chunks + 255) / 256)), dim3(256), 0,
-                           stream, sa2);
+        hipLaunchKernelGGL(k_s2d, dim3((unsigned)std::min(16384, (sa2.chunks + 255) / 256)), dim3(256), 0, stream, sa2);
         if (int rc = check_hip(hipGetLastError(), "k_s2d")) return rc;
         pa.X = sa2.Xs;
         pa.x_bytes = (uint32_t)p.s2d_bytes;
