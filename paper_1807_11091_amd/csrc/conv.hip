@@ -534,68 +534,103 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
     const int rowchunks = a.Wp * nch;
     const int total = (g1 - g0) * rowchunks;
     const __amdgpu_buffer_rsrc_t xrs = rsrc(a.X, a.x_bytes);
-    {
-        // item tid, then steps of NT items: one carry at most per coordinate
-        int pr = (int)fdiv((uint32_t)tid, G.divRow);
-        const int rem = tid - pr * rowchunks;
-        int wpad = (int)fdiv((uint32_t)rem, G.divNch);
-        int ch = rem - wpad * nch;
-        constexpr int kFill = 16;  // 16-byte loads in flight per thread
-        for (int base = tid; base < total; base += NT * kFill) {
-            uint4 v[kFill];
-            int dst[kFill];
+
+    // 2. column table: (kernel row, kernel column, channel) -> byte offset.
+    // Its sources are read before the copy's loads are issued, so both wait
+    // on one memory round trip.
+    const int ntab = (nsl + 2) * kPatchSlice;
+    auto tab_entry = [&](int k, int t, int ch) {
+        int c, d;
+        if (a.s2d > 1) {
+            const int kh = (int)fdiv((uint32_t)t, a.divDo), kw = t - kh * a.Do;
+            c = (int)fdiv((uint32_t)kh, a.divS2d);
+            d = (int)fdiv((uint32_t)kw, a.divS2d);
+            ch += ((kh - c * a.s2d) * a.s2d + (kw - d * a.s2d)) * a.Cxo;
+        } else {
+            c = (int)fdiv((uint32_t)t, a.divD);
+            d = t - c * a.D;
+        }
+        const int dph = (int)fdiv((uint32_t)d, a.divS);
+        tab[k] = (c * a.Wpp + (d - dph * a.stride) * a.Ws + dph) * pixb + (ch - G.ch_lo) * 2;
+    };
+    constexpr int kTabRegs = 4;  // entries per thread held across the copy's loads
+    int ttap[kTabRegs], tch[kTabRegs];
 #pragma unroll
-            for (int u = 0; u < kFill; ++u) {
-                dst[u] = -1;
-                v[u] = make_uint4(0, 0, 0, 0);
-                if (base + u * NT < total) {
-                    const int jw = a.stride == 1 ? wpad : (int)fdiv((uint32_t)wpad, a.divS);
-                    const int cp = (wpad - jw * a.stride) * a.Ws + jw;
-                    const int gr = g0 + pr;
-                    const int img = (int)fdiv((uint32_t)gr, a.divHp);
-                    const int h = gr - img * a.Hp - a.pad, w = wpad - a.pad;
-                    dst[u] = (pr * a.Wpp + cp) * pixb + ch * 16;
-                    if (img < a.N && (unsigned)h < (unsigned)a.H && (unsigned)w < (unsigned)a.W)
-                        v[u] = bload16(xrs, ((((uint32_t)(img * a.H + h) * a.W + w) * a.Cx + G.ch_lo) + ch * 8) * 2u);
-                }
-                ch += G.dch;
-                const int c1 = ch >= nch;
-                ch -= c1 ? nch : 0;
-                wpad += G.dw + c1;
-                const int c2 = wpad >= a.Wp;
-                wpad -= c2 ? a.Wp : 0;
-                pr += G.dpr + c2;
+    for (int q = 0; q < kTabRegs; ++q) {
+        const int k = tid + q * NT;
+        ttap[q] = 0;
+        tch[q] = 0;
+        if (k < G.K) {
+            ttap[q] = G.col_tap[k];
+            tch[q] = G.col_ch[k];
+        }
+    }
+
+    // 1. the copy, in source order (padded row, padded column, chunk): item
+    //    tid, then steps of NT items (one carry at most per coordinate)
+    int pr = (int)fdiv((uint32_t)tid, G.divRow);
+    const int rem = tid - pr * rowchunks;
+    int wpad = (int)fdiv((uint32_t)rem, G.divNch);
+    int ch = rem - wpad * nch;
+    constexpr int kFill = 32;  // 16-byte loads in flight per thread
+    for (int base = tid; base < total; base += NT * kFill) {
+        uint4 v[kFill];
+        int dst[kFill];
+#pragma unroll
+        for (int u = 0; u < kFill; ++u) {
+            dst[u] = -1;
+            v[u] = make_uint4(0, 0, 0, 0);
+            if (base + u * NT < total) {
+                const int jw = a.stride == 1 ? wpad : (int)fdiv((uint32_t)wpad, a.divS);
+                const int cp = (wpad - jw * a.stride) * a.Ws + jw;
+                const int gr = g0 + pr;
+                const int img = (int)fdiv((uint32_t)gr, a.divHp);
+                const int h = gr - img * a.Hp - a.pad, w = wpad - a.pad;
+                dst[u] = (pr * a.Wpp + cp) * pixb + ch * 16;
+                if (img < a.N && (unsigned)h < (unsigned)a.H && (unsigned)w < (unsigned)a.W)
+                    v[u] = bload16(xrs, ((((uint32_t)(img * a.H + h) * a.W + w) * a.Cx + G.ch_lo) + ch * 8) * 2u);
             }
+            ch += G.dch;
+            const int c1 = ch >= nch;
+            ch -= c1 ? nch : 0;
+            wpad += G.dw + c1;
+            const int c2 = wpad >= a.Wp;
+            wpad -= c2 ? a.Wp : 0;
+            pr += G.dpr + c2;
+        }
+        if (base == tid) {  // while the first loads are in flight: the table
 #pragma unroll
-            for (int u = 0; u < kFill; ++u) {
-                if (dst[u] < 0) continue;
-                uint32_t *d32 = reinterpret_cast<uint32_t *>(patch + dst[u]);
-                d32[0] = v[u].x;
-                d32[1] = v[u].y;
-                d32[2] = v[u].z;
-                d32[3] = v[u].w;
+            for (int q = 0; q < kTabRegs; ++q) {
+                const int k = tid + q * NT;
+                if (k < ntab) {
+                    if (k < G.K) tab_entry(k, ttap[q], tch[q]);
+                    else tab[k] = 0;  // columns past K: zeroed after the gather
+                }
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < kFill; ++u) {
+            if (dst[u] < 0) continue;
+            uint32_t *d32 = reinterpret_cast<uint32_t *>(patch + dst[u]);
+            d32[0] = v[u].x;
+            d32[1] = v[u].y;
+            d32[2] = v[u].z;
+            d32[3] = v[u].w;
+        }
+    }
+    if (total <= tid) {  // a thread without copy items still writes its table entries
+#pragma unroll
+        for (int q = 0; q < kTabRegs; ++q) {
+            const int k = tid + q * NT;
+            if (k < ntab) {
+                if (k < G.K) tab_entry(k, ttap[q], tch[q]);
+                else tab[k] = 0;
             }
         }
     }
-    // 2. column table: (kernel row, kernel column, channel) -> byte offset
-    for (int k = tid; k < (nsl + 2) * kPatchSlice; k += NT) {
-        int32_t off = 0;  // columns past K: zeroed after the gather
-        if (k < G.K) {
-            const int t = G.col_tap[k];
-            int c, d, ch = G.col_ch[k];
-            if (a.s2d > 1) {
-                const int kh = (int)fdiv((uint32_t)t, a.divDo), kw = t - kh * a.Do;
-                c = (int)fdiv((uint32_t)kh, a.divS2d);
-                d = (int)fdiv((uint32_t)kw, a.divS2d);
-                ch += ((kh - c * a.s2d) * a.s2d + (kw - d * a.s2d)) * a.Cxo;
-            } else {
-                c = (int)fdiv((uint32_t)t, a.divD);
-                d = t - c * a.D;
-            }
-            const int dph = (int)fdiv((uint32_t)d, a.divS);
-            off = (c * a.Wpp + (d - dph * a.stride) * a.Ws + dph) * pixb + (ch - G.ch_lo) * 2;
-        }
-        tab[k] = off;
+    for (int k = tid + kTabRegs * NT; k < ntab; k += NT) {  // long rows: the rest of the table
+        if (k < G.K) tab_entry(k, G.col_tap[k], G.col_ch[k]);
+        else tab[k] = 0;
     }
     store_a(0);
     if (nsl > 1) load_a(1);
