@@ -8,7 +8,8 @@ the paper's AlexNet shapes; no dataset, no trained weights).
 One step = one pass of the whole path over one batch:
   1. structadmm_project     fused Z-update + dual update + regulariser gradient, 5 layers in one call
   2. structadmm_dual_update per-SGD-step gradient rho (W - Z + U) of the 5 layers
-  3. per layer: structadmm_compact (pruned and dense matrices) and structadmm_pack_nhwc
+  3. per layer: structadmm_compact (pruned and dense matrices), then structadmm_pack_nhwc of
+     every layer's input
   4. structadmm_conv_fwd of every layer over its compacted matrix, then over the dense one
 Inputs are resident in HBM before the timed region.
 
@@ -46,6 +47,8 @@ def parse():
     p.add_argument("--warmup", type=int, default=3)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU time of the oracle sample")
+    p.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
+                   help="only copy MIB MiB device-to-device 5 times (HBM counter calibration) and exit")
     return p.parse_args()
 
 
@@ -111,7 +114,6 @@ def run_step(torch, sa, wl, layers, ws, cws, ev, record):
         rows = o.mask if o.kind == sa.FILTER else None
         c = sa.compact(o.Z, L.groups, row_mask=rows, col_mask=cols, ws=cws, out=o.comp_out)
         d = sa.compact(o.Z, L.groups, ws=cws, out=o.dense_out)
-        sa.pack_nhwc(o.X, out=o.Xp)
         sizes, sized = c[4], d[4]
         if o.Yc is None:
             o.Yc = torch.empty(sa.conv_out_shape(*o.Xp.shape[:3], L.C, L.D, L.stride, L.pad, sizes),
@@ -126,6 +128,10 @@ def run_step(torch, sa, wl, layers, ws, cws, ev, record):
         if o.cvws is None or o.cvws.numel() < need:
             o.cvws = torch.empty(need, dtype=torch.uint8, device="cuda")
         comp.append((c, d))
+    # the packs are enqueued after the last compaction, so the GPU is busy with
+    # them while the host enqueues the first CONV
+    for o in layers:
+        sa.pack_nhwc(o.X, out=o.Xp)
     for i, (o, (c, d)) in enumerate(zip(layers, comp)):
         L = o.cfg
         mark(f"c{i}a")
@@ -181,8 +187,43 @@ def cpu_baseline(wl, seconds):
                       f"{t_admm * 1e3:.0f} ms on one core"}
 
 
+def copy_probe(mib):
+    """A plain copy of known size: the reference the HBM byte counters
+    (FETCH_SIZE, WRITE_SIZE) are scaled by."""
+    import torch
+    n = mib << 20
+    src = torch.ones(n, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes": n, "copies": 5}))
+
+
+def traffic_per_launch():
+    """HBM bytes per k_conv_patch launch from the committed counter summary,
+    if it was taken on the current CONV source (else None)."""
+    import hashlib
+    summ = os.path.join(ROOT, "profiles", "k_conv_patch_alexnet_shape30_traffic.md")
+    src = os.path.join(ROOT, "paper_1807_11091_amd", "csrc", "conv.hip")
+    if not os.path.exists(summ):
+        return None
+    fields = {}
+    for line in open(summ):
+        if line.startswith("- ") and ":" in line:
+            k, v = line[2:].split(":", 1)
+            fields[k.strip()] = v.strip().strip("`")
+    digest = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    if fields.get("conv.hip sha256") != digest or "bytes per launch" not in fields:
+        return None
+    return int(fields["bytes per launch"])
+
+
 def main():
     args = parse()
+    if args.copy_probe:
+        copy_probe(args.copy_probe)
+        return
     if args.gpus != 1:
         print(json.dumps({"error": "this build measures one GPU only; run with --gpus 1"}))
         sys.exit(2)
@@ -257,7 +298,7 @@ def main():
                      "bound": "mfma", "achieved": round(patch_tflops, 2), "peak": BF16_PEAK_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(patch_tflops / BF16_PEAK_TFLOPS, 4),
                      "avg_launch_us": round(patch_ms * 1e3 / len(patch), 2), "launches_per_step": len(patch),
-                     "traffic": None},
+                     "traffic": traffic_per_launch()},
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
