@@ -47,6 +47,9 @@ def parse():
     p.add_argument("--warmup", type=int, default=3)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU time of the oracle sample")
+    p.add_argument("--suite", metavar="JSON", default=None,
+                   help="measure every workload (ADMM one-call and replicated, CONV per layer against "
+                        "MIOpen, density sweep, achievable peaks) and write the report to JSON")
     p.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                    help="only copy MIB MiB device-to-device 5 times (HBM counter calibration) and exit")
     return p.parse_args()
@@ -219,10 +222,185 @@ def traffic_per_launch():
     return int(fields["bytes per launch"])
 
 
+# ---------------------------------------------------------------- suite
+def _time(torch, fn, reps=20, warm=5, trials=5):
+    """Per-call time (ms) of reps back-to-back calls between two HIP events on
+    the current stream (host enqueue overlaps the GPU work); median, min and
+    max over trials."""
+    for _ in range(warm):
+        fn()
+    t = []
+    for _ in range(trials):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        t.append(a.elapsed_time(b) / reps)
+    t.sort()
+    return {"median_ms": t[len(t) // 2], "p10_ms": t[0], "p90_ms": t[-1]}
+
+
+def _admm_layers(torch, sa, wl, variant, copies=1):
+    """Device tensors of every layer (times copies) for one projection call."""
+    from workloads import layer_tensors
+    kind, pct = wl.variants[variant]
+    layers, grads = [], []
+    for _ in range(copies):
+        prev = None
+        for li, L in enumerate(wl.layers):
+            W, U = layer_tensors(wl, li)
+            k = wl.k_for(li, kind, pct)
+            dW = torch.from_numpy(W).cuda()
+            dU = torch.from_numpy(U).cuda()
+            dZ, dG, dG2 = torch.empty_like(dW), torch.empty_like(dW), torch.empty_like(dW)
+            mask = torch.empty(L.n_groups(kind), dtype=torch.uint8, device="cuda")
+            kept = torch.empty(max(k, 1), dtype=torch.int32, device="cuda")
+            inm = prev if wl.chain else None
+            layers.append(sa.ProjectLayer(dW, dU, dZ, mask, kept, kind, k, L.groups, inm, None, wl.rho, dG))
+            grads.append((dW, dZ, dU, wl.rho, dG2, False))
+            prev = mask
+    return layers, grads
+
+
+def suite_admm(torch, sa, wl, variant):
+    n = sum(L.n for L in wl.layers)
+    res = {"n_weights": n, "layers": len(wl.layers)}
+    for label, copies in (("one_call", 1), ("replicated", max(1, min(1024, -(-512_000_000 // (20 * n)))))):
+        if label == "replicated" and copies == 1:
+            res[label] = "one call already moves 512 MB or more"
+            continue
+        layers, grads = _admm_layers(torch, sa, wl, variant, copies)
+        ws = torch.empty(max(256, sa.project_workspace(layers)), dtype=torch.uint8, device="cuda")
+        pd, dd = sa._descs(layers), sa.dual_descs(grads)
+        tp = _time(torch, lambda: sa.project(layers, ws, descs=pd))
+        tg = _time(torch, lambda: sa.dual_update(None, descs=dd))
+        nn = n * copies
+        step = tp["median_ms"] + tg["median_ms"]
+        res[label] = {"copies": copies,
+                      "project_us": round(tp["median_ms"] * 1e3, 2), "project_GBps": round(20 * nn / tp["median_ms"] / 1e6, 1),
+                      "gradient_us": round(tg["median_ms"] * 1e3, 2), "gradient_GBps": round(16 * nn / tg["median_ms"] / 1e6, 1),
+                      "step_us": round(step * 1e3, 2), "step_GBps": round(36 * nn / step / 1e6, 1),
+                      "step_frac_of_8TBps": round(36 * nn / step / 1e6 / HBM_PEAK_GBS, 4),
+                      "project_min_max_us": [round(tp["p10_ms"] * 1e3, 2), round(tp["p90_ms"] * 1e3, 2)]}
+        del layers, grads, ws
+        torch.cuda.empty_cache()
+    return res
+
+
+def suite_conv(torch, sa, wl, variant, layer_ids=None):
+    """Per layer: compacted and dense CONV with this library, dense bf16 CONV of MIOpen (torch)."""
+    import torch.nn.functional as F
+    from workloads import input_nchw, layer_tensors
+    kind, pct = wl.variants[variant]
+    out, prev = [], None
+    ids = range(len(wl.layers)) if layer_ids is None else layer_ids
+    for li in ids:
+        L = wl.layers[li]
+        W, U = layer_tensors(wl, li)
+        k = wl.k_for(li, kind, pct)
+        dW, dU = torch.from_numpy(W).cuda(), torch.from_numpy(U).cuda()
+        dZ = torch.empty_like(dW)
+        mask = torch.empty(L.n_groups(kind), dtype=torch.uint8, device="cuda")
+        kept = torch.empty(max(k, 1), dtype=torch.int32, device="cuda")
+        inm = prev if wl.chain else None
+        lay = sa.ProjectLayer(dW, dU, dZ, mask, kept, kind, k, L.groups, inm)
+        ws = torch.empty(max(256, sa.project_workspace([lay])), dtype=torch.uint8, device="cuda")
+        sa.project([lay], ws)
+        rows = mask if kind == sa.FILTER else None
+        cols = mask if kind == sa.SHAPE else None
+        Wc, ri, cc, ct, sz = sa.compact(dZ, L.groups, row_mask=rows, col_mask=cols, in_ch_mask=inm,
+                                        in_compacted=inm is not None)
+        Wd, rid, ccd, ctd, szd = sa.compact(dZ, L.groups)
+        X = torch.from_numpy(input_nchw(wl, li)).cuda()
+        Xc = sa.pack_nhwc(X, keep=inm)
+        Xf = sa.pack_nhwc(X)
+        need = max(sa.conv_workspace(Xc, sz, L.C, L.D, L.stride, L.pad),
+                   sa.conv_workspace(Xf, szd, L.C, L.D, L.stride, L.pad), 256)
+        cws = torch.empty(need, dtype=torch.uint8, device="cuda")
+        Yc = sa.conv_fwd(Xc, Wc, cc, ct, sz, L.C, L.D, L.stride, L.pad, ws=cws)
+        Yd = sa.conv_fwd(Xf, Wd, ccd, ctd, szd, L.C, L.D, L.stride, L.pad, ws=cws)
+        dc, dd = sa.conv_desc(Xc, Wc, cc, ct, sz, L.C, L.D, L.stride, L.pad, Yc, cws), \
+            sa.conv_desc(Xf, Wd, ccd, ctd, szd, L.C, L.D, L.stride, L.pad, Yd, cws)
+        tc = _time(torch, lambda: sa.conv_fwd(None, None, None, None, sz, 0, 0, 0, 0, desc=dc), reps=10)
+        td = _time(torch, lambda: sa.conv_fwd(None, None, None, None, szd, 0, 0, 0, 0, desc=dd), reps=10)
+        xb = X.to(torch.bfloat16)
+        wb = dZ.to(torch.bfloat16)
+        tm = _time(torch, lambda: F.conv2d(xb, wb, stride=L.stride, padding=L.pad, groups=L.groups), reps=10)
+        fc = 2 * wl.batch * L.P * L.Q * sum(sz.M[g] * sz.K[g] for g in range(sz.groups))
+        fd = 2 * wl.batch * L.P * L.Q * sum(szd.M[g] * szd.K[g] for g in range(szd.groups))
+        best_dense = min(td["median_ms"], tm["median_ms"])
+        out.append({"layer": L.name, "compact_us": round(tc["median_ms"] * 1e3, 1),
+                    "dense_us": round(td["median_ms"] * 1e3, 1), "miopen_dense_us": round(tm["median_ms"] * 1e3, 1),
+                    "compact_tflops": round(fc / tc["median_ms"] / 1e9, 1),
+                    "dense_tflops": round(fd / td["median_ms"] / 1e9, 1),
+                    "speedup_vs_best_dense": round(best_dense / tc["median_ms"], 3),
+                    "compact_gflop": round(fc / 1e9, 3), "dense_gflop": round(fd / 1e9, 3)})
+        prev = mask
+        del X, Xc, Xf, Yc, Yd, xb, wb, cws
+    tot_c = sum(r["compact_us"] for r in out)
+    tot_b = sum(min(r["dense_us"], r["miopen_dense_us"]) for r in out)
+    gf = sum(r["compact_gflop"] for r in out)
+    return {"layers": out, "compact_total_us": round(tot_c, 1), "best_dense_total_us": round(tot_b, 1),
+            "compact_tflops": round(gf / tot_c * 1e3, 1), "speedup_vs_best_dense": round(tot_b / tot_c, 3)}
+
+
+def suite(path):
+    import torch
+    import paper_1807_11091_amd as sa
+    from workloads import WORKLOADS
+    import dataclasses
+    if not torch.cuda.is_available():
+        raise SystemExit("bench.py needs a GPU")
+    sa.lib()
+    prop = torch.cuda.get_device_properties(0)
+    rep = {"device": {"name": prop.name, "compute_units": prop.multi_processor_count}}
+    # achievable peaks on this box
+    n = 1 << 30
+    a = torch.empty(n, dtype=torch.uint8, device="cuda")
+    b = torch.empty_like(a)
+    t = _time(torch, lambda: b.copy_(a), reps=10)
+    rep["achievable"] = {"copy_GBps": round(2 * n / t["median_ms"] / 1e6, 1)}
+    del a, b
+    m = torch.randn(8192, 8192, device="cuda", dtype=torch.bfloat16)
+    t = _time(torch, lambda: torch.matmul(m, m), reps=10)
+    rep["achievable"]["bf16_matmul_8192_TFLOPs"] = round(2 * 8192 ** 3 / t["median_ms"] / 1e9, 1)
+    del m
+    torch.cuda.empty_cache()
+    print(json.dumps(rep["achievable"]), flush=True)
+    rep["admm"], rep["conv"] = {}, {}
+    for name in ("cifar_conv64", "alexnet_shape30", "alexnet_chain_f50c50", "resnet50_filter60"):
+        wl = WORKLOADS[name]
+        rep["admm"][name] = suite_admm(torch, sa, wl, 0)
+        print(name, "admm", json.dumps(rep["admm"][name]), flush=True)
+        rep["conv"][name] = suite_conv(torch, sa, wl, 0)
+        print(name, "conv", json.dumps({k: v for k, v in rep["conv"][name].items() if k != "layers"}), flush=True)
+        torch.cuda.empty_cache()
+    # ResNet-50 stage-3 layer: every kind at every density, and the extra densities
+    wl = WORKLOADS["resnet50_s3_sweep"]
+    variants = list(wl.variants) + [(kd, p) for kd in (sa.FILTER, sa.SHAPE) for p in wl.extra_percents]
+    rep["sweep"] = []
+    for kd, p in variants:
+        w = dataclasses.replace(wl, variants=((kd, p),))
+        r = {"kind": {0: "filter", 1: "channel", 2: "shape", 3: "element"}[kd], "percent": p,
+             "admm": suite_admm(torch, sa, w, 0)["one_call"], "conv": suite_conv(torch, sa, w, 0)["layers"][0]}
+        rep["sweep"].append(r)
+        print("sweep", json.dumps({"kind": r["kind"], "percent": p, "speedup": r["conv"]["speedup_vs_best_dense"]}),
+              flush=True)
+        torch.cuda.empty_cache()
+    with open(path, "w") as f:
+        json.dump(rep, f, indent=1)
+    print("suite written to", path)
+
+
 def main():
     args = parse()
     if args.copy_probe:
         copy_probe(args.copy_probe)
+        return
+    if args.suite:
+        suite(args.suite)
         return
     if args.gpus != 1:
         print(json.dumps({"error": "this build measures one GPU only; run with --gpus 1"}))

@@ -72,6 +72,64 @@ __device__ inline int xcd_remap(int bid, int n) {
     return xcd < r ? xcd * (q + 1) + local : r * (q + 1) + (xcd - r) * q + local;
 }
 
+// Stores n <= 8 consecutive bf16 outputs (a 16-byte aligned row of the LDS
+// output tile) with the widest stores the destination's alignment allows:
+// output rows of sum(M_g) channels are 16-byte aligned only when that sum is a
+// multiple of 8 (pruned layers keep any number of filters).
+__device__ inline void store_out8(uint16_t *dst, const uint16_t *src, int n) {
+    const uintptr_t ad = reinterpret_cast<uintptr_t>(dst);
+    if (n == 8 && (ad & 15) == 0) {
+        *reinterpret_cast<uint4 *>(dst) = *reinterpret_cast<const uint4 *>(src);
+        return;
+    }
+    if (n == 8 && (ad & 7) == 0) {
+        reinterpret_cast<uint2 *>(dst)[0] = reinterpret_cast<const uint2 *>(src)[0];
+        reinterpret_cast<uint2 *>(dst)[1] = reinterpret_cast<const uint2 *>(src)[1];
+        return;
+    }
+    int e = 0;
+    if (ad & 2) {  // one element to reach 4-byte alignment
+        dst[0] = src[0];
+        e = 1;
+    }
+    for (; e + 2 <= n; e += 2)
+        *reinterpret_cast<uint32_t *>(dst + e) = (uint32_t)src[e] | ((uint32_t)src[e + 1] << 16);
+    if (e < n) dst[e] = src[e];
+}
+
+// An output tile that holds whole output rows (one conv group owns every output
+// channel and one filter tile covers them) is one contiguous range of Y: it is
+// written with 16-byte stores whatever the row length, the elements read back
+// from the LDS tile (row pitch RP) one by one.  Y + n0 * Cy is 16-byte aligned
+// when Y is (n0 is a multiple of 8).
+template <int RP>
+__device__ inline void store_tile_rows(uint16_t *Y, const uint16_t *sC, int n0, int rows, int Cy,
+                                       const FastDiv &divCy, int tid, int nt) {
+    const int total = rows * Cy;
+    uint16_t *base = Y + (int64_t)n0 * Cy;
+    for (int c = tid; c * 8 < total; c += nt) {
+        const int e0 = c * 8;
+        int pl = (int)fdiv((uint32_t)e0, divCy);
+        int m = e0 - pl * Cy;
+        uint16_t v[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            v[q] = e0 + q < total ? sC[pl * RP + m] : (uint16_t)0;
+            if (++m == Cy) {
+                m = 0;
+                ++pl;
+            }
+        }
+        if (e0 + 8 <= total) {
+            *reinterpret_cast<uint4 *>(base + e0) =
+                make_uint4(v[0] | ((uint32_t)v[1] << 16), v[2] | ((uint32_t)v[3] << 16),
+                           v[4] | ((uint32_t)v[5] << 16), v[6] | ((uint32_t)v[7] << 16));
+        } else {
+            for (int q = 0; e0 + q < total; ++q) base[e0 + q] = v[q];
+        }
+    }
+}
+
 // ---------------------------------------------------------------- k_conv
 // One conv group of a launch (every group of a layer runs in one launch).
 struct ConvGroup {
@@ -85,7 +143,7 @@ struct ConvArgs {
     uint16_t *Y;
     int32_t H, W, D, stride, pad, P, Q, NPQ, Cy;
     int32_t ngroups, nblocks;
-    FastDiv divPQ, divQ, divD;
+    FastDiv divPQ, divQ, divD, divCy;
     ConvGroup g[SA_MAX_CONV_GROUPS];
 };
 
@@ -243,19 +301,17 @@ __global__ __launch_bounds__(64 * WN * WM) void k_conv(ConvArgs a) {
                 *reinterpret_cast<bf16x4 *>(&sC[pl * (BN + 8) + ml]) = o;
             }
     __syncthreads();
-    const bool vec_out = (a.Cy % 8 == 0) && ((G.o_off + m0) % 8 == 0) && ((uintptr_t)a.Y % 16 == 0);
+    if (a.Cy % 8 != 0 && G.mtiles == 1 && G.M == a.Cy && ((uintptr_t)a.Y & 15) == 0) {  // whole, unaligned rows
+        store_tile_rows<BN + 8>(a.Y, sC, n0, min(BM, a.NPQ - n0), a.Cy, a.divCy, tid, NT);
+        return;
+    }
     constexpr int CPR = BN / 8;  // 16-byte chunks per output row
     for (int c = tid; c < BM * CPR; c += NT) {
         const int pl = c / CPR, mc = c - pl * CPR;
         const int px = n0 + pl, m = m0 + mc * 8;
         if (px >= a.NPQ || m >= G.M) continue;
         uint16_t *dst = a.Y + (int64_t)px * a.Cy + G.o_off + m;
-        const uint16_t *srcp = &sC[pl * (BN + 8) + mc * 8];
-        if (vec_out && m + 8 <= G.M) {
-            *reinterpret_cast<uint4 *>(dst) = *reinterpret_cast<const uint4 *>(srcp);
-        } else {
-            for (int e = 0; e < 8 && m + e < G.M; ++e) dst[e] = srcp[e];
-        }
+        store_out8(dst, &sC[pl * (BN + 8) + mc * 8], min(8, G.M - m));
     }
 }
 
@@ -458,7 +514,7 @@ struct PatchArgs {
     // as s*s*Cxo channels; column (kh, kw, c) of the compacted matrix reads
     // tap (kh / s, kw / s), channel ((kh % s) * s + kw % s) * Cxo + c
     int32_t s2d, Do, Cxo;
-    FastDiv divQ, divP, divHp, divD, divS, divDo, divS2d;
+    FastDiv divQ, divP, divHp, divD, divS, divDo, divS2d, divCy;
     PatchGroup g[SA_MAX_CONV_GROUPS];
 };
 
@@ -743,31 +799,30 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
                 *reinterpret_cast<bf16x4 *>(&sC[pl * (BNB + 8) + ml]) = o;
             }
     __syncthreads();
-    const bool vec_out = (a.Cy % 8 == 0) && ((G.o_off + m0) % 8 == 0) && ((uintptr_t)a.Y % 16 == 0);
+    if (a.Cy % 8 != 0 && G.mtiles == 1 && G.M == a.Cy && ((uintptr_t)a.Y & 15) == 0) {  // whole, unaligned rows
+        store_tile_rows<BNB + 8>(a.Y, sC, n0, min(BMB, a.NPQ - n0), a.Cy, a.divCy, tid, NT);
+        return;
+    }
     constexpr int CPR = BNB / 8;
     for (int c = tid; c < BMB * CPR; c += NT) {
         const int pl = c / CPR, mc = c - pl * CPR;
         const int px = n0 + pl, m = m0 + mc * 8;
         if (px >= a.NPQ || m >= G.M) continue;
         uint16_t *dst = a.Y + (int64_t)px * a.Cy + G.o_off + m;
-        const uint16_t *srcp = &sC[pl * (BNB + 8) + mc * 8];
-        if (vec_out && m + 8 <= G.M) {
-            *reinterpret_cast<uint4 *>(dst) = *reinterpret_cast<const uint4 *>(srcp);
-        } else {
-            for (int e = 0; e < 8 && m + e < G.M; ++e) dst[e] = srcp[e];
-        }
+        store_out8(dst, &sC[pl * (BNB + 8) + mc * 8], min(8, G.M - m));
     }
 }
 
 // ---------------------------------------------------------------- k_s2d
-// Space-to-depth image of the zero-padded input for strided layers with few
-// channels: Xs[n][i][j][(a*s + b)*Cx + c] = Xpad[n][i*s + a][j*s + b][c].  The
-// strided CONV over X is then a stride-1 CONV over Xs with ceil(C/s) x
-// ceil(D/s) taps and s*s*Cx channels (8-aligned), which k_conv_patch runs.
+// Space-to-depth image of the zero-padded input for layers with few channels:
+// Xs[n][i][j][(a*s + b)*Cx + c] = Xpad[n][i*s + a][j*s + b][c], channels from
+// s*s*Cx up to the next multiple of 8 zero.  The CONV over X (stride s) is then
+// a stride-1 CONV over Xs with ceil(C/s) x ceil(D/s) taps, which k_conv_patch
+// runs; s = 1 only pads the channels (and folds the zero border in).
 struct S2dArgs {
     const uint16_t *X;
     uint16_t *Xs;
-    int32_t N, H, W, Cx, s, pad, Hs, Ws, Cs;  // Cs = s*s*Cx
+    int32_t N, H, W, Cx, s, pad, Hs, Ws, Cs, Creal;  // Creal = s*s*Cx, Cs = Creal rounded up to 8
     int32_t chunks;                           // N*Hs*Ws*Cs / 8 (< 2^27: the image is below 2 GiB)
     FastDiv divCs8, divWs, divHs, divCx, divS;
 };
@@ -792,7 +847,7 @@ __global__ __launch_bounds__(256) void k_s2d(S2dArgs a) {
 #pragma unroll
         for (int q = 0; q < 8; ++q) {
             const int h = i * a.s + ra - a.pad, w = j * a.s + rb - a.pad;
-            v[q] = ((unsigned)h < (unsigned)a.H && (unsigned)w < (unsigned)a.W)
+            v[q] = (c0 + q < a.Creal && (unsigned)h < (unsigned)a.H && (unsigned)w < (unsigned)a.W)
                        ? a.X[(img + (int64_t)h * a.W + w) * a.Cx + c]
                        : 0u;
             if (++c == a.Cx) {
@@ -853,6 +908,7 @@ int run_conv(ConvArgs a, hipStream_t stream) {
         maxM = std::max(maxM, a.g[i].M);
     }
     a.divPQ = make_fastdiv((uint32_t)(a.P * a.Q));
+    a.divCy = make_fastdiv((uint32_t)std::max(1, a.Cy));
     a.divQ = make_fastdiv((uint32_t)a.Q);
     a.divD = make_fastdiv((uint32_t)a.D);
     if (all256) return launch_conv<128, 256, 2, 2>(a, stream);
@@ -939,8 +995,8 @@ struct ConvPlan {
     int path[SA_MAX_CONV_GROUPS];
     int pix_bytes[SA_MAX_CONV_GROUPS], nch[SA_MAX_CONV_GROUPS], ch_lo8[SA_MAX_CONV_GROUPS];
     int TM, TN, patch_bytes, tab_bytes, lds;  // k_conv_patch launch (when any group takes it)
-    // geometry the footprint kernel sees: the input itself, or (s2d > 1) its
-    // space-to-depth image, which then takes the first s2d_bytes of the scratch
+    // geometry the footprint kernel sees: the input itself, or (s2d = factor > 0)
+    // its space-to-depth image, which then takes the first s2d_bytes of the scratch
     int s2d, gH, gW, gCx, gC, gD, gs, gpad;
     size_t s2d_bytes;
     size_t ws_need;  // scratch: space-to-depth image, then the two-phase groups' rows
@@ -972,22 +1028,24 @@ int conv_plan(const sa_conv_desc &d, ConvPlan *pl) {
     p.P = (int)P;
     p.Q = (int)Q;
     p.NPQ = (int)NPQ;
-    // a strided layer whose pixels are not whole 16-byte chunks (few input
-    // channels) runs on its space-to-depth image when that one's are
+    // pixels that are not whole 16-byte chunks (few input channels): the layer
+    // runs on its space-to-depth image (s = stride; s = 1 only pads), whose
+    // s*s*Cx channels are padded with zeros to a multiple of 8
     const int st = d.stride;
-    p.s2d = (d.Cx % 8 != 0 && st > 1 && (d.Cx * st * st) % 8 == 0) ? st : 1;
-    if (p.s2d > 1) {
+    p.s2d = 0;
+    if (d.Cx % 8 != 0) {
+        p.s2d = st;
         p.gH = (d.H + 2 * d.pad + st - 1) / st;
         p.gW = (d.W + 2 * d.pad + st - 1) / st;
-        p.gCx = d.Cx * st * st;
+        p.gCx = (d.Cx * st * st + 7) / 8 * 8;
         p.gC = (d.C + st - 1) / st;
         p.gD = (d.D + st - 1) / st;
         p.gs = 1;
         p.gpad = 0;
         p.s2d_bytes = (size_t)d.N * p.gH * p.gW * p.gCx * 2;
-        if (p.s2d_bytes >= (size_t(1) << 31)) p.s2d = 1;  // too large for 32-bit offsets: two-phase
+        if (p.s2d_bytes >= (size_t(1) << 31) || p.gCx > 65535) p.s2d = 0;  // too large: two-phase
     }
-    if (p.s2d == 1) {
+    if (p.s2d == 0) {
         p.gH = d.H;
         p.gW = d.W;
         p.gCx = d.Cx;
@@ -1017,7 +1075,7 @@ int conv_plan(const sa_conv_desc &d, ConvPlan *pl) {
             // separate pass instead
             p.path[g] = p.gCx % 8 == 0 ? kPatch : kGather;
             if (p.path[g] == kGather) continue;
-            if (p.s2d > 1) {  // every channel of the space-to-depth pixel
+            if (p.s2d > 0) {  // every channel of the space-to-depth pixel
                 p.ch_lo8[g] = 0;
                 p.nch[g] = p.gCx / 8;
             } else {
@@ -1161,6 +1219,7 @@ extern "C" int structadmm_conv_fwd(const sa_conv_desc *desc, hipStream_t stream)
         sa2.Hs = p.gH;
         sa2.Ws = p.gW;
         sa2.Cs = p.gCx;
+        sa2.Creal = d.Cx * p.s2d * p.s2d;
         sa2.chunks = (int32_t)(p.s2d_bytes / 16);
         sa2.divCs8 = make_fastdiv((uint32_t)(p.gCx / 8));
         sa2.divWs = make_fastdiv((uint32_t)p.gW);
@@ -1188,16 +1247,17 @@ extern "C" int structadmm_conv_fwd(const sa_conv_desc *desc, hipStream_t stream)
     pa.Wpp = pa.Ws * p.gs;
     pa.patch_bytes = p.patch_bytes;
     pa.tab_bytes = p.tab_bytes;
-    pa.s2d = p.s2d;
+    pa.s2d = p.s2d > 1 ? p.s2d : 1;  // factor 1: channel padding only, taps unchanged
     pa.Do = d.D;
     pa.Cxo = d.Cx;
     pa.divQ = make_fastdiv((uint32_t)Q);
+    pa.divCy = make_fastdiv((uint32_t)std::max(1, p.Cy));
     pa.divP = make_fastdiv((uint32_t)P);
     pa.divHp = make_fastdiv((uint32_t)pa.Hp);
     pa.divD = make_fastdiv((uint32_t)p.gD);
     pa.divS = make_fastdiv((uint32_t)p.gs);
     pa.divDo = make_fastdiv((uint32_t)d.D);
-    pa.divS2d = make_fastdiv((uint32_t)p.s2d);
+    pa.divS2d = make_fastdiv((uint32_t)std::max(1, p.s2d));
     size_t ws_off = (p.s2d_bytes + 255) / 256 * 256;
     for (int g = 0; g < s.groups; ++g) {
         if (p.path[g] == kSkip) continue;

@@ -173,9 +173,12 @@ def test_compact_and_conv_validation():
                                              sizes=ctypes.pointer(s), X=FAKE, Wc=FAKE, col_ch=FAKE,
                                              col_tap=FAKE, Y=FAKE, ws=None, ws_bytes=0), **kw})
     assert L.structadmm_conv_workspace(ctypes.byref(desc(Cx=8))) == 0
-    # channels not 8-aligned: the compacted im2col rows go through caller scratch
+    # channels not 8-aligned: the input's space-to-depth image (here stride 1: the
+    # zero border folded in, 2 channels padded to 8) goes to caller scratch
     need = L.structadmm_conv_workspace(ctypes.byref(desc()))
-    assert need == 8 * 8 * 64 * 2
+    assert need == (10 * 10 * 8 * 2 + 255) // 256 * 256
+    s2 = L.structadmm_conv_workspace(ctypes.byref(desc(stride=2)))
+    assert s2 == (5 * 5 * 8 * 2 + 255) // 256 * 256  # 2x2 blocks of 2 channels: 8 channels
     assert conv() == -3
     assert conv(ws=FAKE + 2048, ws_bytes=need - 1) == -3
     assert conv(ws=FAKE + 2048 + 16, ws_bytes=need) == -2

@@ -132,6 +132,12 @@ SMALL = [
     # strided, few channels: space-to-depth image of the input, then the footprint kernel
     (2, 2, 19, 17, 40, 5, 5, 2, 2, 1, sa.SHAPE, 0.4),
     (2, 4, 16, 16, 24, 3, 3, 2, 1, 2, sa.SHAPE, 0.5),
+    # space-to-depth channels padded to 8 (ResNet stem shape), and channel padding only
+    (2, 3, 30, 28, 20, 7, 7, 2, 3, 1, sa.FILTER, 0.6),
+    (2, 3, 12, 11, 16, 3, 3, 1, 1, 1, sa.SHAPE, 0.5),
+    # odd numbers of kept filters: output rows not 16-byte aligned
+    (2, 16, 9, 9, 38, 1, 1, 1, 0, 1, sa.FILTER, 0.6),
+    (2, 32, 8, 8, 50, 3, 3, 1, 1, 2, sa.FILTER, 0.62),
     # input rows too wide for an LDS copy of the footprint: two-phase gather
     (1, 64, 3, 2100, 40, 3, 3, 1, 1, 1, sa.SHAPE, 0.3),
 ]
