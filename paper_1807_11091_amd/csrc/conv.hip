@@ -897,24 +897,51 @@ int launch_conv(ConvArgs a, hipStream_t stream) {
     return check_hip(hipGetLastError(), "k_conv");
 }
 
-// One launch for every group of a; the tile shape follows the widest group.
+// One launch for every group of a.  Tile shape (measured on gfx950): 256 x 32
+// for groups of at most 32 filters; else the least padded filter work first and,
+// among those, 128 x 128 tiles while the launch has at least 320 of them, else
+// the shape with the most tiles (more wavefronts per CU hide the operand
+// latency better than bigger tiles save LDS reads), the 64-pixel one on a tie.
 int run_conv(ConvArgs a, hipStream_t stream) {
     if (a.ngroups == 0) return SA_OK;
-    bool all256 = true;
-    int maxM = 0;
-    for (int i = 0; i < a.ngroups; ++i) {
+    for (int i = 0; i < a.ngroups; ++i)
         a.g[i].divRun = make_fastdiv((uint32_t)std::max(1, a.g[i].run));  // a group without columns has run 0
-        all256 = all256 && a.g[i].M % 256 == 0;
-        maxM = std::max(maxM, a.g[i].M);
-    }
     a.divPQ = make_fastdiv((uint32_t)(a.P * a.Q));
     a.divCy = make_fastdiv((uint32_t)std::max(1, a.Cy));
     a.divQ = make_fastdiv((uint32_t)a.Q);
     a.divD = make_fastdiv((uint32_t)a.D);
-    if (all256) return launch_conv<128, 256, 2, 2>(a, stream);
-    if (maxM > 64) return launch_conv<128, 128, 2, 2>(a, stream);
-    if (maxM > 32) return launch_conv<256, 64, 4, 1>(a, stream);
-    return launch_conv<256, 32, 4, 1>(a, stream);
+    struct Shape {
+        int BM, BN;
+    };
+    constexpr Shape shapes[3] = {{128, 128}, {128, 64}, {64, 128}};
+    int maxM = 0;
+    for (int i = 0; i < a.ngroups; ++i) maxM = std::max(maxM, a.g[i].M);
+    if (maxM <= 32) return launch_conv<256, 32, 4, 1>(a, stream);
+    int64_t work[3], blocks[3], best = -1;
+    for (int c = 0; c < 3; ++c) {
+        int64_t mt = 0, pm = 0;
+        for (int i = 0; i < a.ngroups; ++i) {
+            const int t = (a.g[i].M + shapes[c].BN - 1) / shapes[c].BN;
+            mt += t;
+            pm += (int64_t)t * shapes[c].BN;
+        }
+        work[c] = pm;
+        blocks[c] = mt * ((a.NPQ + shapes[c].BM - 1) / shapes[c].BM);
+        if (best < 0 || pm < best) best = pm;
+    }
+    auto near = [&](int c) { return work[c] * 50 <= best * 51; };  // within 2% of the least work
+    int pick = -1;
+    if (near(0) && blocks[0] >= 320) {
+        pick = 0;
+    } else {
+        for (int c : {2, 1, 0})
+            if (near(c) && (pick < 0 || blocks[c] > blocks[pick])) pick = c;
+    }
+    switch (pick) {
+        case 0: return launch_conv<128, 128, 2, 2>(a, stream);
+        case 1: return launch_conv<128, 64, 2, 2>(a, stream);
+        default: return launch_conv<64, 128, 1, 4>(a, stream);
+    }
 }
 
 bool is_vec(const sa_compact_sizes &s, int g, int Cx) {
