@@ -35,6 +35,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 METRIC = "compacted-conv TFLOP/s & speedup vs dense; ADMM projection+update HBM GB/s"
+FILTER_KIND, SHAPE_KIND = 0, 2  # sparsity-set kinds (the C ABI's enum)
 WORKLOAD = "alexnet_shape30"
 HBM_PEAK_GBS = 8000.0
 BF16_PEAK_TFLOPS = 2500.0
@@ -346,6 +347,46 @@ def suite_conv(torch, sa, wl, variant, layer_ids=None):
             "compact_tflops": round(gf / tot_c * 1e3, 1), "speedup_vs_best_dense": round(tot_b / tot_c, 3)}
 
 
+def suite_oracle(wl, variant, images):
+    """The oracle on the host: the fused ADMM step of every layer (one thread)
+    and the compacted and dense CONV of ``images`` images per layer (OpenMP
+    over images)."""
+    import oracle
+    from workloads import input_nchw, layer_tensors
+    kind, pct = wl.variants[variant]
+    t_admm, fc, fd, tc, td, prev = 0.0, 0, 0, 0.0, 0.0, None
+    for li, L in enumerate(wl.layers):
+        W, U = layer_tensors(wl, li)
+        k = wl.k_for(li, kind, pct)
+        inm = prev if wl.chain else None
+        t0 = time.perf_counter()
+        r = oracle.project(W, U, kind, k, L.groups, in_ch_mask=inm, rho=wl.rho, fused=True)
+        t_admm += time.perf_counter() - t0
+        rows = r["mask"] if kind == FILTER_KIND else None
+        cols = r["mask"] if kind == SHAPE_KIND else None
+        rc = oracle.compact(r["Z"], L.groups, row_mask=rows, col_mask=cols, in_ch_mask=inm,
+                            in_compacted=inm is not None)
+        rd = oracle.compact(r["Z"], L.groups)
+        X = input_nchw(wl, li, batch=images)
+        Xc, Xf = oracle.pack(X, keep=inm), oracle.pack(X)
+        t0 = time.perf_counter()
+        oracle.conv(Xc, rc, L.C, L.D, L.stride, L.pad)
+        t1 = time.perf_counter()
+        oracle.conv(Xf, rd, L.C, L.D, L.stride, L.pad)
+        t2 = time.perf_counter()
+        tc += t1 - t0
+        td += t2 - t1
+        fc += 2 * images * L.P * L.Q * int(np.sum(rc["M"].astype(np.int64) * rc["K"]))
+        fd += 2 * images * L.P * L.Q * int(np.sum(rd["M"].astype(np.int64) * rd["K"]))
+        prev = r["mask"]
+    n = sum(L.n for L in wl.layers)
+    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    return {"fused_step_s_1_thread": round(t_admm, 4), "fused_step_GBps": round(20 * n / t_admm / 1e9, 3),
+            "conv_images": images, "conv_threads": min(threads, images),
+            "conv_compact_s": round(tc, 3), "conv_compact_GFLOPs": round(fc / tc / 1e9, 2),
+            "conv_dense_s": round(td, 3), "conv_dense_GFLOPs": round(fd / td / 1e9, 2)}
+
+
 def suite(path):
     import torch
     import paper_1807_11091_amd as sa
@@ -370,8 +411,11 @@ def suite(path):
     torch.cuda.empty_cache()
     print(json.dumps(rep["achievable"]), flush=True)
     rep["admm"], rep["conv"] = {}, {}
+    rep["oracle"] = {}
     for name in ("cifar_conv64", "alexnet_shape30", "alexnet_chain_f50c50", "resnet50_filter60"):
         wl = WORKLOADS[name]
+        rep["oracle"][name] = suite_oracle(wl, 0, 4 if name == "resnet50_filter60" else 16)
+        print(name, "oracle", json.dumps(rep["oracle"][name]), flush=True)
         rep["admm"][name] = suite_admm(torch, sa, wl, 0)
         print(name, "admm", json.dumps(rep["admm"][name]), flush=True)
         rep["conv"][name] = suite_conv(torch, sa, wl, 0)
@@ -385,6 +429,8 @@ def suite(path):
         w = dataclasses.replace(wl, variants=((kd, p),))
         r = {"kind": {0: "filter", 1: "channel", 2: "shape", 3: "element"}[kd], "percent": p,
              "admm": suite_admm(torch, sa, w, 0)["one_call"], "conv": suite_conv(torch, sa, w, 0)["layers"][0]}
+        if p in (10, 50):
+            r["oracle"] = suite_oracle(w, 0, 8)
         rep["sweep"].append(r)
         print("sweep", json.dumps({"kind": r["kind"], "percent": p, "speedup": r["conv"]["speedup_vs_best_dense"]}),
               flush=True)
