@@ -895,6 +895,28 @@ extern "C" int structadmm_project(const sa_project_desc *layers, int n_layers, v
         max_level = std::max(max_level, level[i]);
     }
 
+    auto fill_row = [&](int i, RowLayer &R) {
+        const sa_project_desc &d = layers[i];
+        const LayerPlan &p = plan[i];
+        R.W = d.W;
+        R.U = d.U;
+        R.Z = d.Z;
+        R.G = d.G;
+        R.rowkeep = d.kind == SA_FILTER ? d.mask : nullptr;
+        if (d.kind == SA_FILTER)
+            R.colkeep = d.in_ch_mask ? ws_at<uint8_t>(ws, p.off_allowed) : nullptr;
+        else
+            R.colkeep = ws_at<uint8_t>(ws, p.off_colkeep);
+        R.allowed = d.in_ch_mask ? ws_at<uint8_t>(ws, p.off_allowed) : nullptr;
+        R.scores = d.scores ? d.scores : (p.off_scores != SIZE_MAX ? ws_at<double>(ws, p.off_scores) : nullptr);
+        R.A = (int)d.A;
+        R.K = p.K;
+        R.Ag = p.Ag;
+        R.rpb = p.rpb;
+        R.vec = p.vec;
+        R.rho = d.rho;
+    };
+
     for (int lv = 0; lv <= max_level; ++lv) {
         std::vector<int> ids;
         for (int i = 0; i < n_layers; ++i)
@@ -912,27 +934,6 @@ extern "C" int structadmm_project(const sa_project_desc *layers, int n_layers, v
             if (int rc = launch_check("k_expand_allowed")) return rc;
         }
 
-        auto fill_row = [&](int i, RowLayer &R) {
-            const sa_project_desc &d = layers[i];
-            const LayerPlan &p = plan[i];
-            R.W = d.W;
-            R.U = d.U;
-            R.Z = d.Z;
-            R.G = d.G;
-            R.rowkeep = d.kind == SA_FILTER ? d.mask : nullptr;
-            if (d.kind == SA_FILTER)
-                R.colkeep = d.in_ch_mask ? ws_at<uint8_t>(ws, p.off_allowed) : nullptr;
-            else
-                R.colkeep = ws_at<uint8_t>(ws, p.off_colkeep);
-            R.allowed = d.in_ch_mask ? ws_at<uint8_t>(ws, p.off_allowed) : nullptr;
-            R.scores = d.scores ? d.scores : (p.off_scores != SIZE_MAX ? ws_at<double>(ws, p.off_scores) : nullptr);
-            R.A = (int)d.A;
-            R.K = p.K;
-            R.Ag = p.Ag;
-            R.rpb = p.rpb;
-            R.vec = p.vec;
-            R.rho = d.rho;
-        };
 
         // filter scores
         {
@@ -1063,39 +1064,40 @@ extern "C" int structadmm_project(const sa_project_desc *layers, int n_layers, v
             hipLaunchKernelGGL(k_elem_apply, dim3(p.nchunks), dim3(kElemThreads), 0, stream, a);
             if (int rc = launch_check("k_elem_apply")) return rc;
         }
-        // apply for every structured layer
-        {
-            std::vector<int> sl;
-            for (int i : ids)
-                if (layers[i].kind != SA_ELEMENT) sl.push_back(i);
-            for (size_t s = 0; s < sl.size(); s += kTab) {
-                ApplyTab tab;
-                memset(&tab, 0, sizeof tab);
-                int blocks = 0;
-                tab.nl = (int)std::min<size_t>(kTab, sl.size() - s);
-                for (int t = 0; t < tab.nl; ++t) {
-                    RowLayer R;
-                    fill_row(sl[s + t], R);
-                    const sa_project_desc &d = layers[sl[s + t]];
-                    ApplyLayer &L = tab.L[t];
-                    L.W = R.W;
-                    L.U = R.U;
-                    L.Z = R.Z;
-                    L.G = R.G;
-                    L.rowkeep = R.rowkeep;
-                    L.colkeep = R.colkeep;
-                    L.divK = make_fastdiv((uint32_t)R.K);
-                    L.divAg = make_fastdiv((uint32_t)R.Ag);
-                    L.n = (int32_t)(d.A * d.B * d.C * d.D);
-                    L.K = R.K;
-                    L.rho = R.rho;
-                    tab.begin[t] = blocks;
-                    blocks += (int)((L.n + kApplyChunk - 1) / kApplyChunk);
-                }
-                tab.begin[tab.nl] = blocks;
-                hipLaunchKernelGGL(k_apply, dim3(blocks), dim3(kApplyThreads), 0, stream, tab);
-                if (int rc = launch_check("k_apply")) return rc;
+    }
+    // apply for every structured layer, all levels at once: a level only needs
+    // the masks of the levels before it, never their Z / U / G
+    {
+        std::vector<int> sl;
+        for (int i = 0; i < n_layers; ++i)
+            if (layers[i].kind != SA_ELEMENT) sl.push_back(i);
+        for (size_t s = 0; s < sl.size(); s += kTab) {
+            ApplyTab tab;
+            memset(&tab, 0, sizeof tab);
+            int blocks = 0;
+            tab.nl = (int)std::min<size_t>(kTab, sl.size() - s);
+            for (int t = 0; t < tab.nl; ++t) {
+                RowLayer R;
+                fill_row(sl[s + t], R);
+                const sa_project_desc &d = layers[sl[s + t]];
+                ApplyLayer &L = tab.L[t];
+                L.W = R.W;
+                L.U = R.U;
+                L.Z = R.Z;
+                L.G = R.G;
+                L.rowkeep = R.rowkeep;
+                L.colkeep = R.colkeep;
+                L.divK = make_fastdiv((uint32_t)R.K);
+                L.divAg = make_fastdiv((uint32_t)R.Ag);
+                L.n = (int32_t)(d.A * d.B * d.C * d.D);
+                L.K = R.K;
+                L.rho = R.rho;
+                tab.begin[t] = blocks;
+                blocks += (int)((L.n + kApplyChunk - 1) / kApplyChunk);
             }
+            tab.begin[tab.nl] = blocks;
+            hipLaunchKernelGGL(k_apply, dim3(blocks), dim3(kApplyThreads), 0, stream, tab);
+            if (int rc = launch_check("k_apply")) return rc;
         }
     }
     return SA_OK;
