@@ -48,7 +48,9 @@ struct RowLayer {
     const uint8_t *colkeep;  // [groups*K] or null: every column kept
     const uint8_t *allowed;  // [groups*K] or null: every entry inside the support
     double *scores;          // [A] (row scores)
-    int32_t A, K, Ag, rpb;   // rows, row length, rows per conv group, rows per workgroup
+    double *rowpart;         // [A][nchunk] partial row sums when nchunk > 1
+    int32_t A, K, Ag;        // rows, row length, rows per conv group
+    int32_t R, nchunk;       // rows per wavefront item (short rows), 1024-weight chunks per row
     int32_t vec;             // K % 4 == 0: float4 path
     float rho;
 };
@@ -73,12 +75,13 @@ struct ColTab {
 
 struct SelLayer {
     const double *partials;  // channel / shape: [nbands][K]
-    double *scores;          // [G]: filter: input; channel / shape: output
+    const double *rowpart;   // filter with chunked rows: [G][nchunk]
+    double *scores;          // [G]: filter: input (or output with rowpart); channel / shape: output
     uint8_t *mask;           // [G]
     int32_t *kept_idx;       // [k]
     uint8_t *colkeep;        // [groups*K] or null
     const uint8_t *allowed;  // [groups*K] or null
-    int32_t kind, G, k, K, CD, nbands, groups;
+    int32_t kind, G, k, K, CD, nbands, groups, nchunk;
 };
 struct SelTab {
     SelLayer L[kTab];
@@ -122,9 +125,9 @@ __global__ void k_expand_allowed(const uint8_t *__restrict__ in_ch_mask, uint8_t
 __device__ inline float masked(float v, uint8_t keep) { return keep ? v : 0.0f; }
 
 // O_a = sum_j (double)v_aj^2 for each filter a (Section 4, filter-wise set).
-// A wavefront reduces R rows per pass with all their loads issued together:
-// R = 4 when a row has at most 64 float4 (one per lane), 2 up to 128, else 1
-// row looped in slices of 256 float4.
+// Every wavefront takes one item: R = 4 rows when a row has at most 64 float4
+// (one per lane), 2 rows up to 128, else one 1024-weight chunk of a row, whose
+// partial sums k_select adds in chunk order.
 __device__ inline float4 row_v(const RowLayer &L, const uint8_t *al, int64_t base, int i) {
     float4 x = *reinterpret_cast<const float4 *>(L.W + base + 4 * (int64_t)i);
     float4 y = *reinterpret_cast<const float4 *>(L.U + base + 4 * (int64_t)i);
@@ -148,60 +151,66 @@ __global__ __launch_bounds__(kRowThreads) void k_row_scores(RowTab tab) {
     const int li = find_layer(tab.begin, tab.nl, blockIdx.x);
     const RowLayer &L = tab.L[li];
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    const int r0 = (blockIdx.x - tab.begin[li]) * L.rpb;
-    const int r1 = min(L.A, r0 + L.rpb);
     constexpr int kWaves = kRowThreads / kWave;
-    if (!L.vec) {
-        for (int a = r0 + wave; a < r1; a += kWaves) {
-            const int64_t base = (int64_t)a * L.K;
-            const uint8_t *al = L.allowed ? L.allowed + (int64_t)(a / L.Ag) * L.K : nullptr;
-            double acc = 0.0;
-            for (int i = lane; i < L.K; i += kWave) {
-                float v = L.W[base + i] + L.U[base + i];
-                if (al) v = masked(v, al[i]);
-                acc += (double)v * (double)v;
-            }
-            acc = wave_sum(acc);
-            if (lane == 0) L.scores[a] = acc;
+    // one work item per wavefront, all of its loads issued together
+    const int item = (blockIdx.x - tab.begin[li]) * kWaves + wave;
+    if (!L.vec) {  // item = row
+        const int a = item;
+        if (a >= L.A) return;
+        const int64_t base = (int64_t)a * L.K;
+        const uint8_t *al = L.allowed ? L.allowed + (int64_t)(a / L.Ag) * L.K : nullptr;
+        double acc = 0.0;
+        for (int i = lane; i < L.K; i += kWave) {
+            float v = L.W[base + i] + L.U[base + i];
+            if (al) v = masked(v, al[i]);
+            acc += (double)v * (double)v;
         }
+        acc = wave_sum(acc);
+        if (lane == 0) L.scores[a] = acc;
         return;
     }
     const int K4 = L.K >> 2;
-    const int R = K4 <= kWave ? 4 : (K4 <= 2 * kWave ? 2 : 1);
-    for (int a0 = r0 + wave * R; a0 < r1; a0 += kWaves * R) {
+    if (L.R > 1) {  // item = R short rows; slot u: row a0 + u / (4 / R), float4 lane + 64 * (u % (4 / R))
+        const int R = L.R;
+        const int a0 = item * R;
+        if (a0 >= L.A) return;
         double acc[4] = {0.0, 0.0, 0.0, 0.0};
-        if (R > 1) {
-            // slot u: row a0 + u / (4 / R), float4 lane + 64 * (u % (4 / R))
-            float4 v[4];
+        float4 v[4];
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                const int a = a0 + u / (4 / R), i = lane + kWave * (u % (4 / R));
-                v[u] = make_float4(0.f, 0.f, 0.f, 0.f);
-                if (a < r1 && i < K4) {
-                    const uint8_t *al = L.allowed ? L.allowed + (int64_t)(a / L.Ag) * L.K : nullptr;
-                    v[u] = row_v(L, al, (int64_t)a * L.K, i);
-                }
-            }
-#pragma unroll
-            for (int u = 0; u < 4; ++u) acc[u / (4 / R)] += sq4(v[u]);
-        } else {
-            const uint8_t *al = L.allowed ? L.allowed + (int64_t)(a0 / L.Ag) * L.K : nullptr;
-            const int64_t base = (int64_t)a0 * L.K;
-            for (int i0 = 0; i0 < K4; i0 += 4 * kWave) {
-                float4 v[4];
-#pragma unroll
-                for (int u = 0; u < 4; ++u) {
-                    const int i = i0 + u * kWave + lane;
-                    v[u] = i < K4 ? row_v(L, al, base, i) : make_float4(0.f, 0.f, 0.f, 0.f);
-                }
-#pragma unroll
-                for (int u = 0; u < 4; ++u) acc[0] += sq4(v[u]);
+        for (int u = 0; u < 4; ++u) {
+            const int a = a0 + u / (4 / R), i = lane + kWave * (u % (4 / R));
+            v[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (a < L.A && i < K4) {
+                const uint8_t *al = L.allowed ? L.allowed + (int64_t)(a / L.Ag) * L.K : nullptr;
+                v[u] = row_v(L, al, (int64_t)a * L.K, i);
             }
         }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) acc[u / (4 / R)] += sq4(v[u]);
         for (int r = 0; r < R; ++r) {
             const double t = wave_sum(acc[r]);
-            if (lane == 0 && a0 + r < r1) L.scores[a0 + r] = t;
+            if (lane == 0 && a0 + r < L.A) L.scores[a0 + r] = t;
         }
+        return;
+    }
+    // item = (row, chunk of 256 float4): long rows spread over several wavefronts
+    const int a = item / L.nchunk, c = item - a * L.nchunk;
+    if (a >= L.A) return;
+    const uint8_t *al = L.allowed ? L.allowed + (int64_t)(a / L.Ag) * L.K : nullptr;
+    const int64_t base = (int64_t)a * L.K;
+    float4 v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        const int i = c * 4 * kWave + u * kWave + lane;
+        v[u] = i < K4 ? row_v(L, al, base, i) : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+    double acc = 0.0;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) acc += sq4(v[u]);
+    acc = wave_sum(acc);
+    if (lane == 0) {
+        if (L.nchunk == 1) L.scores[a] = acc;
+        else L.rowpart[(int64_t)a * L.nchunk + c] = acc;
     }
 }
 
@@ -303,14 +312,19 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelTab tab) {
     for (int g = tid; g < G; g += kSelThreads) {
         double s;
         if (L.kind == SA_FILTER) {
-            s = L.scores[g];
+            if (L.rowpart) {  // chunk partials, added in chunk order
+                s = 0.0;
+                for (int c = 0; c < L.nchunk; ++c) s += L.rowpart[(int64_t)g * L.nchunk + c];
+            } else {
+                s = L.scores[g];
+            }
         } else if (L.kind == SA_SHAPE) {
             s = sum_bands(L.partials + g, L.K, L.nbands, 0.0);
         } else {  // channel: over taps, then bands
             s = 0.0;
             for (int t = 0; t < L.CD; ++t) s = sum_bands(L.partials + g * L.CD + t, L.K, L.nbands, s);
         }
-        if (L.kind != SA_FILTER) L.scores[g] = s;
+        if (L.kind != SA_FILTER || L.rowpart) L.scores[g] = s;
         skey[g] = (uint64_t)__double_as_longlong(s);
         smask[g] = 0;
     }
@@ -794,8 +808,8 @@ __global__ __launch_bounds__(kDualThreads) void k_dual(DualTab tab) {
 // ---------------------------------------------------------------- host planning
 struct LayerPlan {
     int64_t G;
-    int K, CD, Ag, rpb, nbands, ctiles, vec, nchunks;
-    size_t off_scores, off_partials, off_allowed, off_colkeep, off_elem;
+    int K, CD, Ag, R, rchunks, ritems, nbands, ctiles, vec, nchunks;
+    size_t off_scores, off_rowpart, off_partials, off_allowed, off_colkeep, off_elem;
     size_t end;
 };
 
@@ -807,18 +821,25 @@ void plan_layer(const sa_project_desc &d, size_t start, LayerPlan &p) {
     p.CD = (int)(d.C * d.D);
     p.Ag = (int)(d.A / d.groups);
     p.vec = (p.K % 4 == 0) ? 1 : 0;
-    int rpb = (int)std::max<int64_t>(4, std::min<int64_t>(64, 16384 / std::max(1, p.K)));
-    p.rpb = rpb / 4 * 4;
+    // filter scores: work items of one wavefront each
+    const int K4 = p.K / 4;
+    p.R = !p.vec ? 1 : (K4 <= kWave ? 4 : (K4 <= 2 * kWave ? 2 : 1));
+    p.rchunks = (p.vec && p.R == 1) ? (K4 + 4 * kWave - 1) / (4 * kWave) : 1;
+    p.ritems = !p.vec ? (int)d.A : (p.R > 1 ? (int)((d.A + p.R - 1) / p.R) : (int)d.A * p.rchunks);
     p.nbands = (int)((d.A + kColBand - 1) / kColBand);
     const int cols_per_block = (kColThreads / kColSlices) * (p.vec ? 4 : 1);
     p.ctiles = (p.K + cols_per_block - 1) / cols_per_block;
     const int64_t n = d.A * d.B * d.C * d.D;
     p.nchunks = (int)((n + kElemChunk - 1) / kElemChunk);
     size_t off = align256(start);
-    p.off_scores = p.off_partials = p.off_allowed = p.off_colkeep = p.off_elem = SIZE_MAX;
+    p.off_scores = p.off_rowpart = p.off_partials = p.off_allowed = p.off_colkeep = p.off_elem = SIZE_MAX;
     if (d.kind != SA_ELEMENT && !d.scores) {
         p.off_scores = off;
         off = align256(off + sizeof(double) * p.G);
+    }
+    if (d.kind == SA_FILTER && p.rchunks > 1) {
+        p.off_rowpart = off;
+        off = align256(off + sizeof(double) * (size_t)d.A * p.rchunks);
     }
     if (d.kind == SA_CHANNEL || d.kind == SA_SHAPE) {
         p.off_partials = off;
@@ -912,7 +933,9 @@ extern "C" int structadmm_project(const sa_project_desc *layers, int n_layers, v
         R.A = (int)d.A;
         R.K = p.K;
         R.Ag = p.Ag;
-        R.rpb = p.rpb;
+        R.R = p.R;
+        R.nchunk = p.rchunks;
+        R.rowpart = p.off_rowpart != SIZE_MAX ? ws_at<double>(ws, p.off_rowpart) : nullptr;
         R.vec = p.vec;
         R.rho = d.rho;
     };
@@ -948,7 +971,7 @@ extern "C" int structadmm_project(const sa_project_desc *layers, int n_layers, v
                 for (int t = 0; t < tab.nl; ++t) {
                     fill_row(f[s + t], tab.L[t]);
                     tab.begin[t] = blocks;
-                    blocks += (tab.L[t].A + tab.L[t].rpb - 1) / tab.L[t].rpb;
+                    blocks += (plan[f[s + t]].ritems + kRowThreads / kWave - 1) / (kRowThreads / kWave);
                 }
                 tab.begin[tab.nl] = blocks;
                 hipLaunchKernelGGL(k_row_scores, dim3(blocks), dim3(kRowThreads), 0, stream, tab);
@@ -1002,6 +1025,8 @@ extern "C" int structadmm_project(const sa_project_desc *layers, int n_layers, v
                     SelLayer &L = tab.L[t];
                     L.partials = p.off_partials != SIZE_MAX ? ws_at<double>(ws, p.off_partials) : nullptr;
                     L.scores = d.scores ? d.scores : ws_at<double>(ws, p.off_scores);
+                    L.rowpart = p.off_rowpart != SIZE_MAX ? ws_at<double>(ws, p.off_rowpart) : nullptr;
+                    L.nchunk = p.rchunks;
                     L.mask = d.mask;
                     L.kept_idx = d.kept_idx;
                     L.colkeep = p.off_colkeep != SIZE_MAX ? ws_at<uint8_t>(ws, p.off_colkeep) : nullptr;
