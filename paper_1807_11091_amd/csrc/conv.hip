@@ -824,6 +824,7 @@ struct S2dArgs {
     uint16_t *Xs;
     int32_t N, H, W, Cx, s, pad, Hs, Ws, Cs, Creal;  // Creal = s*s*Cx, Cs = Creal rounded up to 8
     int32_t chunks;                           // N*Hs*Ws*Cs / 8 (< 2^27: the image is below 2 GiB)
+    uint32_t x_bytes;                         // bytes of X (below 2 GiB)
     FastDiv divCs8, divWs, divHs, divCx, divS;
 };
 
@@ -859,6 +860,69 @@ __global__ __launch_bounds__(256) void k_s2d(S2dArgs a) {
             }
         }
         *reinterpret_cast<uint4 *>(a.Xs + (int64_t)e * 8) =
+            make_uint4(v[0] | (v[1] << 16), v[2] | (v[3] << 16), v[4] | (v[5] << 16), v[6] | (v[7] << 16));
+    }
+}
+
+// The same image one output row (n, i) per workgroup.  The s input rows it
+// draws on are one contiguous NHWC range: it is read as aligned 16-byte chunks
+// (all of a thread's loads in flight together) into LDS, then the row is
+// written in 16-byte chunks.  Rows above or below the image are masked when
+// read back, so whatever the range picks up there is never used.  Used when
+// the range fits kS2dRowLds (the kernel above covers the rest).
+constexpr int kS2dRowLds = 64 * 1024;
+
+__global__ __launch_bounds__(256) void k_s2d_rows(S2dArgs a) {
+    extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+    const int ni = blockIdx.x;  // (n, i)
+    const int n = (int)fdiv((uint32_t)ni, a.divHs);
+    const int i = ni - n * a.Hs;
+    const int rowlen = a.W * a.Cx;
+    const int h0 = i * a.s - a.pad;
+    const int64_t b0 = ((int64_t)n * a.H + h0) * rowlen * 2;  // byte offset of (n, h0, 0, 0); may be < 0
+    const int64_t a0 = b0 & ~(int64_t)15;
+    const int nchunk = (int)((b0 - a0 + (int64_t)a.s * rowlen * 2 + 15) >> 4);
+    const __amdgpu_buffer_rsrc_t xrs = rsrc(a.X, a.x_bytes);
+    for (int base = 0; base < nchunk; base += 4 * 256) {
+        uint4 v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int ch = base + u * 256 + (int)threadIdx.x;
+            const int64_t off = a0 + (int64_t)ch * 16;
+            v[u] = bload16(xrs, (ch < nchunk && off >= 0 && off < (int64_t)a.x_bytes) ? (uint32_t)off : kInvalidOffset);
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int ch = base + u * 256 + (int)threadIdx.x;
+            if (ch < nchunk) reinterpret_cast<uint4 *>(smem)[ch] = v[u];
+        }
+    }
+    __syncthreads();
+    const uint16_t *rowbuf = reinterpret_cast<const uint16_t *>(smem) + (int)((b0 - a0) >> 1);
+    const int cs8 = a.Cs / 8;
+    uint16_t *dst = a.Xs + (int64_t)ni * a.Ws * a.Cs;
+    for (int e = threadIdx.x; e < a.Ws * cs8; e += 256) {
+        const int j = (int)fdiv((uint32_t)e, a.divCs8);
+        const int c0 = (e - j * cs8) * 8;
+        int blk = (int)fdiv((uint32_t)c0, a.divCx);
+        int c = c0 - blk * a.Cx;
+        int ra = (int)fdiv((uint32_t)blk, a.divS);
+        int rb = blk - ra * a.s;
+        uint32_t v[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            const int w = j * a.s + rb - a.pad;
+            const bool in = c0 + q < a.Creal && (unsigned)(h0 + ra) < (unsigned)a.H && (unsigned)w < (unsigned)a.W;
+            v[q] = in ? rowbuf[ra * rowlen + w * a.Cx + c] : 0u;
+            if (++c == a.Cx) {
+                c = 0;
+                if (++rb == a.s) {
+                    rb = 0;
+                    ++ra;
+                }
+            }
+        }
+        *reinterpret_cast<uint4 *>(dst + e * 8) =
             make_uint4(v[0] | (v[1] << 16), v[2] | (v[3] << 16), v[4] | (v[5] << 16), v[6] | (v[7] << 16));
     }
 }
@@ -1253,7 +1317,15 @@ extern "C" int structadmm_conv_fwd(const sa_conv_desc *desc, hipStream_t stream)
         sa2.divHs = make_fastdiv((uint32_t)p.gH);
         sa2.divCx = make_fastdiv((uint32_t)d.Cx);
         sa2.divS = make_fastdiv((uint32_t)p.s2d);
-        hipLaunchKernelGGL(k_s2d, dim3((unsigned)std::min(16384, (sa2.chunks + 255) / 256)), dim3(256), 0, stream, sa2);
+        sa2.x_bytes = x_bytes;
+        const size_t rowbytes = (size_t)p.s2d * d.W * d.Cx * 2 + 32;  // the s rows plus alignment slack
+        if (rowbytes <= (size_t)kS2dRowLds) {
+            if (int rc = allow_full_lds(reinterpret_cast<const void *>(k_s2d_rows))) return rc;
+            hipLaunchKernelGGL(k_s2d_rows, dim3(d.N * p.gH), dim3(256), rowbytes, stream, sa2);
+        } else {
+            hipLaunchKernelGGL(k_s2d, dim3((unsigned)std::min(16384, (sa2.chunks + 255) / 256)), dim3(256), 0, stream,
+                               sa2);
+        }
         if (int rc = check_hip(hipGetLastError(), "k_s2d")) return rc;
         pa.X = sa2.Xs;
         pa.x_bytes = (uint32_t)p.s2d_bytes;
