@@ -147,7 +147,10 @@ int structadmm_dual_update(const sa_dual_desc *layers, int n_layers, hipStream_t
  *         (every row when row_mask is NULL), ascending;
  *   columns: the pairs (tap t = c*D + d, channel b) with col_mask[b*C*D + t],
  *         chan_mask[b] and in_ch_mask[gc*B + b] all set (a NULL mask sets
- *         nothing aside), in tap-major order: t ascending, then b ascending;
+ *         nothing aside).  When col_mask is NULL and the kept channels sit at
+ *         consecutive input positions (sizes->run > 0), in tap-major order:
+ *         t ascending, then b ascending; otherwise in channel-major order:
+ *         b ascending, then t ascending;
  *   entries: Wc[m][j] = Z[row m, column j] rounded to bfloat16 (nearest even).
  * Matrices are concatenated over conv groups, each row-major [M_g][ldk_g]
  * with ldk_g = K_g rounded up to a multiple of 64; the padding columns
@@ -235,12 +238,13 @@ typedef struct sa_conv_desc {
     size_t ws_bytes;
 } sa_conv_desc;
 
-/* Scratch bytes structadmm_conv_fwd needs.  Groups whose columns are every
- * tap times one run of 8k input channels (dense, filter- or channel-pruned)
- * need none; other groups (filter-shape pruning, inputs with few channels)
- * first gather their compacted im2col rows, N*P*Q x ldk bfloat16, into the
- * scratch (groups run one after another and share it).  Returns 0 for an
- * invalid descriptor; structadmm_conv_fwd reports those. */
+/* Scratch bytes structadmm_conv_fwd needs.  None when the input has a
+ * multiple of 8 channels and each group's input footprint fits in LDS (any
+ * column set).  An input with other channel counts is first rewritten as its
+ * space-to-depth image (bfloat16, channels padded to a multiple of 8) in the
+ * scratch; a group whose footprint does not fit in LDS first gathers its
+ * compacted im2col rows, N*P*Q x ldk bfloat16, into a region of its own.
+ * Returns 0 for an invalid descriptor; structadmm_conv_fwd reports those. */
 size_t structadmm_conv_workspace(const sa_conv_desc *desc);
 
 int structadmm_conv_fwd(const sa_conv_desc *desc, hipStream_t stream);

@@ -119,6 +119,10 @@ __global__ __launch_bounds__(kCompThreads) void k_compact_tables(CompArgs a) {
         row_off += a.counts[kCS * g + 0];
         col_off += a.counts[kCS * g + 1];
     }
+    // a dense channel run is listed tap-major (the direct CONV reads 8
+    // consecutive channels of one tap per load); any other column set
+    // channel-major, so that every channel range is one range of columns
+    const bool tap_major = a.counts[kCS * gc + 2] > 0;
     uint32_t running = 0;
     const int64_t ncand = (int64_t)taps * a.B;
     for (int64_t base = 0; base < ncand; base += kCompThreads) {
@@ -126,8 +130,13 @@ __global__ __launch_bounds__(kCompThreads) void k_compact_tables(CompArgs a) {
         bool keep = false;
         int t = 0, b = 0;
         if (i < ncand) {
-            t = (int)(i / a.B);
-            b = (int)(i - (int64_t)t * a.B);
+            if (tap_major) {
+                t = (int)(i / a.B);
+                b = (int)(i - (int64_t)t * a.B);
+            } else {
+                b = (int)(i / taps);
+                t = (int)(i - (int64_t)b * taps);
+            }
             keep = col_kept(a, gc, t, b);
         }
         uint32_t tot;

@@ -3,7 +3,8 @@
   * bf16 rounding equals torch's float32 -> bfloat16 conversion (round to
     nearest even), a library routine;
   * the compacted matrix equals torch indexing of Z (kept rows, kept
-    columns in tap-major order) converted by torch, bit for bit;
+    columns tap-major for a dense channel run, channel-major otherwise)
+    converted by torch, bit for bit;
   * the CONV oracle equals torch.nn.functional.conv2d in float64 on the same
     bf16-rounded operands (grouped, strided, padded, non-square kernels);
   * CONV over the compacted matrix equals the dense CONV with the masked
@@ -41,15 +42,24 @@ def test_bf16_rounding_matches_torch():
     assert np.array_equal(ours, ref)
 
 
-def tapmajor_columns(B, C, D, keep_fn):
-    """Kept (tap, b) pairs in tap-major order, as flat indices into the
-    (c, d, b)-ordered view of a filter."""
-    cols = []
-    for t in range(C * D):
-        for b in range(B):
-            if keep_fn(b, t):
-                cols.append((t, b))
-    return cols
+def kept_columns(B, C, D, keep_fn, tap_major):
+    """Kept (tap, b) pairs, tap-major (tap, then b) or channel-major (b, then
+    tap)."""
+    pairs = [(t, b) for t in range(C * D) for b in range(B) if keep_fn(b, t)]
+    return sorted(pairs) if tap_major else sorted(pairs, key=lambda tb: (tb[1], tb[0]))
+
+
+def dense_run(B, gc, im, in_compacted):
+    """No shape mask: are the group's kept channels consecutive in the input?"""
+    kept = [b for b in range(B) if im is None or im[gc * B + b]]
+    if not kept:
+        return False
+    if in_compacted:
+        pos = np.cumsum(im) - 1
+        p = [int(pos[gc * B + b]) for b in kept]
+    else:
+        p = kept
+    return p == list(range(p[0], p[0] + len(p)))
 
 
 @pytest.mark.parametrize("shape,groups", [((8, 6, 3, 3), 1), ((12, 4, 5, 5), 2), ((6, 3, 3, 2), 3)])
@@ -61,6 +71,7 @@ def test_compact_matches_torch_indexing(shape, groups):
     col_mask = (rng.random(B * C * D) < 0.5).astype(np.uint8)
     in_mask = (rng.random(groups * B) < 0.7).astype(np.uint8)
     for use in [(True, False, False, False), (False, True, False, False), (True, True, True, False),
+                (False, False, True, False),
                 (True, False, True, True)]:
         rm = row_mask if use[0] else None
         cm = col_mask if use[1] else None
@@ -71,8 +82,9 @@ def test_compact_matches_torch_indexing(shape, groups):
         off = roff = coff = 0
         for gc in range(groups):
             rows = [a for a in range(gc * Ag, (gc + 1) * Ag) if rm is None or rm[a]]
-            cols = tapmajor_columns(B, C, D, lambda b, t: (cm is None or cm[b * C * D + t]) and
-                                    (im is None or im[gc * B + b]))
+            tap_major = cm is None and dense_run(B, gc, im, use[3])
+            cols = kept_columns(B, C, D, lambda b, t: (cm is None or cm[b * C * D + t]) and
+                                (im is None or im[gc * B + b]), tap_major)
             view = Zt.permute(0, 2, 3, 1).reshape(A, C * D, B)  # [a, tap, b]
             if rows and cols:
                 ref = view[rows][:, [t for t, _ in cols], [b for _, b in cols]]
