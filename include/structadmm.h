@@ -139,6 +139,36 @@ typedef struct sa_dual_desc {
 
 int structadmm_dual_update(const sa_dual_desc *layers, int n_layers, hipStream_t stream);
 
+/* ---- W-subproblem SGD step / masked retraining: structadmm_sgd_step -- */
+/*
+ * One stochastic-gradient step on a layer's weights (Section 4).  During ADMM
+ * regularisation the W-subproblem (eq. (3)) adds rho/2 ||W - Z + U||_F^2 to the
+ * loss; in masked retraining ("Masked mapping and retraining") the weights of
+ * pruned groups are held at zero while the rest train on.
+ *   t  = Gf + rho * ((W - Z) + U)          (t = Gf when Z is NULL)
+ *   W' = keep(group of e) ? W - lr * t : +0  (every entry kept when mask is NULL)
+ * in binary32, each operation rounded in this order: d = W - Z, s = d + U,
+ * r = rho * s, t = Gf + r, q = lr * t, W' = W - q.  Gf is the loss gradient from
+ * the caller's backward pass.  mask is a group mask as structadmm_project writes
+ * it for (A, B, C, D, kind): group of entry (a, b, c, d) = a (filter), b
+ * (channel), (b*C + c)*D + d (shape), the entry itself (element).
+ * W is updated in place.  Float arrays: [A,B,C,D] binary32, 16-byte aligned;
+ * Z and U are both given or both NULL; Gf may not alias W.
+ */
+typedef struct sa_sgd_desc {
+    int64_t A, B, C, D;      /* shape; A*B*C*D < 2^31 */
+    int32_t kind;            /* group map of mask: SA_FILTER .. SA_ELEMENT */
+    const uint8_t *mask;     /* [n_groups] (1 = kept) or NULL */
+    float *W;                /* in/out */
+    const float *Gf;         /* loss gradient */
+    const float *Z;          /* NULL: no ADMM term */
+    const float *U;          /* NULL exactly when Z is NULL */
+    float rho;
+    float lr;
+} sa_sgd_desc;
+
+int structadmm_sgd_step(const sa_sgd_desc *layers, int n_layers, hipStream_t stream);
+
 /* ---- compaction: structadmm_compact --------------------------------- */
 /*
  * Builds, per conv group gc, the dense GEMM matrix that remains after row and

@@ -54,6 +54,8 @@ def lib():
         L.oracle_project.restype = ctypes.c_int
         L.oracle_dual_update.argtypes = [i64, vp, vp, vp, f32, vp, i32]
         L.oracle_dual_update.restype = None
+        L.oracle_sgd_step.argtypes = [i64, i64, i64, i64, i32, vp, vp, vp, vp, vp, f32, f32]
+        L.oracle_sgd_step.restype = None
         L.oracle_bf16_array.argtypes = [i64, vp, vp]
         L.oracle_bf16_array.restype = None
         L.oracle_compact.argtypes = [i64, i64, i64, i64, i32, vp, vp, vp, vp, vp, i32,
@@ -117,6 +119,20 @@ def dual_update(W, Z, U, rho: float, update_dual: bool = True, want_grad: bool =
     lib().oracle_dual_update(W.size, _p(W), _p(Z), _p(U), ctypes.c_float(rho), _p(G),
                              1 if update_dual else 0)
     return U, G
+
+
+def sgd_step(W, Gf, Z=None, U=None, mask=None, kind: int = FILTER, rho: float = 0.0, lr: float = 0.01):
+    """One SGD step of the W-subproblem / masked retraining; returns the new W
+    (W [A,B,C,D] is not modified)."""
+    W = np.array(W, dtype=np.float32, copy=True)
+    A, B, C, D = W.shape
+    Gf = _c(Gf, np.float32)
+    Z = None if Z is None else _c(Z, np.float32)
+    U = None if U is None else _c(U, np.float32)
+    mask = None if mask is None else _c(mask, np.uint8)
+    lib().oracle_sgd_step(A, B, C, D, kind, _p(mask), _p(W), _p(Gf), _p(Z), _p(U),
+                          ctypes.c_float(rho), ctypes.c_float(lr))
+    return W
 
 
 def bf16_bits(x) -> np.ndarray:

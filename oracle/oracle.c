@@ -224,6 +224,33 @@ void oracle_dual_update(int64_t n, const float *W, const float *Z, float *U, flo
     }
 }
 
+/* One SGD step of the W-subproblem (Section 4, eq. (3)) or of masked
+ * retraining ("Masked mapping and retraining": pruned weights stay zero):
+ * t = Gf + rho * ((W - Z) + U) (t = Gf without Z), then
+ * W' = kept(group of the entry) ? W - lr * t : +0, every entry kept when mask
+ * is NULL.  Each binary32 operation is rounded on its own, in that order. */
+void oracle_sgd_step(int64_t A, int64_t B, int64_t C, int64_t D, int32_t kind,
+                     const uint8_t *mask, float *W, const float *Gf, const float *Z,
+                     const float *U, float rho, float lr)
+{
+    for (int64_t a = 0; a < A; ++a)
+        for (int64_t b = 0; b < B; ++b)
+            for (int64_t c = 0; c < C; ++c)
+                for (int64_t d = 0; d < D; ++d) {
+                    int64_t e = ((a * B + b) * C + c) * D + d;
+                    int keep = !mask || mask[group_of(a, b, c, d, B, C, D, kind)];
+                    float t = Gf[e];
+                    if (Z) {
+                        float w_minus_z = W[e] - Z[e];
+                        float s = w_minus_z + U[e];
+                        float r = rho * s;
+                        t = Gf[e] + r;
+                    }
+                    float q = lr * t;
+                    W[e] = keep ? W[e] - q : 0.0f;
+                }
+}
+
 /* binary32 -> bfloat16 with round to nearest, ties to even, on the 16
  * discarded bits (NaN kept quiet). */
 uint16_t oracle_bf16_rne(float x)

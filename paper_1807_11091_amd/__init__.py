@@ -9,6 +9,7 @@ Entry points (same names as the C ABI):
   project(layers, ws=None, stream=None)
   project_workspace(layers)
   dual_update(layers, stream=None)
+  sgd_step(items, stream=None)
   compact(Z, groups, ..., ws=None, stream=None) -> (Wc, row_idx, col_ch, col_tap, sizes)
   pack_nhwc(X, keep=None, Cx=None, stream=None)
   conv_fwd(X, Wc, col_ch, col_tap, sizes, C, D, stride, pad, Y=None, stream=None)
@@ -42,6 +43,12 @@ class ProjectDesc(ctypes.Structure):
 class DualDesc(ctypes.Structure):
     _fields_ = [("n", ctypes.c_int64), ("W", _vp), ("Z", _vp), ("U", _vp), ("rho", ctypes.c_float),
                 ("G", _vp), ("update_dual", ctypes.c_int32)]
+
+
+class SgdDesc(ctypes.Structure):
+    _fields_ = [("A", ctypes.c_int64), ("B", ctypes.c_int64), ("C", ctypes.c_int64), ("D", ctypes.c_int64),
+                ("kind", ctypes.c_int32), ("mask", _vp), ("W", _vp), ("Gf", _vp), ("Z", _vp), ("U", _vp),
+                ("rho", ctypes.c_float), ("lr", ctypes.c_float)]
 
 
 class CompactDesc(ctypes.Structure):
@@ -95,6 +102,8 @@ def lib():
         L.structadmm_project.restype = ctypes.c_int
         L.structadmm_dual_update.argtypes = [ctypes.POINTER(DualDesc), ctypes.c_int, _vp]
         L.structadmm_dual_update.restype = ctypes.c_int
+        L.structadmm_sgd_step.argtypes = [ctypes.POINTER(SgdDesc), ctypes.c_int, _vp]
+        L.structadmm_sgd_step.restype = ctypes.c_int
         L.structadmm_compact.argtypes = [ctypes.POINTER(CompactDesc), ctypes.POINTER(CompactSizes), _vp]
         L.structadmm_compact.restype = ctypes.c_int
         L.structadmm_pack_nhwc.argtypes = [_vp, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
@@ -182,6 +191,23 @@ def dual_descs(items) -> "ctypes.Array":
 def dual_update(items, stream=None, descs=None):
     d = descs if descs is not None else dual_descs(items)
     _check(lib().structadmm_dual_update(d, len(d), _stream(stream)), "structadmm_dual_update")
+
+
+def sgd_descs(items) -> "ctypes.Array":
+    """items: iterable of (W, Gf, Z, U, mask, kind, rho, lr); W is [A,B,C,D];
+    Z, U and mask may be None."""
+    items = list(items)
+    arr = (SgdDesc * len(items))()
+    for i, (W, Gf, Z, U, mask, kind, rho, lr) in enumerate(items):
+        A, B, C, D = W.shape
+        arr[i] = SgdDesc(A, B, C, D, kind, _ptr(mask), _ptr(W), _ptr(Gf), _ptr(Z), _ptr(U), rho, lr)
+    return arr
+
+
+def sgd_step(items, stream=None, descs=None):
+    """structadmm_sgd_step: W <- keep ? W - lr * (Gf + rho((W - Z) + U)) : 0, in place."""
+    d = descs if descs is not None else sgd_descs(items)
+    _check(lib().structadmm_sgd_step(d, len(d), _stream(stream)), "structadmm_sgd_step")
 
 
 def compact(Z, groups: int = 1, row_mask=None, col_mask=None, chan_mask=None, in_ch_mask=None,

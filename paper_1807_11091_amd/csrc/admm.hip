@@ -1,6 +1,7 @@
 // gfx950 kernels and entry points of the ADMM Z-update (projection onto the
-// sparsity sets of Section 3, as solved in Section 4) and of the dual update /
-// gradient of eq. (3).
+// sparsity sets of Section 3, as solved in Section 4), of the dual update /
+// gradient of eq. (3), and of the W-subproblem's SGD step, also used for masked
+// retraining (k_sgd).
 //
 // Data flow of structadmm_project for one dependency level of layers:
 //   k_expand_allowed  (layers with an input-channel support) per-column support bytes
@@ -98,6 +99,22 @@ struct DualLayer {
 };
 struct DualTab {
     DualLayer L[kTab];
+    int32_t begin[kTab + 1];
+    int32_t nl;
+};
+
+struct SgdLayer {
+    float *W;
+    const float *Gf;
+    const float *Z;
+    const float *U;
+    const uint8_t *mask;
+    int32_t n, kind;
+    FastDiv divK, divCD;  // entry -> filter, column -> channel
+    float rho, lr;
+};
+struct SgdTab {
+    SgdLayer L[kTab];
     int32_t begin[kTab + 1];
     int32_t nl;
 };
@@ -435,7 +452,7 @@ struct ApplyTab {
 };
 
 static_assert(sizeof(RowTab) < 4096 && sizeof(ColTab) < 4096 && sizeof(SelTab) < 4096 &&
-                  sizeof(DualTab) < 4096 && sizeof(ApplyTab) < 4096,
+                  sizeof(DualTab) < 4096 && sizeof(ApplyTab) < 4096 && sizeof(SgdTab) < 4096,
               "layer tables must fit the kernel-argument segment");
 
 constexpr int kApplyThreads = 256;
@@ -805,6 +822,68 @@ __global__ __launch_bounds__(kDualThreads) void k_dual(DualTab tab) {
     }
 }
 
+// ---------------------------------------------------------------- SGD step
+constexpr int kSgdThreads = 256;
+constexpr int kSgdVecPerThread = 4;
+constexpr int kSgdChunk = kSgdThreads * kSgdVecPerThread * 4;
+
+__device__ inline bool sgd_keep(const SgdLayer &L, uint32_t e) {
+    if (!L.mask) return true;
+    uint32_t g = e;
+    if (L.kind != SA_ELEMENT) {
+        const uint32_t a = fdiv(e, L.divK);
+        const uint32_t j = e - a * L.divK.d;  // column (b*C + c)*D + d
+        g = L.kind == SA_FILTER ? a : L.kind == SA_CHANNEL ? fdiv(j, L.divCD) : j;
+    }
+    return L.mask[g] != 0;
+}
+
+// t = Gf + rho * ((W - Z) + U) (or Gf);  W <- keep ? W - lr * t : +0
+__device__ inline float sgd_one(const SgdLayer &L, float w, float gf, float z, float u, bool keep) {
+    float t = gf;
+    if (L.Z) {
+        const float d = w - z;
+        const float sum = d + u;
+        const float r = L.rho * sum;
+        t = gf + r;
+    }
+    const float q = L.lr * t;
+    return keep ? w - q : 0.0f;
+}
+
+__global__ __launch_bounds__(kSgdThreads) void k_sgd(SgdTab tab) {
+    const int li = find_layer(tab.begin, tab.nl, blockIdx.x);
+    const SgdLayer &L = tab.L[li];
+    const int64_t c0 = (int64_t)(blockIdx.x - tab.begin[li]) * kSgdChunk;
+    const int n4 = L.n >> 2;
+#pragma unroll
+    for (int v = 0; v < kSgdVecPerThread; ++v) {
+        const int64_t i = (c0 >> 2) + (int64_t)v * kSgdThreads + threadIdx.x;
+        if (i < n4) {
+            const float4 w = reinterpret_cast<const float4 *>(L.W)[i];
+            const float4 g = reinterpret_cast<const float4 *>(L.Gf)[i];
+            float4 z = make_float4(0.f, 0.f, 0.f, 0.f), u = z;
+            if (L.Z) {
+                z = reinterpret_cast<const float4 *>(L.Z)[i];
+                u = reinterpret_cast<const float4 *>(L.U)[i];
+            }
+            const uint32_t e = (uint32_t)i * 4u;
+            float4 o;
+            o.x = sgd_one(L, w.x, g.x, z.x, u.x, sgd_keep(L, e));
+            o.y = sgd_one(L, w.y, g.y, z.y, u.y, sgd_keep(L, e + 1));
+            o.z = sgd_one(L, w.z, g.z, z.z, u.z, sgd_keep(L, e + 2));
+            o.w = sgd_one(L, w.w, g.w, z.w, u.w, sgd_keep(L, e + 3));
+            reinterpret_cast<float4 *>(L.W)[i] = o;
+        }
+    }
+    // scalar tail (n % 4 entries), handled by the layer's first workgroup
+    if (blockIdx.x == tab.begin[li] && threadIdx.x < (L.n & 3)) {
+        const uint32_t e = (uint32_t)n4 * 4u + threadIdx.x;
+        const float z = L.Z ? L.Z[e] : 0.f, u = L.Z ? L.U[e] : 0.f;
+        L.W[e] = sgd_one(L, L.W[e], L.Gf[e], z, u, sgd_keep(L, e));
+    }
+}
+
 // ---------------------------------------------------------------- host planning
 struct LayerPlan {
     int64_t G;
@@ -1154,6 +1233,41 @@ extern "C" int structadmm_dual_update(const sa_dual_desc *layers, int n_layers, 
         tab.begin[tab.nl] = blocks;
         hipLaunchKernelGGL(k_dual, dim3(blocks), dim3(kDualThreads), 0, stream, tab);
         if (int rc = launch_check("k_dual")) return rc;
+    }
+    return SA_OK;
+}
+
+extern "C" int structadmm_sgd_step(const sa_sgd_desc *layers, int n_layers, hipStream_t stream) {
+    clear_error();
+    if (!layers || n_layers <= 0) return fail(SA_E_ARG, "sgd_step: layers must be a non-empty array");
+    for (int i = 0; i < n_layers; ++i)
+        if (int rc = validate_sgd(layers[i], i)) return rc;
+    for (int s = 0; s < n_layers; s += kTab) {
+        SgdTab tab;
+        memset(&tab, 0, sizeof tab);
+        tab.nl = std::min(kTab, n_layers - s);
+        int blocks = 0;
+        for (int t = 0; t < tab.nl; ++t) {
+            const sa_sgd_desc &d = layers[s + t];
+            SgdLayer &L = tab.L[t];
+            const int64_t n = d.A * d.B * d.C * d.D;
+            L.W = d.W;
+            L.Gf = d.Gf;
+            L.Z = d.Z;
+            L.U = d.U;
+            L.mask = d.mask;
+            L.n = (int32_t)n;
+            L.kind = d.kind;
+            L.divK = make_fastdiv((uint32_t)(d.B * d.C * d.D));
+            L.divCD = make_fastdiv((uint32_t)(d.C * d.D));
+            L.rho = d.rho;
+            L.lr = d.lr;
+            tab.begin[t] = blocks;
+            blocks += (int)std::max<int64_t>(1, (n + kSgdChunk - 1) / kSgdChunk);
+        }
+        tab.begin[tab.nl] = blocks;
+        hipLaunchKernelGGL(k_sgd, dim3(blocks), dim3(kSgdThreads), 0, stream, tab);
+        if (int rc = launch_check("k_sgd")) return rc;
     }
     return SA_OK;
 }

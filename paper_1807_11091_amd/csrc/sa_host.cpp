@@ -71,6 +71,20 @@ int validate_dual(const sa_dual_desc &d, int i) {
     return SA_OK;
 }
 
+int validate_sgd(const sa_sgd_desc &d, int i) {
+    if (d.A <= 0 || d.B <= 0 || d.C <= 0 || d.D <= 0)
+        return fail(SA_E_ARG, "layer %d: shape must be positive", i);
+    if (d.A > kMaxElems / d.B || d.A * d.B > kMaxElems / (d.C * d.D))
+        return fail(SA_E_ARG, "layer %d: A*B*C*D must be below 2^31", i);
+    if (d.kind < SA_FILTER || d.kind > SA_ELEMENT) return fail(SA_E_ARG, "layer %d: unknown kind %d", i, d.kind);
+    if (!d.W || !d.Gf) return fail(SA_E_ARG, "layer %d: W and Gf are required", i);
+    if ((d.Z == nullptr) != (d.U == nullptr)) return fail(SA_E_ARG, "layer %d: give both Z and U or neither", i);
+    if (d.Gf == d.W) return fail(SA_E_ARG, "layer %d: Gf must not alias W", i);
+    if (!aligned(d.W, 16) || !aligned(d.Gf, 16) || (d.Z && (!aligned(d.Z, 16) || !aligned(d.U, 16))))
+        return fail(SA_E_ALIGN, "layer %d: W, Gf, Z and U must be 16-byte aligned", i);
+    return SA_OK;
+}
+
 int validate_compact(const sa_compact_desc &d) {
     if (d.A <= 0 || d.B <= 0 || d.C <= 0 || d.D <= 0)
         return fail(SA_E_ARG, "compact: shape must be positive");

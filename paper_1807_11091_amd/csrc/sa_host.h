@@ -32,6 +32,7 @@ inline int64_t n_groups(const sa_project_desc &d) {
 // Host validation of one projection descriptor (index i for messages).
 int validate_project(const sa_project_desc &d, int i);
 int validate_dual(const sa_dual_desc &d, int i);
+int validate_sgd(const sa_sgd_desc &d, int i);
 int validate_compact(const sa_compact_desc &d);
 int validate_conv(const sa_conv_desc &d);
 

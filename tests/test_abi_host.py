@@ -26,7 +26,7 @@ def declared_functions():
 def test_library_exports_every_declared_symbol():
     names = declared_functions()
     assert {"structadmm_project", "structadmm_project_workspace", "structadmm_dual_update",
-            "structadmm_compact", "structadmm_conv_fwd", "structadmm_pack_nhwc",
+            "structadmm_compact", "structadmm_conv_fwd", "structadmm_pack_nhwc", "structadmm_sgd_step",
             "structadmm_last_error", "structadmm_version"} <= names
     L = sa.lib()
     for n in names:
@@ -41,6 +41,7 @@ def _c_layout():
     fields = {
         "sa_project_desc": ("ProjectDesc", ["A", "groups", "kind", "k", "W", "in_ch_mask", "scores", "rho", "G"]),
         "sa_dual_desc": ("DualDesc", ["n", "W", "U", "rho", "G", "update_dual"]),
+        "sa_sgd_desc": ("SgdDesc", ["A", "kind", "mask", "W", "Gf", "Z", "U", "rho", "lr"]),
         "sa_compact_desc": ("CompactDesc", ["groups", "Z", "in_compacted", "Wc", "ws"]),
         "sa_compact_sizes": ("CompactSizes", ["M", "K", "ldk", "wc_offset", "row_offset", "run", "run_base",
                                               "ch_lo", "ch_span"]),
@@ -129,6 +130,25 @@ def test_dual_validation():
     assert call(update_dual=0, G=None) == -1
     assert call(Z=FAKE + 4) == -2
     assert L.structadmm_dual_update(None, 1, None) == -1
+
+
+def test_sgd_validation():
+    L = sa.lib()
+    def call(**kw):
+        d = dict(A=4, B=2, C=3, D=3, kind=sa.FILTER, mask=None, W=FAKE, Gf=FAKE + 256, Z=None, U=None,
+                 rho=0.1, lr=0.01)
+        d.update(kw)
+        return L.structadmm_sgd_step((sa.SgdDesc * 1)(sa.SgdDesc(**d)), 1, None)
+    assert call(A=0) == -1
+    assert call(kind=9) == -1
+    assert call(W=None) == -1
+    assert call(Gf=None) == -1
+    assert call(Z=FAKE + 512) == -1          # Z without U
+    assert call(Gf=FAKE) == -1               # Gf aliases W
+    assert call(W=FAKE + 4) == -2
+    assert call(Z=FAKE + 512, U=FAKE + 1024 + 8) == -2
+    assert call(A=1 << 16, B=1 << 16) == -1
+    assert L.structadmm_sgd_step(None, 1, None) == -1
 
 
 def test_compact_and_conv_validation():
