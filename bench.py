@@ -51,6 +51,8 @@ def parse():
     p.add_argument("--suite", metavar="JSON", default=None,
                    help="measure every workload (ADMM one-call and replicated, CONV per layer against "
                         "MIOpen, density sweep, achievable peaks) and write the report to JSON")
+    p.add_argument("--tables", metavar="JSON", default=None,
+                   help="only the batch-1 replay of the pruned AlexNet layers of Tables 1-2 (CONV speedups)")
     p.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                    help="only copy MIB MiB device-to-device 5 times (HBM counter calibration) and exit")
     return p.parse_args()
@@ -243,6 +245,103 @@ def _time(torch, fn, reps=20, warm=5, trials=5):
     return {"median_ms": t[len(t) // 2], "p10_ms": t[0], "p90_ms": t[-1]}
 
 
+def _time_graph(torch, fn, reps=20, warm=3, trials=5):
+    """Per-call GPU time (ms) of fn, from a HIP graph of reps calls replayed
+    between two events: no host enqueue gaps (for calls of a few microseconds).
+    fn must enqueue on the current stream only; median, min and max over trials."""
+    for _ in range(warm):
+        fn()
+    torch.cuda.synchronize()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        fn()
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for _ in range(reps):
+            fn()
+    torch.cuda.synchronize()
+    g.replay()
+    torch.cuda.synchronize()
+    t = []
+    for _ in range(trials):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        g.replay()
+        b.record()
+        torch.cuda.synchronize()
+        t.append(a.elapsed_time(b) / reps)
+    t.sort()
+    del g
+    return {"median_ms": t[len(t) // 2], "p10_ms": t[0], "p90_ms": t[-1]}
+
+
+def suite_tables(torch, sa):
+    """Batch-1 CONVs of AlexNet conv1-5 pruned to the per-layer row / column
+    sparsities of Tables 1-2 (masks drawn by projecting the synthetic weights),
+    against the same-shape dense CONV; GPU times from graph replays."""
+    import torch.nn.functional as F
+    from workloads import PAPER_TABLE_SPARSITY, WORKLOADS, input_nchw, kept_from_sparsity, layer_tensors
+    wl = WORKLOADS["alexnet_shape30"]
+    res = {}
+    for block, table in PAPER_TABLE_SPARSITY.items():
+        rows_out = []
+        for li, L in enumerate(wl.layers):
+            rs, cs = table[L.name]
+            W, U = layer_tensors(wl, li)
+            dW, dU = torch.from_numpy(W).cuda(), torch.from_numpy(U).cuda()
+            masks = []
+            for kind, sp, G in ((sa.FILTER, rs, L.A), (sa.SHAPE, cs, L.K)):
+                if sp == 0.0:
+                    masks.append(None)
+                    continue
+                k = kept_from_sparsity(sp, G)
+                mask = torch.empty(G, dtype=torch.uint8, device="cuda")
+                kept = torch.empty(max(k, 1), dtype=torch.int32, device="cuda")
+                lay = sa.ProjectLayer(dW, dU, torch.empty_like(dW), mask, kept, kind, k, L.groups)
+                ws = torch.empty(max(256, sa.project_workspace([lay])), dtype=torch.uint8, device="cuda")
+                sa.project([lay], ws)
+                masks.append(mask)
+            Wc, ri, cc, ct, sz = sa.compact(dW, L.groups, row_mask=masks[0], col_mask=masks[1])
+            Wd, rid, ccd, ctd, szd = sa.compact(dW, L.groups)
+            X = torch.from_numpy(input_nchw(wl, li, batch=1)).cuda()
+            Xp = sa.pack_nhwc(X)
+            need = max(sa.conv_workspace(Xp, sz, L.C, L.D, L.stride, L.pad),
+                       sa.conv_workspace(Xp, szd, L.C, L.D, L.stride, L.pad), 256)
+            cws = torch.empty(need, dtype=torch.uint8, device="cuda")
+            Yc = sa.conv_fwd(Xp, Wc, cc, ct, sz, L.C, L.D, L.stride, L.pad, ws=cws)
+            Yd = sa.conv_fwd(Xp, Wd, ccd, ctd, szd, L.C, L.D, L.stride, L.pad, ws=cws)
+            dc = sa.conv_desc(Xp, Wc, cc, ct, sz, L.C, L.D, L.stride, L.pad, Yc, cws)
+            dd = sa.conv_desc(Xp, Wd, ccd, ctd, szd, L.C, L.D, L.stride, L.pad, Yd, cws)
+            tc = _time_graph(torch, lambda: sa.conv_fwd(None, None, None, None, sz, 0, 0, 0, 0, desc=dc))
+            td = _time_graph(torch, lambda: sa.conv_fwd(None, None, None, None, szd, 0, 0, 0, 0, desc=dd))
+            xb, wb = X.to(torch.bfloat16), dW.to(torch.bfloat16)
+            conv = lambda: F.conv2d(xb, wb, stride=L.stride, padding=L.pad, groups=L.groups)
+            try:
+                tm = _time_graph(torch, conv)
+            except RuntimeError:  # a library path that cannot be captured: events around eager calls
+                torch.cuda.synchronize()
+                tm = _time(torch, conv)
+            best = min(td["median_ms"], tm["median_ms"])
+            fc = 2 * L.P * L.Q * sum(sz.M[g] * sz.K[g] for g in range(sz.groups))
+            rows_out.append({"layer": L.name, "row_sparsity_pct": rs, "column_sparsity_pct": cs,
+                             "kept_rows": [sz.M[g] for g in range(sz.groups)], "kept_cols": sz.K[0],
+                             "compact_us": round(tc["median_ms"] * 1e3, 2), "dense_us": round(td["median_ms"] * 1e3, 2),
+                             "miopen_dense_us": round(tm["median_ms"] * 1e3, 2),
+                             "speedup_vs_own_dense": round(td["median_ms"] / tc["median_ms"], 3),
+                             "speedup_vs_best_dense": round(best / tc["median_ms"], 3),
+                             "compact_gflop": round(fc / 1e9, 4)})
+        c25 = sum(r["compact_us"] for r in rows_out[1:])
+        d25 = sum(r["dense_us"] for r in rows_out[1:])
+        b25 = sum(min(r["dense_us"], r["miopen_dense_us"]) for r in rows_out[1:])
+        res[block] = {"layers": rows_out, "conv2_5_compact_us": round(c25, 2),
+                      "conv2_5_speedup_vs_own_dense": round(d25 / c25, 3),
+                      "conv2_5_speedup_vs_best_dense": round(b25 / c25, 3)}
+    return res
+
+
 def _admm_layers(torch, sa, wl, variant, copies=1):
     """Device tensors of every layer (times copies) for one projection call."""
     from workloads import layer_tensors
@@ -277,6 +376,14 @@ def suite_admm(torch, sa, wl, variant):
         pd, dd = sa._descs(layers), sa.dual_descs(grads)
         tp = _time(torch, lambda: sa.project(layers, ws, descs=pd))
         tg = _time(torch, lambda: sa.dual_update(None, descs=dd))
+        # SGD steps on the same layers: the W-subproblem's step (loss gradient
+        # plus the ADMM term: read W, Gf, Z, U, write W = 20 B/weight) and the
+        # masked-retraining step (read W, Gf, write W = 12 B/weight)
+        gfs = [torch.zeros_like(l.W) for l in layers]
+        sd_admm = sa.sgd_descs([(l.W, gf, l.Z, l.U, None, l.kind, wl.rho, 1e-3) for l, gf in zip(layers, gfs)])
+        sd_mask = sa.sgd_descs([(l.W, gf, None, None, l.mask, l.kind, 0.0, 1e-3) for l, gf in zip(layers, gfs)])
+        ts = _time(torch, lambda: sa.sgd_step(None, descs=sd_admm))
+        tm = _time(torch, lambda: sa.sgd_step(None, descs=sd_mask))
         nn = n * copies
         step = tp["median_ms"] + tg["median_ms"]
         res[label] = {"copies": copies,
@@ -284,8 +391,10 @@ def suite_admm(torch, sa, wl, variant):
                       "gradient_us": round(tg["median_ms"] * 1e3, 2), "gradient_GBps": round(16 * nn / tg["median_ms"] / 1e6, 1),
                       "step_us": round(step * 1e3, 2), "step_GBps": round(36 * nn / step / 1e6, 1),
                       "step_frac_of_8TBps": round(36 * nn / step / 1e6 / HBM_PEAK_GBS, 4),
-                      "project_min_max_us": [round(tp["p10_ms"] * 1e3, 2), round(tp["p90_ms"] * 1e3, 2)]}
-        del layers, grads, ws
+                      "project_min_max_us": [round(tp["p10_ms"] * 1e3, 2), round(tp["p90_ms"] * 1e3, 2)],
+                      "sgd_admm_us": round(ts["median_ms"] * 1e3, 2), "sgd_admm_GBps": round(20 * nn / ts["median_ms"] / 1e6, 1),
+                      "sgd_masked_us": round(tm["median_ms"] * 1e3, 2), "sgd_masked_GBps": round(12 * nn / tm["median_ms"] / 1e6, 1)}
+        del layers, grads, ws, gfs
         torch.cuda.empty_cache()
     return res
 
@@ -435,15 +544,36 @@ def suite(path):
         print("sweep", json.dumps({"kind": r["kind"], "percent": p, "speedup": r["conv"]["speedup_vs_best_dense"]}),
               flush=True)
         torch.cuda.empty_cache()
+    rep["tables_batch1"] = suite_tables(torch, sa)
+    print("tables", json.dumps({b: v["conv2_5_speedup_vs_best_dense"] for b, v in rep["tables_batch1"].items()}),
+          flush=True)
     with open(path, "w") as f:
         json.dump(rep, f, indent=1)
     print("suite written to", path)
+
+
+def tables(path):
+    import torch
+    import paper_1807_11091_amd as sa
+    if not torch.cuda.is_available():
+        raise SystemExit("bench.py needs a GPU")
+    sa.lib()
+    rep = suite_tables(torch, sa)
+    for b, v in rep.items():
+        print(b, json.dumps({k: x for k, x in v.items() if k != "layers"}), flush=True)
+        for r in v["layers"]:
+            print("   ", json.dumps(r), flush=True)
+    with open(path, "w") as f:
+        json.dump(rep, f, indent=1)
 
 
 def main():
     args = parse()
     if args.copy_probe:
         copy_probe(args.copy_probe)
+        return
+    if args.tables:
+        tables(args.tables)
         return
     if args.suite:
         suite(args.suite)

@@ -889,7 +889,16 @@ __global__ __launch_bounds__(256) void k_s2d_rows(S2dArgs a) {
         for (int u = 0; u < 4; ++u) {
             const int ch = base + u * 256 + (int)threadIdx.x;
             const int64_t off = a0 + (int64_t)ch * 16;
-            v[u] = bload16(xrs, (ch < nchunk && off >= 0 && off < (int64_t)a.x_bytes) ? (uint32_t)off : kInvalidOffset);
+            v[u] = bload16(xrs, (ch < nchunk && off >= 0 && off + 16 <= (int64_t)a.x_bytes) ? (uint32_t)off : kInvalidOffset);
+            // the chunk that holds the input's last bytes (a buffer load reads
+            // zero for a dword reaching past the range, and an odd element
+            // count leaves the last dword half inside): its elements one by one
+            if (ch < nchunk && off < (int64_t)a.x_bytes && off + 16 > (int64_t)a.x_bytes && off >= 0) {
+                uint32_t w[4] = {0, 0, 0, 0};
+                for (int q = 0; q < 8 && off + 2 * q < (int64_t)a.x_bytes; ++q)
+                    w[q >> 1] |= (uint32_t)a.X[(off >> 1) + q] << (16 * (q & 1));
+                v[u] = make_uint4(w[0], w[1], w[2], w[3]);
+            }
         }
 #pragma unroll
         for (int u = 0; u < 4; ++u) {

@@ -14,7 +14,7 @@ import oracle
 import paper_1807_11091_amd as sa
 from gpu_helpers import (DEV, GpuLayer, bf16_bits_to_f64, bitwise_equal, maxabs_over_rms, run_project,
                          to_dev, torch)
-from workloads import WORKLOADS, input_nchw, layer_tensors
+from workloads import PAPER_TABLE_SPARSITY, WORKLOADS, input_nchw, kept_from_sparsity, layer_tensors
 
 pytestmark = pytest.mark.gpu
 
@@ -135,6 +135,9 @@ SMALL = [
     # space-to-depth channels padded to 8 (ResNet stem shape), and channel padding only
     (2, 3, 30, 28, 20, 7, 7, 2, 3, 1, sa.FILTER, 0.6),
     (2, 3, 12, 11, 16, 3, 3, 1, 1, 1, sa.SHAPE, 0.5),
+    # inputs whose byte size is not a multiple of 4: the space-to-depth copy's last chunk
+    (1, 3, 13, 13, 16, 3, 3, 2, 1, 1, sa.SHAPE, 0.5),
+    (1, 3, 11, 9, 8, 3, 3, 1, 1, 1, sa.FILTER, 0.5),
     # odd numbers of kept filters: output rows not 16-byte aligned
     (2, 16, 9, 9, 38, 1, 1, 1, 0, 1, sa.FILTER, 0.6),
     (2, 32, 8, 8, 50, 3, 3, 1, 1, 2, sa.FILTER, 0.62),
@@ -262,6 +265,45 @@ def test_conv_workload_resnet50_sampled_layers():
 @pytest.mark.parametrize("variant", [0, 2, 3, 5, 6, 8])
 def test_conv_workload_sweep(variant):
     workload_conv("resnet50_s3_sweep", variant=variant)
+
+
+def table_masks(W, U, L, block):
+    """Row (filter) and column (filter-shape) masks with the per-layer
+    sparsities of the pruned AlexNet models of Tables 1-2, drawn by projecting
+    the layer's synthetic V = W + U; GPU and oracle masks must agree."""
+    rs, cs = PAPER_TABLE_SPARSITY[block][L.name]
+    out = []
+    for kind, sp, G in ((sa.FILTER, rs, L.A), (sa.SHAPE, cs, L.K)):
+        if sp == 0.0:
+            out.append(None)
+            continue
+        k = kept_from_sparsity(sp, G)
+        ref = oracle.project(W, U, kind, k, L.groups)
+        got = run_project([GpuLayer(W, U, kind, k, L.groups)])[0]
+        assert np.array_equal(got["mask"], ref["mask"])
+        out.append(ref["mask"])
+    return out
+
+
+@pytest.mark.parametrize("block", list(PAPER_TABLE_SPARSITY))
+def test_conv_table_replay_batch1(block):
+    """The batch-1 CONVs of AlexNet conv1-5 pruned to the row / column
+    sparsities of Tables 1-2 (rows and columns removed together)."""
+    wl = WORKLOADS["alexnet_shape30"]
+    for li, L in enumerate(wl.layers):
+        W, U = layer_tensors(wl, li)
+        rows, cols = table_masks(W, U, L, block)
+        dW = to_dev(W)
+        got = sa.compact(dW, L.groups, row_mask=None if rows is None else to_dev(rows),
+                         col_mask=None if cols is None else to_dev(cols))
+        rc = oracle.compact(W, L.groups, row_mask=rows, col_mask=cols)
+        check_compact(got, rc)
+        X = input_nchw(wl, li, batch=1)
+        Xp = sa.pack_nhwc(to_dev(X))
+        Y = sa.conv_fwd(Xp, got[0], got[2], got[3], got[4], L.C, L.D, L.stride, L.pad)
+        Yr = oracle.conv(oracle.pack(X), rc, L.C, L.D, L.stride, L.pad)
+        err = maxabs_over_rms(bf16_bits_to_f64(Y.cpu().numpy()), Yr)
+        assert err <= TOL, (block, L.name, err)
 
 
 def test_conv_is_deterministic():

@@ -168,5 +168,27 @@ WORKLOADS = {
 }
 
 
+# Per-layer row (filter) and column (filter-shape) sparsity, in percent, of the
+# pruned AlexNet models whose batch-1 CONV speedups Tables 1 and 2 report
+# (Table 1: column pruning at 0% accuracy loss; Table 2: row and column pruning
+# at 0.7% and 2.0% loss, with the same row sparsities in both).  Only these
+# counts are taken; the masks are drawn by projecting synthetic weights.
+PAPER_TABLE_SPARSITY = {
+    "table1": {"conv1": (0.0, 0.0), "conv2": (0.0, 70.0), "conv3": (0.0, 77.0), "conv4": (0.0, 85.0),
+               "conv5": (0.0, 81.0)},
+    "table2_loss0.7": {"conv1": (9.4, 0.0), "conv2": (12.9, 63.9), "conv3": (40.6, 78.1), "conv4": (46.9, 87.0),
+                       "conv5": (0.0, 84.9)},
+    "table2_loss2.0": {"conv1": (9.4, 0.0), "conv2": (12.9, 87.5), "conv3": (40.6, 90.0), "conv4": (46.9, 90.5),
+                       "conv5": (0.0, 90.7)},
+}
+
+
+def kept_from_sparsity(sparsity_percent: float, n_groups: int) -> int:
+    """Groups kept when sparsity_percent of n_groups are pruned (pruned count
+    rounded half up)."""
+    pruned = int(sparsity_percent * n_groups / 100.0 + 0.5)
+    return n_groups - pruned
+
+
 def get_workload(name: str) -> Workload:
     return WORKLOADS[name]
