@@ -297,22 +297,6 @@ __global__ __launch_bounds__(kColThreads) void k_col_partials(ColTab tab) {
 // 64-bit keys (eight 8-bit digits, one LDS histogram per digit), and the ties
 // are ranked by an ordered scan in index order.  Counting is order-free and
 // the scans have a fixed order, so the result is reproducible.
-// s + p[0] + p[stride] + ... + p[(n-1)*stride], added in that order; the
-// loads of each group of 8 are issued together (latency, not bandwidth,
-// bounds this reduction).
-__device__ inline double sum_bands(const double *p, int stride, int n, double s) {
-    int b = 0;
-    for (; b + 8 <= n; b += 8) {
-        double v[8];
-#pragma unroll
-        for (int q = 0; q < 8; ++q) v[q] = p[(int64_t)(b + q) * stride];
-#pragma unroll
-        for (int q = 0; q < 8; ++q) s += v[q];
-    }
-    for (; b < n; ++b) s += p[(int64_t)b * stride];
-    return s;
-}
-
 __global__ __launch_bounds__(kSelThreads) void k_select(SelTab tab) {
     __shared__ uint64_t skey[SA_MAX_STRUCT_GROUPS];
     __shared__ uint8_t smask[SA_MAX_STRUCT_GROUPS];
@@ -335,11 +319,29 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelTab tab) {
             } else {
                 s = L.scores[g];
             }
-        } else if (L.kind == SA_SHAPE) {
-            s = sum_bands(L.partials + g, L.K, L.nbands, 0.0);
-        } else {  // channel: over taps, then bands
+        } else {
+            // shape: over bands; channel: over taps, then bands.  The terms are
+            // loaded 16 at a time (every load in flight together) and added in
+            // that order; the padding terms past the end add +0 to a sum of
+            // squares, which leaves it unchanged.
+            const int taps = L.kind == SA_SHAPE ? 1 : L.CD, nb = L.nbands;
+            const double *base = L.partials + (L.kind == SA_SHAPE ? g : g * L.CD);
+            const int n = taps * nb;
+            int t = 0, b = 0;
             s = 0.0;
-            for (int t = 0; t < L.CD; ++t) s = sum_bands(L.partials + g * L.CD + t, L.K, L.nbands, s);
+            for (int i0 = 0; i0 < n; i0 += 16) {
+                double v[16];
+#pragma unroll
+                for (int q = 0; q < 16; ++q) {
+                    v[q] = i0 + q < n ? base[(int64_t)b * L.K + t] : 0.0;
+                    if (++b == nb) {
+                        b = 0;
+                        ++t;
+                    }
+                }
+#pragma unroll
+                for (int q = 0; q < 16; ++q) s += v[q];
+            }
         }
         if (L.kind != SA_FILTER || L.rowpart) L.scores[g] = s;
         skey[g] = (uint64_t)__double_as_longlong(s);
@@ -356,9 +358,22 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelTab tab) {
         for (int shift = 56; shift >= 0; shift -= 8) {
             if (tid < 256) hist[tid] = 0;
             __syncthreads();
-            for (int g = tid; g < G; g += kSelThreads) {
-                const uint64_t key = skey[g];
-                if ((key & pmask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
+            // the keys of a wavefront that share the first matching key's
+            // digit are counted with one atomic (in the leading digits most
+            // keys share one bin)
+            for (int g0w = tid - lane; g0w < G; g0w += kSelThreads) {
+                const int g = g0w + lane;
+                const uint64_t key = g < G ? skey[g] : 0;
+                const bool in = g < G && (key & pmask) == prefix;
+                const uint32_t dig = (uint32_t)(key >> shift) & 255u;
+                const unsigned long long vm = __ballot(in);
+                if (vm) {
+                    const int leader = (int)__builtin_ctzll(vm);
+                    const uint32_t d0 = (uint32_t)__shfl((int)dig, leader);
+                    const unsigned long long same = __ballot(in && dig == d0);
+                    if (lane == leader) atomicAdd(&hist[d0], (uint32_t)__popcll(same));
+                    if (in && dig != d0) atomicAdd(&hist[dig], 1u);
+                }
             }
             __syncthreads();
             if (tid < kWave) {
