@@ -66,6 +66,11 @@ def lib():
         L.oracle_conv.argtypes = [i64, i64, i64, i64, vp, i32, i64, i64, i64, i64,
                                   vp, vp, vp, vp, vp, vp]
         L.oracle_conv.restype = None
+        L.oracle_csr.argtypes = [i64, i64, i64, i64, vp, vp, vp, vp, vp]
+        L.oracle_csr.restype = i64
+        L.oracle_conv_csr.argtypes = [i64, i64, i64, vp, i64, i64, i64, i64, i32, i64, i64,
+                                      vp, vp, vp, vp]
+        L.oracle_conv_csr.restype = None
         _lib = L
     return _lib
 
@@ -195,4 +200,38 @@ def conv(Xb, comp, C: int, D: int, stride: int, pad: int) -> np.ndarray:
     lib().oracle_conv(N, Cx, H, W, _p(Xb), groups, C, D, stride, pad,
                       _p(comp["Wc"]), _p(comp["M"]), _p(comp["K"]),
                       _p(comp["col_ch"]), _p(comp["col_tap"]), _p(Y))
+    return Y
+
+
+def csr(Z, mask) -> dict:
+    """CSR of a non-structured pruned layer's [A, B*C*D] GEMM matrix (kept
+    entries of ``mask``, bf16 values): dict with row_ptr, col, val."""
+    Z = _c(Z, np.float32)
+    A = Z.shape[0]
+    m = _c(mask, np.uint8).reshape(-1)
+    assert m.size == Z.size
+    nnz = int(np.count_nonzero(m))
+    row_ptr = np.empty(A + 1, np.int32)
+    col = np.empty(max(nnz, 1), np.int32)
+    val = np.empty(max(nnz, 1), np.uint16)
+    got = lib().oracle_csr(*Z.shape, _p(Z), _p(m), _p(row_ptr), _p(col), _p(val))
+    assert got == nnz
+    return {"row_ptr": row_ptr, "col": col[:nnz].copy(), "val": val[:nnz].copy()}
+
+
+def conv_csr(Xb, csr_, shape, groups: int, stride: int, pad: int) -> np.ndarray:
+    """fp64 CONV of a CSR layer of weight shape (A, B, C, D); Xb = bf16 bits
+    NCHW with groups*B channels.  Returns NHWC fp64 [N, P, Q, A]."""
+    Xb = np.ascontiguousarray(Xb, dtype=np.uint16)
+    N, Cx, H, W = Xb.shape
+    A, B, C, D = shape
+    assert Cx == groups * B and A % groups == 0
+    P = (H + 2 * pad - C) // stride + 1
+    Q = (W + 2 * pad - D) // stride + 1
+    Y = np.empty((N, P, Q, A), np.float64)
+    col = csr_["col"] if csr_["col"].size else np.zeros(1, np.int32)
+    val = csr_["val"] if csr_["val"].size else np.zeros(1, np.uint16)
+    lib().oracle_conv_csr(N, H, W, _p(Xb), A, B, C, D, groups, stride, pad,
+                          _p(_c(csr_["row_ptr"], np.int32)), _p(_c(col, np.int32)),
+                          _p(_c(val, np.uint16)), _p(Y))
     return Y

@@ -441,3 +441,63 @@ void oracle_conv(int64_t N, int64_t Cx, int64_t H, int64_t W, const uint16_t *Xb
             }
     }
 }
+
+/* The non-structured set of Section 3 keeps an arbitrary pattern of weights;
+ * the CONV of such a layer is a sparse-matrix product (Section 5 runs it with
+ * a CSR sparse library on the GPU).  CSR form of the [A, B*C*D] GEMM matrix:
+ * row a lists the columns j with mask[a*B*C*D + j] set, ascending, with values
+ * bf16(Z[a*B*C*D + j]) (round to nearest even); row_ptr has A + 1 entries.
+ * A kept entry whose value is zero stays an explicit entry.  Returns the
+ * number of entries. */
+int64_t oracle_csr(int64_t A, int64_t B, int64_t C, int64_t D, const float *Z,
+                   const uint8_t *mask, int32_t *row_ptr, int32_t *col, uint16_t *val)
+{
+    int64_t K = B * C * D, e = 0;
+    for (int64_t a = 0; a < A; ++a) {
+        row_ptr[a] = (int32_t)e;
+        for (int64_t j = 0; j < K; ++j) {
+            if (!mask[a * K + j])
+                continue;
+            col[e] = (int32_t)j;
+            val[e] = oracle_bf16_rne(Z[a * K + j]);
+            ++e;
+        }
+    }
+    row_ptr[A] = (int32_t)e;
+    return e;
+}
+
+/* CONV of a CSR layer, by definition: for filter a of conv group
+ * gc = a / (A / groups),
+ * Y[n, p, q, a] = sum over the entries e of row a of
+ *     val[e] * Xb[n, gc*B + b, p*stride - pad + c, q*stride - pad + d],
+ * where col[e] = (b*C + c)*D + d; zero outside the image; every product and
+ * sum in binary64, entries in row order.  Xb is bfloat16 NCHW
+ * [N, groups*B, H, W]; Y is binary64 NHWC [N, P, Q, A]. */
+void oracle_conv_csr(int64_t N, int64_t H, int64_t W, const uint16_t *Xb, int64_t A, int64_t B,
+                     int64_t C, int64_t D, int32_t groups, int64_t stride, int64_t pad,
+                     const int32_t *row_ptr, const int32_t *col, const uint16_t *val, double *Y)
+{
+    int64_t P = (H + 2 * pad - C) / stride + 1;
+    int64_t Q = (W + 2 * pad - D) / stride + 1;
+    int64_t Cx = groups * B, per_group = A / groups;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t n = 0; n < N; ++n)
+        for (int64_t p = 0; p < P; ++p)
+            for (int64_t q = 0; q < Q; ++q)
+                for (int64_t a = 0; a < A; ++a) {
+                    int64_t gc = a / per_group;
+                    double acc = 0.0;
+                    for (int64_t e = row_ptr[a]; e < row_ptr[a + 1]; ++e) {
+                        int64_t j = col[e];
+                        int64_t b = j / (C * D), c = (j / D) % C, d = j % D;
+                        int64_t h = p * stride - pad + c;
+                        int64_t w = q * stride - pad + d;
+                        if (h < 0 || h >= H || w < 0 || w >= W)
+                            continue;
+                        acc += oracle_bf16_to_double(val[e]) *
+                               oracle_bf16_to_double(Xb[((n * Cx + gc * B + b) * H + h) * W + w]);
+                    }
+                    Y[((n * P + p) * Q + q) * A + a] = acc;
+                }
+}
