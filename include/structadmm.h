@@ -12,12 +12,15 @@
  *     U <- U + W - Z (Section 4, below eq. (3)) and the gradient of the
  *     quadratic term of eq. (3), G = rho * (W - Z + U);
  *   - the standalone dual update / gradient;
+ *   - one SGD step of the W-subproblem or of masked retraining (Section 4);
  *   - the compaction of a pruned layer into the smaller dense GEMM matrix
  *     that filter (row) and channel / shape (column) pruning leave
  *     (Section 3, "Combination of structured sparsities");
  *   - the CONV over that compacted matrix as an implicit GEMM on the bf16
  *     matrix cores (the same kernel with an uncompacted matrix is the dense
- *     baseline).
+ *     baseline);
+ *   - for non-structured (element-wise) pruning, the CSR form of the layer
+ *     and its CONV as a sparse product (Section 5's comparison).
  *
  * Conventions shared by every entry point
  *   - Every tensor argument is DEVICE memory owned by the caller.  The
@@ -278,6 +281,71 @@ typedef struct sa_conv_desc {
 size_t structadmm_conv_workspace(const sa_conv_desc *desc);
 
 int structadmm_conv_fwd(const sa_conv_desc *desc, hipStream_t stream);
+
+/* ---- non-structured layers as CSR: structadmm_csr -------------------- */
+/*
+ * The non-structured set of Section 3 keeps an arbitrary pattern of weights,
+ * which leaves no smaller dense GEMM; its CONV is a sparse-matrix product
+ * (Section 5 runs it with a CSR sparse library and finds little or no
+ * speedup).  From the ascending kept indices of an element-wise projection
+ * (structadmm_project with kind SA_ELEMENT: flat indices a*B*C*D + j), builds
+ * the CSR form of the [A, B*C*D] GEMM matrix:
+ *   row_ptr[a] = number of kept indices below a*B*C*D (row_ptr[A] = nnz),
+ *   col[e]     = kept_idx[e] - a*B*C*D for row_ptr[a] <= e < row_ptr[a+1],
+ *   val[e]     = bfloat16(Z[kept_idx[e]]) (round to nearest even).
+ * kept_idx must be strictly ascending and below A*B*C*D (as the projection
+ * writes it); it is not re-validated on the device, where an index out of
+ * range yields a zero entry instead of an out-of-bounds access.
+ */
+typedef struct sa_csr_desc {
+    int64_t A, B, C, D;        /* weight tensor shape; A*B*C*D < 2^31           */
+    int64_t nnz;               /* number of kept weights, 0 <= nnz <= A*B*C*D  */
+    const float *Z;            /* [A,B,C,D] binary32                            */
+    const int32_t *kept_idx;   /* [nnz] ascending flat indices (NULL if nnz == 0) */
+    int32_t *row_ptr;          /* out [A+1]                                     */
+    int32_t *col;              /* out [nnz] (NULL if nnz == 0)                  */
+    uint16_t *val;             /* out [nnz] bfloat16 bits (NULL if nnz == 0)   */
+} sa_csr_desc;
+
+int structadmm_csr(const sa_csr_desc *desc, hipStream_t stream);
+
+/* ---- sparse CONV of a CSR layer: structadmm_conv_sparse_fwd ---------- */
+/*
+ * Y[n, p, q, a] = sum over the entries e of row a of
+ *     val[e] * X[n, p*stride - pad + c, q*stride - pad + d, gc*B + b]
+ * with conv group gc = a / (A / groups) and col[e] = (b*C + c)*D + d; zero
+ * outside the image (cross-correlation, no bias, no dilation).  bfloat16
+ * operands, binary32 accumulation (packed bf16 dot products on the vector
+ * ALUs: a pattern of single weights has no dense tile for the matrix cores),
+ * bfloat16 output (nearest even).  The result equals structadmm_conv_fwd over
+ * the uncompacted matrix of the same weights up to the order of the sums.
+ * X: bfloat16 NHWC [N, H, W, Cx], Cx = groups*B a multiple of 8, 16-byte
+ *    aligned, smaller than 2 GiB.
+ * Y: bfloat16 NHWC [N, P, Q, A], P = (H + 2*pad - C)/stride + 1, same for Q,
+ *    16-byte aligned.
+ * The input footprint of a tile of output pixels (the conv group's channels)
+ * must fit in LDS (SA_E_UNSUPPORTED otherwise).
+ */
+typedef struct sa_sparse_conv_desc {
+    int32_t N, H, W, Cx;       /* input */
+    int32_t A, B, C, D;        /* weight tensor shape */
+    int32_t groups, stride, pad;
+    int64_t nnz;               /* row_ptr[A] */
+    const uint16_t *X;
+    const int32_t *row_ptr;    /* [A+1], as structadmm_csr writes it */
+    const int32_t *col;        /* [nnz] */
+    const uint16_t *val;       /* [nnz] bfloat16 bits */
+    uint16_t *Y;
+    void *ws;                  /* device scratch of structadmm_conv_sparse_workspace()
+                                  bytes, 256-byte aligned: the entries' LDS offsets
+                                  and values with every row padded to 8 entries */
+    size_t ws_bytes;
+} sa_sparse_conv_desc;
+
+/* Scratch bytes structadmm_conv_sparse_fwd needs (0 for an invalid descriptor). */
+size_t structadmm_conv_sparse_workspace(const sa_sparse_conv_desc *desc);
+
+int structadmm_conv_sparse_fwd(const sa_sparse_conv_desc *desc, hipStream_t stream);
 
 /* Message describing the last error on the calling thread ("" if none). */
 const char *structadmm_last_error(void);

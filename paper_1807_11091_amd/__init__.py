@@ -13,6 +13,9 @@ Entry points (same names as the C ABI):
   compact(Z, groups, ..., ws=None, stream=None) -> (Wc, row_idx, col_ch, col_tap, sizes)
   pack_nhwc(X, keep=None, Cx=None, stream=None)
   conv_fwd(X, Wc, col_ch, col_tap, sizes, C, D, stride, pad, Y=None, stream=None)
+  csr(Z, kept_idx, row_ptr=None, col=None, val=None, stream=None) -> (row_ptr, col, val)
+  conv_sparse_workspace(Xp, shape, groups, stride, pad, nnz)
+  conv_sparse_fwd(Xp, row_ptr, col, val, shape, groups, stride, pad, Y=None, ws=None, stream=None)
 """
 from __future__ import annotations
 
@@ -82,6 +85,20 @@ class ConvDesc(ctypes.Structure):
                 ("col_tap", _vp), ("Y", _vp), ("ws", _vp), ("ws_bytes", ctypes.c_size_t)]
 
 
+class CsrDesc(ctypes.Structure):
+    _fields_ = [("A", ctypes.c_int64), ("B", ctypes.c_int64), ("C", ctypes.c_int64), ("D", ctypes.c_int64),
+                ("nnz", ctypes.c_int64), ("Z", _vp), ("kept_idx", _vp), ("row_ptr", _vp), ("col", _vp),
+                ("val", _vp)]
+
+
+class SparseConvDesc(ctypes.Structure):
+    _fields_ = [("N", ctypes.c_int32), ("H", ctypes.c_int32), ("W", ctypes.c_int32), ("Cx", ctypes.c_int32),
+                ("A", ctypes.c_int32), ("B", ctypes.c_int32), ("C", ctypes.c_int32), ("D", ctypes.c_int32),
+                ("groups", ctypes.c_int32), ("stride", ctypes.c_int32), ("pad", ctypes.c_int32),
+                ("nnz", ctypes.c_int64), ("X", _vp), ("row_ptr", _vp), ("col", _vp), ("val", _vp),
+                ("Y", _vp), ("ws", _vp), ("ws_bytes", ctypes.c_size_t)]
+
+
 class StructAdmmError(RuntimeError):
     pass
 
@@ -113,6 +130,12 @@ def lib():
         L.structadmm_conv_fwd.restype = ctypes.c_int
         L.structadmm_conv_workspace.argtypes = [ctypes.POINTER(ConvDesc)]
         L.structadmm_conv_workspace.restype = ctypes.c_size_t
+        L.structadmm_csr.argtypes = [ctypes.POINTER(CsrDesc), _vp]
+        L.structadmm_csr.restype = ctypes.c_int
+        L.structadmm_conv_sparse_workspace.argtypes = [ctypes.POINTER(SparseConvDesc)]
+        L.structadmm_conv_sparse_workspace.restype = ctypes.c_size_t
+        L.structadmm_conv_sparse_fwd.argtypes = [ctypes.POINTER(SparseConvDesc), _vp]
+        L.structadmm_conv_sparse_fwd.restype = ctypes.c_int
         L.structadmm_last_error.argtypes = []
         L.structadmm_last_error.restype = ctypes.c_char_p
         L.structadmm_version.argtypes = []
@@ -281,6 +304,60 @@ def conv_fwd(Xp, Wc, col_ch, col_tap, sizes: CompactSizes, C: int, D: int, strid
             ws = torch.empty(need, dtype=torch.uint8, device=Xp.device) if need else None
         desc = conv_desc(Xp, Wc, col_ch, col_tap, sizes, C, D, stride, pad, Y, ws)
     _check(lib().structadmm_conv_fwd(ctypes.byref(desc), _stream(stream)), "structadmm_conv_fwd")
+    return Y
+
+
+def csr(Z, kept_idx, nnz: Optional[int] = None, row_ptr=None, col=None, val=None, stream=None):
+    """structadmm_csr: CSR (row_ptr int32 [A+1], col int32 [nnz], val bf16 bits
+    uint16 [nnz]) of an element-wise pruned layer from its projection's
+    ascending kept indices."""
+    import torch
+    A, B, C, D = Z.shape
+    nnz = int(kept_idx.numel()) if nnz is None else int(nnz)
+    dev = Z.device
+    if row_ptr is None:
+        row_ptr = torch.empty(A + 1, dtype=torch.int32, device=dev)
+    if col is None:
+        col = torch.empty(max(nnz, 1), dtype=torch.int32, device=dev)
+    if val is None:
+        val = torch.empty(max(nnz, 1), dtype=torch.uint16, device=dev)
+    d = CsrDesc(A, B, C, D, nnz, _ptr(Z), _ptr(kept_idx) if nnz else None, _ptr(row_ptr),
+                _ptr(col) if nnz else None, _ptr(val) if nnz else None)
+    _check(lib().structadmm_csr(ctypes.byref(d), _stream(stream)), "structadmm_csr")
+    return row_ptr, col, val
+
+
+def sparse_conv_desc(Xp, row_ptr, col, val, shape, groups, stride, pad, nnz, Y, ws=None) -> SparseConvDesc:
+    N, H, W, Cx = Xp.shape
+    A, B, C, D = shape
+    nbytes = 0 if ws is None else ws.numel() * ws.element_size()
+    return SparseConvDesc(N, H, W, Cx, A, B, C, D, groups, stride, pad, nnz, _ptr(Xp), _ptr(row_ptr),
+                          _ptr(col) if nnz else None, _ptr(val) if nnz else None, _ptr(Y), _ptr(ws), nbytes)
+
+
+def conv_sparse_workspace(Xp, shape, groups: int, stride: int, pad: int, nnz: int) -> int:
+    """Scratch bytes structadmm_conv_sparse_fwd needs."""
+    d = sparse_conv_desc(Xp, None, None, None, shape, groups, stride, pad, nnz, None)
+    return int(lib().structadmm_conv_sparse_workspace(ctypes.byref(d)))
+
+
+def conv_sparse_fwd(Xp, row_ptr, col, val, shape, groups: int, stride: int, pad: int, nnz: int,
+                    Y=None, ws=None, stream=None, desc: Optional[SparseConvDesc] = None):
+    """structadmm_conv_sparse_fwd; Xp bf16 NHWC (uint16), returns Y bf16 NHWC
+    [N, P, Q, A] (uint16)."""
+    import torch
+    if desc is None:
+        N, H, W, Cx = Xp.shape
+        A, B, C, D = shape
+        if Y is None:
+            P = (H + 2 * pad - C) // stride + 1
+            Q = (W + 2 * pad - D) // stride + 1
+            Y = torch.empty((N, P, Q, A), dtype=torch.uint16, device=Xp.device)
+        if ws is None:
+            need = conv_sparse_workspace(Xp, shape, groups, stride, pad, nnz)
+            ws = torch.empty(max(need, 256), dtype=torch.uint8, device=Xp.device)
+        desc = sparse_conv_desc(Xp, row_ptr, col, val, shape, groups, stride, pad, nnz, Y, ws)
+    _check(lib().structadmm_conv_sparse_fwd(ctypes.byref(desc), _stream(stream)), "structadmm_conv_sparse_fwd")
     return Y
 
 

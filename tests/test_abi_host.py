@@ -27,6 +27,7 @@ def test_library_exports_every_declared_symbol():
     names = declared_functions()
     assert {"structadmm_project", "structadmm_project_workspace", "structadmm_dual_update",
             "structadmm_compact", "structadmm_conv_fwd", "structadmm_pack_nhwc", "structadmm_sgd_step",
+            "structadmm_csr", "structadmm_conv_sparse_fwd", "structadmm_conv_sparse_workspace",
             "structadmm_last_error", "structadmm_version"} <= names
     L = sa.lib()
     for n in names:
@@ -46,6 +47,9 @@ def _c_layout():
         "sa_compact_sizes": ("CompactSizes", ["M", "K", "ldk", "wc_offset", "row_offset", "run", "run_base",
                                               "ch_lo", "ch_span"]),
         "sa_conv_desc": ("ConvDesc", ["N", "pad", "sizes", "X", "Y", "ws", "ws_bytes"]),
+        "sa_csr_desc": ("CsrDesc", ["A", "D", "nnz", "Z", "kept_idx", "row_ptr", "col", "val"]),
+        "sa_sparse_conv_desc": ("SparseConvDesc", ["N", "Cx", "A", "D", "groups", "stride", "pad", "nnz", "X",
+                                                   "row_ptr", "col", "val", "Y", "ws", "ws_bytes"]),
     }
     lines = ["#include <stdio.h>", "#include <stddef.h>", '#include "structadmm.h"', "int main(void){"]
     for st, (_, fs) in fields.items():
@@ -209,6 +213,56 @@ def test_compact_and_conv_validation():
     s.ch_span[0] = 16
     wide = dict(W=4000, Cx=16)
     assert L.structadmm_conv_workspace(ctypes.byref(desc(**wide))) == 8 * 4000 * 64 * 2
+
+
+def test_csr_validation():
+    L = sa.lib()
+    def call(**kw):
+        d = dict(A=4, B=2, C=3, D=3, nnz=5, Z=FAKE, kept_idx=FAKE + 256, row_ptr=FAKE + 512, col=FAKE + 768,
+                 val=FAKE + 1024)
+        d.update(kw)
+        return L.structadmm_csr(ctypes.byref(sa.CsrDesc(**d)), None)
+    assert call(A=0) == -1
+    assert call(nnz=-1) == -1
+    assert call(nnz=4 * 18 + 1) == -1
+    assert call(Z=None) == -1
+    assert call(row_ptr=None) == -1
+    assert call(kept_idx=None) == -1
+    assert call(col=FAKE + 2) == -2
+    assert call(A=1 << 16, B=1 << 16) == -4
+    assert L.structadmm_csr(None, None) == -1
+
+
+def test_conv_sparse_validation():
+    L = sa.lib()
+    def desc(**kw):
+        d = dict(N=2, H=14, W=14, Cx=256, A=256, B=256, C=3, D=3, groups=1, stride=1, pad=1, nnz=1000,
+                 X=FAKE, row_ptr=FAKE + 256, col=FAKE + 512, val=FAKE + 768, Y=FAKE + 1024, ws=FAKE + 2048,
+                 ws_bytes=1 << 30)
+        d.update(kw)
+        return sa.SparseConvDesc(**d)
+    def call(**kw):
+        return L.structadmm_conv_sparse_fwd(ctypes.byref(desc(**kw)), None)
+    ws = lambda **kw: L.structadmm_conv_sparse_workspace(ctypes.byref(desc(**kw)))
+    # padded row pointers, offsets and values: (A+1)*4, (nnz + 7A rounded to 8)*4, *2, each 256-aligned
+    cap = (1000 + 7 * 256 + 7) // 8 * 8
+    r = lambda x: (x + 255) // 256 * 256
+    assert ws() == r(257 * 4) + r(cap * 4) + r(cap * 2)
+    assert call(groups=3) == -1                 # A % groups, Cx != groups * B
+    assert call(Cx=128) == -1
+    assert call(nnz=256 * 2304 + 1) == -1
+    assert call(stride=0) == -1
+    assert call(H=1, pad=0) == -1               # empty output
+    assert call(Cx=12, B=12) == -4              # channels not a multiple of 8
+    assert call(H=1000, W=1000) == -4           # footprint of 64 pixels exceeds LDS
+    assert call(X=FAKE + 2) == -2
+    assert call(Y=FAKE + 1024 + 8) == -2
+    assert call(ws=None) == -3
+    assert call(ws_bytes=ws() - 1) == -3
+    assert call(ws=FAKE + 2048 + 16) == -2
+    assert call(col=None) == -1
+    assert ws(Cx=12, B=12) == 0
+    assert L.structadmm_conv_sparse_fwd(None, None) == -1
 
 
 def test_pack_validation():
