@@ -56,6 +56,9 @@ def parse():
                         "MIOpen, density sweep, achievable peaks) and write the report to JSON")
     p.add_argument("--tables", metavar="JSON", default=None,
                    help="only the batch-1 replay of the pruned AlexNet layers of Tables 1-2 (CONV speedups)")
+    p.add_argument("--sparse", metavar="JSON", default=None,
+                   help="only the CSR CONV of non-structured pruning: density sweep of the [256,256,3,3] "
+                        "layer and batch-1 AlexNet conv2-5 at the sparsities of Tables 4-5")
     p.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                    help="only copy MIB MiB device-to-device 5 times (HBM counter calibration) and exit")
     return p.parse_args()
@@ -363,6 +366,121 @@ def suite_tables(torch, sa):
     return res
 
 
+# LDS gather bound of the sparse CONV: one 2-byte gather per kept weight and
+# output pixel; gfx950 serves 32 lanes of a ds_read_u16 per clock per CU
+# (measured: a 64-lane u16 read every 2.0 clocks per CU with 16 wavefronts)
+LDS_GATHER_PEAK_PRODUCTS = 256 * 32 * 2.4e9
+
+
+def _element_csr(torch, sa, dW, dU, k, groups):
+    """Element-wise projection of (W, U) keeping k weights, then its CSR."""
+    Z = torch.empty_like(dW)
+    mask = torch.empty(dW.numel(), dtype=torch.uint8, device="cuda")
+    kept = torch.empty(max(k, 1), dtype=torch.int32, device="cuda")
+    lay = sa.ProjectLayer(dW, dU, Z, mask, kept, sa.ELEMENT, k, groups)
+    ws = torch.empty(max(256, sa.project_workspace([lay])), dtype=torch.uint8, device="cuda")
+    sa.project([lay], ws)
+    return Z, sa.csr(Z, kept, nnz=k)
+
+
+def _sparse_vs_dense(torch, sa, L, Xp, X, dW, Z, csr, k):
+    """Graph-timed sparse CONV of one layer against its own dense CONV (over
+    the masked weights) and MIOpen's bf16 conv2d of the same shape."""
+    import torch.nn.functional as F
+    shape = tuple(dW.shape)
+    rp, col, val = csr
+    need = max(256, sa.conv_sparse_workspace(Xp, shape, L.groups, L.stride, L.pad, k))
+    sws = torch.empty(need, dtype=torch.uint8, device="cuda")
+    Ys = sa.conv_sparse_fwd(Xp, rp, col, val, shape, L.groups, L.stride, L.pad, k, ws=sws)
+    # the padded entries depend only on the pruned layer and its geometry: built
+    # once (first call), reused by the timed CONVs; the full call is timed too
+    ds = sa.sparse_conv_desc(Xp, rp, col, val, shape, L.groups, L.stride, L.pad, k, Ys, sws, reuse_ws=True)
+    ts = _time_graph(torch, lambda: sa.conv_sparse_fwd(None, None, None, None, shape, 0, 0, 0, k, desc=ds))
+    dsf = sa.sparse_conv_desc(Xp, rp, col, val, shape, L.groups, L.stride, L.pad, k, Ys, sws)
+    tsf = _time_graph(torch, lambda: sa.conv_sparse_fwd(None, None, None, None, shape, 0, 0, 0, k, desc=dsf))
+    Wd, _, ccd, ctd, szd = sa.compact(Z, L.groups)
+    cws = torch.empty(max(256, sa.conv_workspace(Xp, szd, L.C, L.D, L.stride, L.pad)), dtype=torch.uint8,
+                      device="cuda")
+    Yd = sa.conv_fwd(Xp, Wd, ccd, ctd, szd, L.C, L.D, L.stride, L.pad, ws=cws)
+    dd = sa.conv_desc(Xp, Wd, ccd, ctd, szd, L.C, L.D, L.stride, L.pad, Yd, cws)
+    td = _time_graph(torch, lambda: sa.conv_fwd(None, None, None, None, szd, 0, 0, 0, 0, desc=dd))
+    xb, wb = X.to(torch.bfloat16), Z.to(torch.bfloat16)
+    conv = lambda: F.conv2d(xb, wb, stride=L.stride, padding=L.pad, groups=L.groups)
+    try:
+        tm = _time_graph(torch, conv)
+    except RuntimeError:  # a library path that cannot be captured: events around eager calls
+        torch.cuda.synchronize()
+        tm = _time(torch, conv)
+    N = X.shape[0]
+    products = N * L.P * L.Q * k
+    best = min(td["median_ms"], tm["median_ms"])
+    return {"kept": k, "density_pct": round(100.0 * k / dW.numel(), 3),
+            "sparse_us": round(ts["median_ms"] * 1e3, 2), "sparse_with_prep_us": round(tsf["median_ms"] * 1e3, 2),
+            "dense_us": round(td["median_ms"] * 1e3, 2),
+            "miopen_dense_us": round(tm["median_ms"] * 1e3, 2),
+            "speedup_vs_best_dense": round(best / ts["median_ms"], 3),
+            "sparse_useful_tflops": round(2 * products / (ts["median_ms"] * 1e-3) / 1e12, 2),
+            "lds_gather_frac": round(products / (ts["median_ms"] * 1e-3) / LDS_GATHER_PEAK_PRODUCTS, 4)}
+
+
+def suite_sparse(torch, sa):
+    """Non-structured pruning through the CSR CONV: (a) the [256,256,3,3] layer
+    on 14x14 at batch 256 over a density sweep, with the density where it
+    starts to beat the best dense CONV; (b) batch-1 AlexNet conv2-5 pruned to
+    the per-layer sparsities of Tables 4 and 5 (Section 5's comparison)."""
+    from workloads import PAPER_ELEMENT_SPARSITY, WORKLOADS, input_nchw, kept_count, kept_from_sparsity, layer_tensors
+    out = {}
+    wl = WORKLOADS["resnet50_s3_sweep"]
+    L = wl.layers[0]
+    W, U = layer_tensors(wl, 0)
+    dW, dU = torch.from_numpy(W).cuda(), torch.from_numpy(U).cuda()
+    X = torch.from_numpy(input_nchw(wl, 0)).cuda()
+    Xp = sa.pack_nhwc(X)
+    sweep = []
+    for pct in (50, 25, 10, 6.2, 2.5, 1):
+        k = kept_count(pct, W.size) if float(pct).is_integer() else int(pct * W.size / 100 + 0.5)
+        Z, csr = _element_csr(torch, sa, dW, dU, k, L.groups)
+        r = _sparse_vs_dense(torch, sa, L, Xp, X, dW, Z, csr, k)
+        sweep.append(r)
+        print("sparse sweep", json.dumps(r), flush=True)
+        torch.cuda.empty_cache()
+    # density where the speedup crosses 1 (log-linear between neighbours)
+    cross = None
+    for a, b in zip(sweep, sweep[1:]):
+        sa_, sb = a["speedup_vs_best_dense"], b["speedup_vs_best_dense"]
+        if (sa_ - 1) * (sb - 1) <= 0 and sa_ != sb:
+            la, lb = np.log(a["density_pct"]), np.log(b["density_pct"])
+            t = (np.log(sa_) - 0.0) / (np.log(sa_) - np.log(sb))
+            cross = round(float(np.exp(la + t * (lb - la))), 3)
+            break
+    out["layer3_conv2_batch256"] = {"sweep": sweep, "crossover_density_pct": cross}
+    del X, Xp
+    torch.cuda.empty_cache()
+    wa = WORKLOADS["alexnet_shape30"]
+    for block, table in PAPER_ELEMENT_SPARSITY.items():
+        rows = []
+        for li, La in enumerate(wa.layers):
+            if table[La.name] == 0.0:
+                continue
+            Wl, Ul = layer_tensors(wa, li)
+            dWl, dUl = torch.from_numpy(Wl).cuda(), torch.from_numpy(Ul).cuda()
+            k = kept_from_sparsity(table[La.name], Wl.size)
+            Z, csr = _element_csr(torch, sa, dWl, dUl, k, La.groups)
+            X1 = torch.from_numpy(input_nchw(wa, li, batch=1)).cuda()
+            r = _sparse_vs_dense(torch, sa, La, sa.pack_nhwc(X1), X1, dWl, Z, csr, k)
+            r["layer"] = La.name
+            r["sparsity_pct"] = table[La.name]
+            rows.append(r)
+        s25 = sum(r["sparse_us"] for r in rows)
+        b25 = sum(min(r["dense_us"], r["miopen_dense_us"]) for r in rows)
+        out[block + "_batch1"] = {"layers": rows, "conv2_5_sparse_us": round(s25, 2),
+                                  "conv2_5_best_dense_us": round(b25, 2),
+                                  "conv2_5_speedup_vs_best_dense": round(b25 / s25, 3)}
+        print("sparse", block, json.dumps({k: v for k, v in out[block + "_batch1"].items() if k != "layers"}),
+              flush=True)
+    return out
+
+
 def _admm_layers(torch, sa, wl, variant, copies=1):
     """Device tensors of every layer (times copies) for one projection call."""
     from workloads import layer_tensors
@@ -565,12 +683,24 @@ def suite(path):
         print("sweep", json.dumps({"kind": r["kind"], "percent": p, "speedup": r["conv"]["speedup_vs_best_dense"]}),
               flush=True)
         torch.cuda.empty_cache()
+    rep["sparse"] = suite_sparse(torch, sa)
     rep["tables_batch1"] = suite_tables(torch, sa)
     print("tables", json.dumps({b: v["conv2_5_speedup_vs_best_dense"] for b, v in rep["tables_batch1"].items()}),
           flush=True)
     with open(path, "w") as f:
         json.dump(rep, f, indent=1)
     print("suite written to", path)
+
+
+def sparse(path):
+    import torch
+    import paper_1807_11091_amd as sa
+    if not torch.cuda.is_available():
+        raise SystemExit("bench.py needs a GPU")
+    sa.lib()
+    rep = suite_sparse(torch, sa)
+    with open(path, "w") as f:
+        json.dump(rep, f, indent=1)
 
 
 def tables(path):
@@ -595,6 +725,9 @@ def main():
         return
     if args.tables:
         tables(args.tables)
+        return
+    if args.sparse:
+        sparse(args.sparse)
         return
     if args.suite:
         suite(args.suite)

@@ -340,6 +340,12 @@ typedef struct sa_sparse_conv_desc {
                                   bytes, 256-byte aligned: the entries' LDS offsets
                                   and values with every row padded to 8 entries */
     size_t ws_bytes;
+    int32_t reuse_ws;          /* 0: (re)build the padded entries in ws, then run
+                                  the CONV.  Nonzero: ws already holds what an
+                                  earlier call with the same row_ptr, col, val,
+                                  nnz, shape, groups and geometry (N, H, W, Cx,
+                                  stride, pad) built, and only the CONV runs (a
+                                  layer's CSR is fixed once it is pruned) */
 } sa_sparse_conv_desc;
 
 /* Scratch bytes structadmm_conv_sparse_fwd needs (0 for an invalid descriptor). */

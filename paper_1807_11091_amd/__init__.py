@@ -96,7 +96,7 @@ class SparseConvDesc(ctypes.Structure):
                 ("A", ctypes.c_int32), ("B", ctypes.c_int32), ("C", ctypes.c_int32), ("D", ctypes.c_int32),
                 ("groups", ctypes.c_int32), ("stride", ctypes.c_int32), ("pad", ctypes.c_int32),
                 ("nnz", ctypes.c_int64), ("X", _vp), ("row_ptr", _vp), ("col", _vp), ("val", _vp),
-                ("Y", _vp), ("ws", _vp), ("ws_bytes", ctypes.c_size_t)]
+                ("Y", _vp), ("ws", _vp), ("ws_bytes", ctypes.c_size_t), ("reuse_ws", ctypes.c_int32)]
 
 
 class StructAdmmError(RuntimeError):
@@ -327,12 +327,14 @@ def csr(Z, kept_idx, nnz: Optional[int] = None, row_ptr=None, col=None, val=None
     return row_ptr, col, val
 
 
-def sparse_conv_desc(Xp, row_ptr, col, val, shape, groups, stride, pad, nnz, Y, ws=None) -> SparseConvDesc:
+def sparse_conv_desc(Xp, row_ptr, col, val, shape, groups, stride, pad, nnz, Y, ws=None,
+                     reuse_ws: bool = False) -> SparseConvDesc:
     N, H, W, Cx = Xp.shape
     A, B, C, D = shape
     nbytes = 0 if ws is None else ws.numel() * ws.element_size()
     return SparseConvDesc(N, H, W, Cx, A, B, C, D, groups, stride, pad, nnz, _ptr(Xp), _ptr(row_ptr),
-                          _ptr(col) if nnz else None, _ptr(val) if nnz else None, _ptr(Y), _ptr(ws), nbytes)
+                          _ptr(col) if nnz else None, _ptr(val) if nnz else None, _ptr(Y), _ptr(ws), nbytes,
+                          1 if reuse_ws else 0)
 
 
 def conv_sparse_workspace(Xp, shape, groups: int, stride: int, pad: int, nnz: int) -> int:
@@ -342,9 +344,10 @@ def conv_sparse_workspace(Xp, shape, groups: int, stride: int, pad: int, nnz: in
 
 
 def conv_sparse_fwd(Xp, row_ptr, col, val, shape, groups: int, stride: int, pad: int, nnz: int,
-                    Y=None, ws=None, stream=None, desc: Optional[SparseConvDesc] = None):
+                    Y=None, ws=None, reuse_ws: bool = False, stream=None, desc: Optional[SparseConvDesc] = None):
     """structadmm_conv_sparse_fwd; Xp bf16 NHWC (uint16), returns Y bf16 NHWC
-    [N, P, Q, A] (uint16)."""
+    [N, P, Q, A] (uint16).  reuse_ws: ws holds the padded entries an earlier
+    call with the same CSR and geometry built."""
     import torch
     if desc is None:
         N, H, W, Cx = Xp.shape
@@ -356,7 +359,7 @@ def conv_sparse_fwd(Xp, row_ptr, col, val, shape, groups: int, stride: int, pad:
         if ws is None:
             need = conv_sparse_workspace(Xp, shape, groups, stride, pad, nnz)
             ws = torch.empty(max(need, 256), dtype=torch.uint8, device=Xp.device)
-        desc = sparse_conv_desc(Xp, row_ptr, col, val, shape, groups, stride, pad, nnz, Y, ws)
+        desc = sparse_conv_desc(Xp, row_ptr, col, val, shape, groups, stride, pad, nnz, Y, ws, reuse_ws)
     _check(lib().structadmm_conv_sparse_fwd(ctypes.byref(desc), _stream(stream)), "structadmm_conv_sparse_fwd")
     return Y
 

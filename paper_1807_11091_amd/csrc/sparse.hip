@@ -45,8 +45,6 @@ namespace {
 
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
-constexpr int kSpRowsPerWave = 8;  // filter rows per wavefront: a workgroup of NW
-                                   // wavefronts covers 8*NW filters
 constexpr int kSpLds = 160 * 1024;
 constexpr int kSpRsrcWord3 = 0x00020000;   // raw buffer resource: 32-bit data, range checked
 constexpr uint32_t kSpInvalid = 0x80000000u;  // past every buffer here: reads return zero
@@ -193,10 +191,11 @@ struct SpConvArgs {
     FastDiv divQ, divP, divHp, divS, divFbg, divNch, divRowc;
 };
 
-template <int TN, int NW>
+template <int TN, int NW, int RPW>
 __global__ __launch_bounds__(64 * NW) void k_conv_csr(SpConvArgs a) {
     constexpr int kSpThreads = 64 * NW, kSpWaves = NW;
-    constexpr int kSpFB = kSpRowsPerWave * NW;  // filters per workgroup
+    constexpr int kSpRowsPerWave = RPW;         // filter rows per wavefront
+    constexpr int kSpFB = kSpRowsPerWave * NW;  // filters per workgroup (a multiple of 8)
     constexpr int kSpOutRow = kSpFB + 8;        // LDS row of the staged output tile (bf16 elements)
     constexpr int BP = 64 * TN;  // output pixels per workgroup
     constexpr int kUn = 8;       // 16-byte loads in flight per thread during the copy
@@ -363,8 +362,14 @@ int sp_patch_rows(int NPQ, int P, int Q, int Hp, int stride, int C, int bp) {
     return best;
 }
 
+// launch shapes in order of preference (see sp_plan)
+struct SpShape {
+    int tn, nw, rpw;
+};
+constexpr SpShape kSpShapes[] = {{2, 16, 8}, {1, 16, 8}, {2, 8, 8}, {1, 8, 8}, {1, 16, 1}, {1, 8, 1}};
+
 struct SpPlan {
-    int P, Q, NPQ, Hp, Wp, Ws, Wpp, nch, pixb, rowb, TN, NW, lds;
+    int P, Q, NPQ, Hp, Wp, Ws, Wpp, nch, pixb, rowb, TN, NW, RPW, lds;
     int64_t cap;  // padded entries: nnz + 7 per row
     size_t off_at, val_at, ws_need;
 };
@@ -411,23 +416,30 @@ int sp_plan(const sa_sparse_conv_desc &d, SpPlan *p) {
     const int pixw = p->pixb / 4;
     const int padw = d.stride == 1 ? (((p->Q - p->Wpp) * pixw) % 64 + 64) % 64 : 0;
     p->rowb = p->Wpp * p->pixb + 4 * padw;
-    // 16 wavefronts (128 filters) per footprint copy when a conv group has more
-    // than 64 filters: more wavefronts to issue gathers, fewer copies
-    p->NW = d.A / d.groups > 8 * kSpRowsPerWave ? 16 : 8;
-    // two pixels per lane when that footprint leaves room for two workgroups per CU
+    // launch shape: 64*TN pixels per workgroup, NW wavefronts of RPW filter
+    // rows each.  First choice: two pixels per lane, 16 wavefronts of 8 rows
+    // (more wavefronts to issue gathers, fewer footprint copies), as long as
+    // the grid holds 512 workgroups; small layers (batch 1) take the shape
+    // with the most workgroups, down to one row per wavefront
+    const int per_group = d.A / d.groups;
     p->TN = 0;
-    for (int pass = 0; pass < 2 && p->TN == 0; ++pass) {
-        const int limit = pass == 0 ? kSpLds / 2 : kSpLds;
-        for (int tn : {2, 1}) {
-            const int64_t rows = sp_patch_rows(p->NPQ, p->P, p->Q, p->Hp, d.stride, d.C, 64 * tn);
-            const int64_t patch = (rows * p->rowb + 15) / 16 * 16;
-            const int64_t lds = std::max<int64_t>(patch, (int64_t)64 * tn * (kSpRowsPerWave * p->NW + 8) * 2);
-            if (lds <= limit) {
-                p->TN = tn;
-                p->lds = (int)lds;
-                break;
-            }
+    int64_t best_grid = -1;
+    for (const SpShape &c : kSpShapes) {
+        const int fb = c.nw * c.rpw;
+        if (c.nw == 16 && c.rpw == 8 && per_group <= 64) continue;
+        const int64_t rows = sp_patch_rows(p->NPQ, p->P, p->Q, p->Hp, d.stride, d.C, 64 * c.tn);
+        const int64_t patch = (rows * p->rowb + 15) / 16 * 16;
+        const int64_t lds = std::max<int64_t>(patch, (int64_t)64 * c.tn * (fb + 8) * 2);
+        if (lds > kSpLds) continue;
+        const int64_t grid = (p->NPQ + 64 * c.tn - 1) / (64 * c.tn) * d.groups * ((per_group + fb - 1) / fb);
+        if (grid > best_grid) {
+            best_grid = grid;
+            p->TN = c.tn;
+            p->NW = c.nw;
+            p->RPW = c.rpw;
+            p->lds = (int)lds;
         }
+        if (grid >= 512) break;
     }
     if (p->TN == 0)
         return fail(SA_E_UNSUPPORTED, "conv_sparse: the input footprint of 64 output pixels exceeds LDS");
@@ -440,12 +452,98 @@ int sp_plan(const sa_sparse_conv_desc &d, SpPlan *p) {
     return SA_OK;
 }
 
-template <int TN, int NW>
+template <int TN, int NW, int RPW>
 int launch_conv_csr(SpConvArgs a, int lds, hipStream_t stream) {
-    auto kern = k_conv_csr<TN, NW>;
+    auto kern = k_conv_csr<TN, NW, RPW>;
     if (int rc = sp_allow_full_lds(reinterpret_cast<const void *>(kern))) return rc;
     hipLaunchKernelGGL(kern, dim3(a.nblocks), dim3(64 * NW), (size_t)lds, stream, a);
     return check_hip(hipGetLastError(), "k_conv_csr");
+}
+
+// Padded row starts, entry offsets and values for the layer's CSR and geometry.
+int sp_prepare(const sa_sparse_conv_desc &d, const SpPlan &p, int32_t *rowp8, int32_t *off8, uint16_t *val8,
+               hipStream_t stream) {
+    PadArgs pa;
+    pa.rp = d.row_ptr;
+    pa.rowp8 = rowp8;
+    pa.A = d.A;
+    pa.nnz = (int32_t)d.nnz;
+    pa.cap = (int32_t)p.cap;
+    hipLaunchKernelGGL(k_csr_rowpad, dim3(1), dim3(1024), 0, stream, pa);
+    if (int rc = check_hip(hipGetLastError(), "k_csr_rowpad")) return rc;
+
+    PrepArgs pr;
+    pr.rp = d.row_ptr;
+    pr.col = d.col;
+    pr.val = d.val;
+    pr.rowp8 = rowp8;
+    pr.off8 = off8;
+    pr.val8 = val8;
+    pr.A = d.A;
+    pr.nnz = (int32_t)d.nnz;
+    pr.K = d.B * d.C * d.D;
+    pr.CD = d.C * d.D;
+    pr.D = d.D;
+    pr.B = d.B;
+    pr.stride = d.stride;
+    pr.Ws = p.Ws;
+    pr.rowb = p.rowb;
+    pr.pixb = p.pixb;
+    pr.divCD = make_fastdiv((uint32_t)pr.CD);
+    pr.divD = make_fastdiv((uint32_t)d.D);
+    pr.divS = make_fastdiv((uint32_t)d.stride);
+    pr.divPG = make_fastdiv((uint32_t)(d.A / d.groups));
+    hipLaunchKernelGGL(k_csr_prep, dim3((d.A + 3) / 4), dim3(256), 0, stream, pr);
+    return check_hip(hipGetLastError(), "k_csr_prep");
+}
+
+int sp_launch(const sa_sparse_conv_desc &d, const SpPlan &p, const int32_t *rowp8, const int32_t *off8,
+              const uint16_t *val8, hipStream_t stream) {
+    SpConvArgs a;
+    a.X = d.X;
+    a.Y = d.Y;
+    a.rowp8 = rowp8;
+    a.off8 = off8;
+    a.val8 = val8;
+    a.x_bytes = (uint32_t)((int64_t)d.N * d.H * d.W * d.Cx * 2);
+    a.N = d.N;
+    a.H = d.H;
+    a.W = d.W;
+    a.Cx = d.Cx;
+    a.A = d.A;
+    a.B = d.B;
+    a.C = d.C;
+    a.stride = d.stride;
+    a.pad = d.pad;
+    a.P = p.P;
+    a.Q = p.Q;
+    a.NPQ = p.NPQ;
+    a.Hp = p.Hp;
+    a.Wp = p.Wp;
+    a.Ws = p.Ws;
+    a.Wpp = p.Wpp;
+    a.rowb = p.rowb;
+    a.nch = p.nch;
+    a.pixb = p.pixb;
+    a.per_group = d.A / d.groups;
+    const int fbs = p.RPW * p.NW;  // filters per workgroup
+    a.fb_per_group = (a.per_group + fbs - 1) / fbs;
+    a.nfb = a.fb_per_group * d.groups;
+    const int64_t ntiles = (p.NPQ + 64 * p.TN - 1) / (64 * p.TN);
+    if (ntiles * a.nfb >= (int64_t(1) << 31)) return fail(SA_E_UNSUPPORTED, "conv_sparse: grid too large");
+    a.nblocks = (int)(ntiles * a.nfb);
+    a.divQ = make_fastdiv((uint32_t)p.Q);
+    a.divP = make_fastdiv((uint32_t)p.P);
+    a.divHp = make_fastdiv((uint32_t)p.Hp);
+    a.divS = make_fastdiv((uint32_t)d.stride);
+    a.divFbg = make_fastdiv((uint32_t)a.fb_per_group);
+    a.divNch = make_fastdiv((uint32_t)p.nch);
+    a.divRowc = make_fastdiv((uint32_t)(p.Wp * p.nch));
+    if (p.RPW == 1)
+        return p.NW == 16 ? launch_conv_csr<1, 16, 1>(a, p.lds, stream) : launch_conv_csr<1, 8, 1>(a, p.lds, stream);
+    if (p.NW == 16)
+        return p.TN == 2 ? launch_conv_csr<2, 16, 8>(a, p.lds, stream) : launch_conv_csr<1, 16, 8>(a, p.lds, stream);
+    return p.TN == 2 ? launch_conv_csr<2, 8, 8>(a, p.lds, stream) : launch_conv_csr<1, 8, 8>(a, p.lds, stream);
 }
 
 }  // namespace
@@ -516,80 +614,8 @@ extern "C" int structadmm_conv_sparse_fwd(const sa_sparse_conv_desc *desc, hipSt
     int32_t *off8 = reinterpret_cast<int32_t *>(ws + p.off_at);
     uint16_t *val8 = reinterpret_cast<uint16_t *>(ws + p.val_at);
 
-    PadArgs pa;
-    pa.rp = d.row_ptr;
-    pa.rowp8 = rowp8;
-    pa.A = d.A;
-    pa.nnz = (int32_t)d.nnz;
-    pa.cap = (int32_t)p.cap;
-    hipLaunchKernelGGL(k_csr_rowpad, dim3(1), dim3(1024), 0, stream, pa);
-    if (int rc = check_hip(hipGetLastError(), "k_csr_rowpad")) return rc;
-
-    PrepArgs pr;
-    pr.rp = d.row_ptr;
-    pr.col = d.col;
-    pr.val = d.val;
-    pr.rowp8 = rowp8;
-    pr.off8 = off8;
-    pr.val8 = val8;
-    pr.A = d.A;
-    pr.nnz = (int32_t)d.nnz;
-    pr.K = d.B * d.C * d.D;
-    pr.CD = d.C * d.D;
-    pr.D = d.D;
-    pr.B = d.B;
-    pr.stride = d.stride;
-    pr.Ws = p.Ws;
-    pr.rowb = p.rowb;
-    pr.pixb = p.pixb;
-    pr.divCD = make_fastdiv((uint32_t)pr.CD);
-    pr.divD = make_fastdiv((uint32_t)d.D);
-    pr.divS = make_fastdiv((uint32_t)d.stride);
-    pr.divPG = make_fastdiv((uint32_t)(d.A / d.groups));
-    hipLaunchKernelGGL(k_csr_prep, dim3((d.A + 3) / 4), dim3(256), 0, stream, pr);
-    if (int rc = check_hip(hipGetLastError(), "k_csr_prep")) return rc;
-
-    SpConvArgs a;
-    a.X = d.X;
-    a.Y = d.Y;
-    a.rowp8 = rowp8;
-    a.off8 = off8;
-    a.val8 = val8;
-    a.x_bytes = (uint32_t)((int64_t)d.N * d.H * d.W * d.Cx * 2);
-    a.N = d.N;
-    a.H = d.H;
-    a.W = d.W;
-    a.Cx = d.Cx;
-    a.A = d.A;
-    a.B = d.B;
-    a.C = d.C;
-    a.stride = d.stride;
-    a.pad = d.pad;
-    a.P = p.P;
-    a.Q = p.Q;
-    a.NPQ = p.NPQ;
-    a.Hp = p.Hp;
-    a.Wp = p.Wp;
-    a.Ws = p.Ws;
-    a.Wpp = p.Wpp;
-    a.rowb = p.rowb;
-    a.nch = p.nch;
-    a.pixb = p.pixb;
-    a.per_group = d.A / d.groups;
-    const int fbs = kSpRowsPerWave * p.NW;  // filters per workgroup
-    a.fb_per_group = (a.per_group + fbs - 1) / fbs;
-    a.nfb = a.fb_per_group * d.groups;
-    const int64_t ntiles = (p.NPQ + 64 * p.TN - 1) / (64 * p.TN);
-    if (ntiles * a.nfb >= (int64_t(1) << 31)) return fail(SA_E_UNSUPPORTED, "conv_sparse: grid too large");
-    a.nblocks = (int)(ntiles * a.nfb);
-    a.divQ = make_fastdiv((uint32_t)p.Q);
-    a.divP = make_fastdiv((uint32_t)p.P);
-    a.divHp = make_fastdiv((uint32_t)p.Hp);
-    a.divS = make_fastdiv((uint32_t)d.stride);
-    a.divFbg = make_fastdiv((uint32_t)a.fb_per_group);
-    a.divNch = make_fastdiv((uint32_t)p.nch);
-    a.divRowc = make_fastdiv((uint32_t)(p.Wp * p.nch));
-    if (p.NW == 16)
-        return p.TN == 2 ? launch_conv_csr<2, 16>(a, p.lds, stream) : launch_conv_csr<1, 16>(a, p.lds, stream);
-    return p.TN == 2 ? launch_conv_csr<2, 8>(a, p.lds, stream) : launch_conv_csr<1, 8>(a, p.lds, stream);
+    if (!d.reuse_ws) {
+        if (int rc = sp_prepare(d, p, rowp8, off8, val8, stream)) return rc;
+    }
+    return sp_launch(d, p, rowp8, off8, val8, stream);
 }

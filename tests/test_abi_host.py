@@ -49,7 +49,8 @@ def _c_layout():
         "sa_conv_desc": ("ConvDesc", ["N", "pad", "sizes", "X", "Y", "ws", "ws_bytes"]),
         "sa_csr_desc": ("CsrDesc", ["A", "D", "nnz", "Z", "kept_idx", "row_ptr", "col", "val"]),
         "sa_sparse_conv_desc": ("SparseConvDesc", ["N", "Cx", "A", "D", "groups", "stride", "pad", "nnz", "X",
-                                                   "row_ptr", "col", "val", "Y", "ws", "ws_bytes"]),
+                                                   "row_ptr", "col", "val", "Y", "ws", "ws_bytes",
+                                                   "reuse_ws"]),
     }
     lines = ["#include <stdio.h>", "#include <stddef.h>", '#include "structadmm.h"', "int main(void){"]
     for st, (_, fs) in fields.items():

@@ -117,3 +117,16 @@ def test_conv_csr_equals_dense_masked(groups, stride, pad):
     Ys = oracle.conv_csr(Xb, oracle.csr(p["Z"], p["mask"]), W.shape, groups, stride, pad)
     Yd = oracle.conv(Xb, oracle.compact(p["Z"], groups), C, D, stride, pad)
     assert np.array_equal(Ys, Yd)
+
+
+def test_table4_table5_element_rates_from_kept_counts():
+    """The per-layer non-structured sparsities of Tables 4 and 5 give the
+    printed conv2-5 pruning rates (16.1x and 40.5x) once turned into kept
+    weight counts of AlexNet's conv2-5 tensors."""
+    from workloads import PAPER_ELEMENT_SPARSITY, WORKLOADS, kept_from_sparsity
+    layers = {L.name: L for L in WORKLOADS["alexnet_shape30"].layers}
+    for block, rate in (("table4_16.1x", 16.1), ("table5_40.5x", 40.5)):
+        sp = PAPER_ELEMENT_SPARSITY[block]
+        n = sum(layers[f"conv{i}"].n for i in range(2, 6))
+        kept = sum(kept_from_sparsity(sp[f"conv{i}"], layers[f"conv{i}"].n) for i in range(2, 6))
+        assert round(n / kept, 1) == rate

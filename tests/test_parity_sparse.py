@@ -53,7 +53,7 @@ def test_csr_bitwise(shape, frac, seed):
     assert np.array_equal(val, r["val"])
 
 
-def sparse_case(N, Cin, H, Wd, A, C, D, stride, pad, groups, frac, seed, empty_rows=0):
+def sparse_case(N, Cin, H, Wd, A, C, D, stride, pad, groups, frac, seed, empty_rows=0, images=None):
     rng = np.random.default_rng(seed)
     B = Cin // groups
     shape = (A, B, C, D)
@@ -70,9 +70,10 @@ def sparse_case(N, Cin, H, Wd, A, C, D, stride, pad, groups, frac, seed, empty_r
     Xp = sa.pack_nhwc(to_dev(X))
     Y = sa.conv_sparse_fwd(Xp, row_ptr, col, val, shape, groups, stride, pad, k)
     torch().cuda.synchronize()
-    got = bf16_bits_to_f64(Y.cpu().numpy())
+    imgs = list(range(N)) if images is None else images
+    got = bf16_bits_to_f64(Y.cpu().numpy()[imgs])
     rc = oracle.csr(ref["Z"], ref["mask"])
-    Yref = oracle.conv_csr(oracle.pack(X), rc, shape, groups, stride, pad)
+    Yref = oracle.conv_csr(oracle.pack(X[imgs]), rc, shape, groups, stride, pad)
     assert got.shape == Yref.shape
     err = maxabs_over_rms(got, Yref) if np.any(Yref) else float(np.max(np.abs(got)))
     assert err <= TOL, err
@@ -118,6 +119,45 @@ def test_conv_sparse_equals_dense_path():
     torch().cuda.synchronize()
     a, b = bf16_bits_to_f64(Ys.cpu().numpy()), bf16_bits_to_f64(Yd.cpu().numpy())
     assert maxabs_over_rms(a, b) <= TOL
+
+
+def test_conv_sparse_reuse_ws():
+    """A call that reuses the padded entries of the previous call on another
+    input gives the same result as a full call."""
+    t = torch()
+    rng = np.random.default_rng(50)
+    shape = (48, 16, 3, 3)
+    W = rng.standard_normal(shape).astype(np.float32)
+    k = W.size // 8
+    L, ref = project_element(W, np.zeros(shape, np.float32), k)
+    rp, col, val = sa.csr(L.Z, L.kept, nnz=k)
+    X1 = sa.pack_nhwc(to_dev(rng.standard_normal((2, 16, 11, 11)).astype(np.float32)))
+    X2 = sa.pack_nhwc(to_dev(rng.standard_normal((2, 16, 11, 11)).astype(np.float32)))
+    ws = t.empty(sa.conv_sparse_workspace(X1, shape, 1, 1, 1, k), dtype=t.uint8, device=DEV)
+    sa.conv_sparse_fwd(X1, rp, col, val, shape, 1, 1, 1, k, ws=ws)
+    Yr = sa.conv_sparse_fwd(X2, rp, col, val, shape, 1, 1, 1, k, ws=ws, reuse_ws=True)
+    Yf = sa.conv_sparse_fwd(X2, rp, col, val, shape, 1, 1, 1, k)
+    t.cuda.synchronize()
+    assert np.array_equal(Yr.cpu().numpy(), Yf.cpu().numpy())
+
+
+@pytest.mark.parametrize("batch", [1, 2])
+def test_conv_sparse_small_grids(batch):
+    """Batch-1 AlexNet conv3 and conv4 shapes at the sparsities of Table 4:
+    the launch shapes with one filter row per wavefront."""
+    sparse_case(batch, 256, 13, 13, 384, 3, 3, 1, 1, 1, 0.057, 60 + batch)
+    sparse_case(batch, 384, 13, 13, 384, 3, 3, 1, 1, 2, 0.064, 70 + batch)
+
+
+@pytest.mark.parametrize("N,Cin,A", [
+    (80, 256, 384),  # 64 pixels per workgroup, 16 wavefronts of 8 rows
+    (200, 32, 64),   # 64 pixels, 8 wavefronts of 8 rows
+    (8, 256, 384),   # 64 pixels, 16 wavefronts of 1 row
+])
+def test_conv_sparse_launch_shapes(N, Cin, A):
+    """13x13 3x3 layers sized so that each launch shape of the CONV is taken;
+    first, middle and last image compared."""
+    sparse_case(N, Cin, 13, 13, A, 3, 3, 1, 1, 1, 0.1, 80 + N, images=[0, N // 2, N - 1])
 
 
 def test_conv_sparse_two_calls_share_scratch():

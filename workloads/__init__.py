@@ -8,6 +8,6 @@ sharing any computation.
 from .configs import (  # noqa: F401
     ConvLayer, Workload, WORKLOADS, get_workload, kept_count,
     alexnet_layers, resnet50_layers, FILTER, CHANNEL, SHAPE, ELEMENT, KIND_NAMES,
-    PAPER_TABLE_SPARSITY, kept_from_sparsity,
+    PAPER_TABLE_SPARSITY, PAPER_ELEMENT_SPARSITY, kept_from_sparsity,
 )
 from .gen import layer_tensors, input_nchw, normal_f32  # noqa: F401

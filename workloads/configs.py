@@ -183,6 +183,16 @@ PAPER_TABLE_SPARSITY = {
 }
 
 
+# Per-layer non-structured (element-wise) sparsity, in percent, of the pruned
+# AlexNet CONV layers of Table 4 (no accuracy loss: 16.1x on conv2-5) and of
+# Table 5's 1.95%-loss row (40.5x on conv2-5), whose GPU speed Section 5
+# discusses.  conv1 is left dense in both.
+PAPER_ELEMENT_SPARSITY = {
+    "table4_16.1x": {"conv1": 0.0, "conv2": 93.0, "conv3": 94.3, "conv4": 93.6, "conv5": 93.5},
+    "table5_40.5x": {"conv1": 0.0, "conv2": 97.0, "conv3": 98.0, "conv4": 97.5, "conv5": 97.0},
+}
+
+
 def kept_from_sparsity(sparsity_percent: float, n_groups: int) -> int:
     """Groups kept when sparsity_percent of n_groups are pruned (pruned count
     rounded half up)."""
