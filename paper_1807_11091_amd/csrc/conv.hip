@@ -141,6 +141,9 @@ struct ConvGroup {
 };
 struct ConvArgs {
     uint16_t *Y;
+    float *part;          // split K: binary32 partial sums [ksplit][part_stride]
+    int64_t part_stride;  // floats per chunk (N*P*Q*Cy rounded up to 4)
+    int32_t ksplit, base_blocks;
     int32_t H, W, D, stride, pad, P, Q, NPQ, Cy;
     int32_t ngroups, nblocks;
     FastDiv divPQ, divQ, divD, divCy;
@@ -160,7 +163,7 @@ struct ConvCfg {
     static_assert(TM >= 1 && TN >= 1 && WTM % 32 == 0 && WTN % 32 == 0, "tile shape");
 };
 
-template <int BM, int BN, int WN, int WM>
+template <int BM, int BN, int WN, int WM, bool SPLIT>
 __global__ __launch_bounds__(64 * WN * WM) void k_conv(ConvArgs a) {
     using Cfg = ConvCfg<BM, BN, WN, WM>;
     constexpr int NT = Cfg::NT, WTM = Cfg::WTM, WTN = Cfg::WTN, TM = Cfg::TM, TN = Cfg::TN;
@@ -176,13 +179,23 @@ __global__ __launch_bounds__(64 * WN * WM) void k_conv(ConvArgs a) {
 
     int bid = blockIdx.x;
     bid = xcd_remap(bid, a.nblocks);
+    int chunk = 0;  // split K: the chunk of column slices this workgroup sums
+    if constexpr (SPLIT) {
+        chunk = bid / a.base_blocks;
+        bid -= chunk * a.base_blocks;
+    }
     int gi = 0;
     while (gi + 1 < a.ngroups && bid >= a.g[gi + 1].begin) ++gi;
     const ConvGroup &G = a.g[gi];
     const int lb = bid - G.begin;
     const int mt = lb % G.mtiles, nt = lb / G.mtiles;
     const int m0 = mt * BN, n0 = nt * BM;
-    const int nst = G.ldk / kBK;
+    int s_begin = 0, s_end = G.ldk / kBK;
+    if constexpr (SPLIT) {
+        const int nst = s_end;
+        s_begin = nst * chunk / a.ksplit;
+        s_end = nst * (chunk + 1) / a.ksplit;
+    }
     const int kc = tid & 7, rb = tid >> 3;
     const int frow = lane & 31, fk = (lane >> 5) * 8;
 
@@ -257,16 +270,16 @@ __global__ __launch_bounds__(64 * WN * WM) void k_conv(ConvArgs a) {
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
-    load_stage(0);
+    load_stage(s_begin);
     store_stage(0);
-    if (nst > 1) load_stage(1);
+    if (s_begin + 1 < s_end) load_stage(s_begin + 1);
     __syncthreads();
 
-    for (int s = 0; s < nst; ++s) {
-        if (s + 1 < nst) store_stage((s + 1) & 1);
-        if (s + 2 < nst) load_stage(s + 2);
-        const uint16_t *A = sA + (s & 1) * BN * kRow;
-        const uint16_t *B = sB + (s & 1) * BM * kRow;
+    for (int s = s_begin; s < s_end; ++s) {
+        if (s + 1 < s_end) store_stage((s + 1 - s_begin) & 1);
+        if (s + 2 < s_end) load_stage(s + 2);
+        const uint16_t *A = sA + ((s - s_begin) & 1) * BN * kRow;
+        const uint16_t *B = sB + ((s - s_begin) & 1) * BM * kRow;
 #pragma unroll
         for (int kk = 0; kk < kBK; kk += 16) {
             bf16x8 af[TM], bfr[TN];
@@ -286,6 +299,24 @@ __global__ __launch_bounds__(64 * WN * WM) void k_conv(ConvArgs a) {
     }
 
     // epilogue: accumulator (i, j, r): m = i*32 + (r/4)*8 + (lane/32)*4 + r%4, px = j*32 + lane%32
+    if constexpr (SPLIT) {  // binary32 partial sums of this chunk; k_splitk_sum adds the chunks
+        float *part = a.part + (int64_t)chunk * a.part_stride;
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+#pragma unroll
+                for (int r4 = 0; r4 < 4; ++r4) {
+                    const int m = m0 + wm * WTM + i * 32 + r4 * 8 + (lane >> 5) * 4;
+                    const int px = n0 + wn * WTN + j * 32 + (lane & 31);
+                    if (px >= a.NPQ) continue;
+                    float *dst = part + (int64_t)px * a.Cy + G.o_off + m;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        if (m + e < G.M) dst[e] = acc[i][j][r4 * 4 + e];
+                }
+        return;
+    }
     uint16_t *sC = reinterpret_cast<uint16_t *>(smem);  // [BM][BN + 8]
 #pragma unroll
     for (int i = 0; i < TM; ++i)
@@ -813,6 +844,36 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
     }
 }
 
+// ---------------------------------------------------------------- k_splitk_sum
+// Split K: Y = bf16(sum over chunks c = 0, 1, ... of part[c]) in that order
+// (one fixed order: the result does not depend on which chunk finished
+// first).  Element f of a chunk is element f of Y = [N*P*Q][Cy].
+__global__ __launch_bounds__(256) void k_splitk_sum(const float *part, int64_t stride, int ksplit, uint16_t *Y,
+                                                     int64_t total) {
+    const int64_t f = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 4;
+    if (f >= total) return;
+    if (f + 4 <= total) {
+        float4 acc = *reinterpret_cast<const float4 *>(part + f);
+#pragma unroll 7
+        for (int c = 1; c < ksplit; ++c) {
+            const float4 v = *reinterpret_cast<const float4 *>(part + c * stride + f);
+            acc.x += v.x;
+            acc.y += v.y;
+            acc.z += v.z;
+            acc.w += v.w;
+        }
+        uint32_t *dst = reinterpret_cast<uint32_t *>(Y + f);  // Y is 4-byte aligned, f a multiple of 4
+        dst[0] = (uint32_t)f32_to_bf16_bits(acc.x) | ((uint32_t)f32_to_bf16_bits(acc.y) << 16);
+        dst[1] = (uint32_t)f32_to_bf16_bits(acc.z) | ((uint32_t)f32_to_bf16_bits(acc.w) << 16);
+        return;
+    }
+    for (int64_t e = f; e < total; ++e) {
+        float acc = part[e];
+        for (int c = 1; c < ksplit; ++c) acc += part[c * stride + e];
+        Y[e] = f32_to_bf16_bits(acc);
+    }
+}
+
 // ---------------------------------------------------------------- k_s2d
 // Space-to-depth image of the zero-padded input for layers with few channels:
 // Xs[n][i][j][(a*s + b)*Cx + c] = Xpad[n][i*s + a][j*s + b][c], channels from
@@ -955,7 +1016,8 @@ int allow_full_lds(const void *kern) {
 template <int BM, int BN, int WN, int WM>
 int launch_conv(ConvArgs a, hipStream_t stream) {
     using Cfg = ConvCfg<BM, BN, WN, WM>;
-    // blocks of group i: [begin, begin + mtiles * ntiles), m-tiles fastest
+    // blocks of group i: [begin, begin + mtiles * ntiles), m-tiles fastest;
+    // with split K, ksplit copies of that range, one per chunk of slices
     const int ntiles = (a.NPQ + BM - 1) / BM;
     int begin = 0;
     for (int i = 0; i < a.ngroups; ++i) {
@@ -963,11 +1025,52 @@ int launch_conv(ConvArgs a, hipStream_t stream) {
         a.g[i].begin = begin;
         begin += a.g[i].mtiles * ntiles;
     }
-    a.nblocks = begin;
-    auto kern = k_conv<BM, BN, WN, WM>;
+    a.base_blocks = begin;
+    a.nblocks = begin * std::max(1, a.ksplit);
+    auto kern = a.ksplit > 1 ? k_conv<BM, BN, WN, WM, true> : k_conv<BM, BN, WN, WM, false>;
     if (int rc = allow_full_lds(reinterpret_cast<const void *>(kern))) return rc;
     hipLaunchKernelGGL(kern, dim3(a.nblocks), dim3(Cfg::NT), Cfg::lds, stream, a);
     return check_hip(hipGetLastError(), "k_conv");
+}
+
+// Tile shape of the direct kernel for groups of Ms filters over NPQ pixels:
+// 0 = 128 x 128, 1 = 128 x 64, 2 = 64 x 128 (pixels x filters), 3 = 256 x 32;
+// *blocks receives the tile count.
+int direct_pick(const int *Ms, int n, int NPQ, int64_t *blocks) {
+    struct Shape {
+        int BM, BN;
+    };
+    constexpr Shape shapes[4] = {{128, 128}, {128, 64}, {64, 128}, {256, 32}};
+    int maxM = 0;
+    for (int i = 0; i < n; ++i) maxM = std::max(maxM, Ms[i]);
+    int64_t work[3], nb[4], best = -1;
+    for (int c = 0; c < 4; ++c) {
+        int64_t mt = 0, pm = 0;
+        for (int i = 0; i < n; ++i) {
+            const int t = (Ms[i] + shapes[c].BN - 1) / shapes[c].BN;
+            mt += t;
+            pm += (int64_t)t * shapes[c].BN;
+        }
+        nb[c] = mt * ((NPQ + shapes[c].BM - 1) / shapes[c].BM);
+        if (c < 3) {
+            work[c] = pm;
+            if (best < 0 || pm < best) best = pm;
+        }
+    }
+    if (maxM <= 32) {
+        *blocks = nb[3];
+        return 3;
+    }
+    auto near = [&](int c) { return work[c] * 50 <= best * 51; };  // within 2% of the least work
+    int pick = -1;
+    if (near(0) && nb[0] >= 320) {
+        pick = 0;
+    } else {
+        for (int c : {2, 1, 0})
+            if (near(c) && (pick < 0 || nb[c] > nb[pick])) pick = c;
+    }
+    *blocks = nb[pick];
+    return pick;
 }
 
 // One launch for every group of a.  Tile shape (measured on gfx950): 256 x 32
@@ -983,36 +1086,13 @@ int run_conv(ConvArgs a, hipStream_t stream) {
     a.divCy = make_fastdiv((uint32_t)std::max(1, a.Cy));
     a.divQ = make_fastdiv((uint32_t)a.Q);
     a.divD = make_fastdiv((uint32_t)a.D);
-    struct Shape {
-        int BM, BN;
-    };
-    constexpr Shape shapes[3] = {{128, 128}, {128, 64}, {64, 128}};
-    int maxM = 0;
-    for (int i = 0; i < a.ngroups; ++i) maxM = std::max(maxM, a.g[i].M);
-    if (maxM <= 32) return launch_conv<256, 32, 4, 1>(a, stream);
-    int64_t work[3], blocks[3], best = -1;
-    for (int c = 0; c < 3; ++c) {
-        int64_t mt = 0, pm = 0;
-        for (int i = 0; i < a.ngroups; ++i) {
-            const int t = (a.g[i].M + shapes[c].BN - 1) / shapes[c].BN;
-            mt += t;
-            pm += (int64_t)t * shapes[c].BN;
-        }
-        work[c] = pm;
-        blocks[c] = mt * ((a.NPQ + shapes[c].BM - 1) / shapes[c].BM);
-        if (best < 0 || pm < best) best = pm;
-    }
-    auto near = [&](int c) { return work[c] * 50 <= best * 51; };  // within 2% of the least work
-    int pick = -1;
-    if (near(0) && blocks[0] >= 320) {
-        pick = 0;
-    } else {
-        for (int c : {2, 1, 0})
-            if (near(c) && (pick < 0 || blocks[c] > blocks[pick])) pick = c;
-    }
-    switch (pick) {
+    int Ms[SA_MAX_CONV_GROUPS];
+    for (int i = 0; i < a.ngroups; ++i) Ms[i] = a.g[i].M;
+    int64_t blocks;
+    switch (direct_pick(Ms, a.ngroups, a.NPQ, &blocks)) {
         case 0: return launch_conv<128, 128, 2, 2>(a, stream);
         case 1: return launch_conv<128, 64, 2, 2>(a, stream);
+        case 3: return launch_conv<256, 32, 4, 1>(a, stream);
         default: return launch_conv<64, 128, 1, 4>(a, stream);
     }
 }
@@ -1095,6 +1175,11 @@ struct ConvPlan {
     int path[SA_MAX_CONV_GROUPS];
     int pix_bytes[SA_MAX_CONV_GROUPS], nch[SA_MAX_CONV_GROUPS], ch_lo8[SA_MAX_CONV_GROUPS];
     int TM, TN, patch_bytes, tab_bytes, lds;  // k_conv_patch launch (when any group takes it)
+    // split K (launches that would fill few CUs): chunks, and the binary32
+    // partial sums [ksplit][part_stride] at byte part_off of the scratch
+    int ksplit;
+    int64_t part_stride;
+    size_t part_off;
     // geometry the footprint kernel sees: the input itself, or (s2d = factor > 0)
     // its space-to-depth image, which then takes the first s2d_bytes of the scratch
     int s2d, gH, gW, gCx, gC, gD, gs, gpad;
@@ -1108,6 +1193,45 @@ int patch_lds(int TM, int TN, int patch_bytes, int tab_bytes) {
     const int a_bytes = 2 * 32 * TM * kPatchRowA * 2;
     const int c_bytes = 128 * TN * (32 * TM + 8) * 2;
     return std::max(patch_bytes + tab_bytes + a_bytes, c_bytes);
+}
+
+// Split K when every group takes the direct kernel (on the input, or on its
+// gathered im2col rows) and the launches would have fewer than 128 tiles (a
+// batch-1 layer): the 64-column slices are cut into
+// ksplit chunks (at least two slices each, at most 8 chunks, about 256
+// workgroups in all), each workgroup writes binary32 partial sums, and
+// k_splitk_sum adds them in chunk order.  (The footprint kernel is not split:
+// each of its workgroups copies the whole input footprint, which then
+// dominates; measured slower at batch 1.)
+void split_plan(const sa_compact_sizes &s, ConvPlan *pl) {
+    ConvPlan &p = *pl;
+    p.ksplit = 1;
+    int nd = 0, ng = 0, Md[SA_MAX_CONV_GROUPS], Mg[SA_MAX_CONV_GROUPS];
+    int min_sl = 1 << 30;
+    for (int g = 0; g < s.groups; ++g) {
+        if (p.path[g] == kSkip) continue;
+        if (p.path[g] == kPatch) return;
+        if (p.path[g] == kDirect) Md[nd++] = s.M[g];
+        else Mg[ng++] = s.M[g];  // two-phase: the direct kernel over the gathered rows
+        min_sl = std::min(min_sl, s.ldk[g] / kBK);
+    }
+    if (nd + ng == 0) return;
+    int64_t base = 0, b;
+    if (nd > 0) {
+        direct_pick(Md, nd, p.NPQ, &b);
+        base += b;
+    }
+    if (ng > 0) {
+        direct_pick(Mg, ng, p.NPQ, &b);
+        base += b;
+    }
+    if (base >= 128) return;
+    const int64_t ks = std::min<int64_t>({8, (256 + base - 1) / base, min_sl / 2});
+    if (ks < 2) return;
+    p.ksplit = (int)ks;
+    p.part_stride = ((int64_t)p.NPQ * p.Cy + 3) / 4 * 4;
+    p.part_off = (p.ws_need + 255) / 256 * 256;
+    p.ws_need = p.part_off + ((size_t)p.ksplit * p.part_stride * 4 + 255) / 256 * 256;
 }
 
 // Validates the descriptor (beyond validate_conv) and chooses, per conv group,
@@ -1249,6 +1373,7 @@ int conv_plan(const sa_conv_desc &d, ConvPlan *pl) {
             return fail(SA_E_UNSUPPORTED, "conv: gathered rows of group %d need 2 GiB or more", g);
         p.ws_need += ((size_t)bytes + 255) / 256 * 256;  // each gathered group has its own rows
     }
+    split_plan(s, &p);
     return SA_OK;
 }
 
@@ -1293,6 +1418,11 @@ extern "C" int structadmm_conv_fwd(const sa_conv_desc *desc, hipStream_t stream)
     memset(&pa, 0, sizeof pa);
     direct.Y = gathered.Y = pa.Y = d.Y;
     direct.Cy = gathered.Cy = pa.Cy = p.Cy;
+    direct.ksplit = gathered.ksplit = p.ksplit;
+    if (p.ksplit > 1) {
+        direct.part = gathered.part = reinterpret_cast<float *>(static_cast<uint8_t *>(d.ws) + p.part_off);
+        direct.part_stride = gathered.part_stride = p.part_stride;
+    }
     direct.NPQ = gathered.NPQ = pa.NPQ = NPQ;
     direct.H = d.H;
     direct.W = d.W;
@@ -1455,5 +1585,13 @@ extern "C" int structadmm_conv_fwd(const sa_conv_desc *desc, hipStream_t stream)
         }
         if (rc) return rc;
     }
-    return run_conv(gathered, stream);
+    if (int rc = run_conv(gathered, stream)) return rc;
+    if (p.ksplit > 1) {
+        const int64_t total = (int64_t)NPQ * p.Cy;
+        const int64_t blocks = (total + 1023) / 1024;
+        hipLaunchKernelGGL(k_splitk_sum, dim3((unsigned)blocks), dim3(256), 0, stream,
+                           static_cast<const float *>(direct.part), p.part_stride, p.ksplit, d.Y, total);
+        return check_hip(hipGetLastError(), "k_splitk_sum");
+    }
+    return SA_OK;
 }

@@ -306,6 +306,21 @@ def test_conv_table_replay_batch1(block):
         assert err <= TOL, (block, L.name, err)
 
 
+def test_conv_dense_batch1():
+    """The same-shape dense CONVs of AlexNet conv1-5 at batch 1 (the layers
+    split their columns over workgroups and add the binary32 partial sums)."""
+    wl = WORKLOADS["alexnet_shape30"]
+    for li, L in enumerate(wl.layers):
+        W, _ = layer_tensors(wl, li)
+        got = sa.compact(to_dev(W), L.groups)
+        rc = oracle.compact(W, L.groups)
+        X = input_nchw(wl, li, batch=1)
+        Y = sa.conv_fwd(sa.pack_nhwc(to_dev(X)), got[0], got[2], got[3], got[4], L.C, L.D, L.stride, L.pad)
+        Yr = oracle.conv(oracle.pack(X), rc, L.C, L.D, L.stride, L.pad)
+        err = maxabs_over_rms(bf16_bits_to_f64(Y.cpu().numpy()), Yr)
+        assert err <= TOL, (L.name, err)
+
+
 def test_conv_is_deterministic():
     t = torch()
     rng = np.random.default_rng(4)
