@@ -28,7 +28,8 @@
 namespace sa {
 namespace {
 
-constexpr int kTab = 32;           // layers per launch (kernel-argument table, < 4 KiB)
+constexpr int kTab = 64;           // layers per launch (kernel-argument table, < 8 KiB; ResNet-50's
+                                   // 53 convolutions take one launch per phase)
 constexpr int kRowThreads = 256;   // 4 wavefronts, one weight row each at a time
 constexpr int kColThreads = 256;
 constexpr int kColBand = 32;       // rows per band of column partial sums
@@ -466,8 +467,8 @@ struct ApplyTab {
     int32_t nl;
 };
 
-static_assert(sizeof(RowTab) < 4096 && sizeof(ColTab) < 4096 && sizeof(SelTab) < 4096 &&
-                  sizeof(DualTab) < 4096 && sizeof(ApplyTab) < 4096 && sizeof(SgdTab) < 4096,
+static_assert(sizeof(RowTab) < 8192 && sizeof(ColTab) < 8192 && sizeof(SelTab) < 8192 &&
+                  sizeof(DualTab) < 8192 && sizeof(ApplyTab) < 8192 && sizeof(SgdTab) < 8192,
               "layer tables must fit the kernel-argument segment");
 
 constexpr int kApplyThreads = 256;

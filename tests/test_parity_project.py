@@ -92,7 +92,7 @@ def test_project_mixed_multilayer_call():
     rng = np.random.default_rng(123)
     specs = [((64, 32, 3, 3), sa.FILTER, 20), ((48, 24, 3, 3), sa.CHANNEL, 7), ((32, 16, 3, 3), sa.SHAPE, 50),
              ((16, 16, 3, 3), sa.ELEMENT, 1000), ((96, 3, 11, 11), sa.SHAPE, 109), ((64, 64, 1, 1), sa.FILTER, 38)]
-    specs = specs * 4  # 24 layers: more than one kernel-argument table
+    specs = specs * 12  # 72 layers: more than one kernel-argument table of 64 layers
     layers, refs = [], []
     for i, (shape, kind, k) in enumerate(specs):
         W = (0.05 * rng.standard_normal(shape)).astype(np.float32)
