@@ -560,7 +560,7 @@ struct PatchCfg {
 };
 
 template <int TM, int TN>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k_conv_patch(PatchArgs a) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(TM >= 6 ? 1 : 2))) void k_conv_patch(PatchArgs a) {
     using Cfg = PatchCfg<TM, TN>;
     constexpr int NT = Cfg::NT, BNB = Cfg::BNB, BMB = Cfg::BMB, AR = Cfg::AR;
     constexpr int CPS = kPatchSlice / 8;  // 16-B chunks per weight row of a slice
@@ -1187,7 +1187,8 @@ struct ConvPlan {
     size_t ws_need;  // scratch: space-to-depth image, then the two-phase groups' rows
 };
 
-constexpr int kPatchTMs[4] = {4, 3, 2, 1};
+constexpr int kPatchTMs[5] = {6, 4, 3, 2, 1};
+constexpr int kPatchFixed = 9;  // per-workgroup footprint copy, in 32-filter-block units
 
 int patch_lds(int TM, int TN, int patch_bytes, int tab_bytes) {
     const int a_bytes = 2 * 32 * TM * kPatchRowA * 2;
@@ -1317,19 +1318,44 @@ int conv_plan(const sa_conv_desc &d, ConvPlan *pl) {
         }
     }
     if (ngath > 0) {
-        // tile shape: least padded filter work, then the larger tile
-        int best_tm = 4;
-        int64_t best_cost = -1;
+        // filter tile: least padded filter work; among those, the fewest
+        // rounds of workgroups times the per-workgroup time, modelled (at 128
+        // pixels per tile) as a fixed part for the footprint copy worth nine
+        // 32-filter blocks (measured on the 13x13 AlexNet layers) plus one
+        // unit per 32-filter block; TM >= 6 runs one workgroup per CU
+        // (registers), smaller tiles up to two (LDS permitting)
+        const int Hp = p.gH + 2 * p.gpad, Wp = p.gW + 2 * p.gpad;
+        const int Ws = (Wp + p.gs - 1) / p.gs, Wpp = Ws * p.gs;
+        p.tab_bytes = ((max_ldk + 2 * kPatchSlice) * 4 + 15) / 16 * 16;  // two slices past the last
+        int64_t least = -1;
         for (int tm : kPatchTMs) {
             int64_t cost = 0;
             for (int g = 0; g < s.groups; ++g)
                 if (p.path[g] == kPatch) cost += (s.M[g] + 32 * tm - 1) / (32 * tm) * (32 * tm);
-            if (best_cost < 0 || cost < best_cost) best_cost = cost, best_tm = tm;
+            if (least < 0 || cost < least) least = cost;
         }
-        const int Hp = p.gH + 2 * p.gpad, Wp = p.gW + 2 * p.gpad;
-        const int Ws = (Wp + p.gs - 1) / p.gs, Wpp = Ws * p.gs;
+        const int rows128 = patch_rows(p.NPQ, p.P, p.Q, Hp, p.gs, p.gC, 128);
+        int64_t pb128 = 0;
+        for (int g = 0; g < s.groups; ++g)
+            if (p.path[g] == kPatch)
+                pb128 = std::max<int64_t>(pb128, ((int64_t)rows128 * Wpp * p.pix_bytes[g] + 15) / 16 * 16);
+        int best_tm = 4;
+        int64_t best_t = -1;
+        for (int tm : kPatchTMs) {
+            int64_t cost = 0, mt = 0;
+            for (int g = 0; g < s.groups; ++g)
+                if (p.path[g] == kPatch) {
+                    cost += (s.M[g] + 32 * tm - 1) / (32 * tm) * (32 * tm);
+                    mt += (s.M[g] + 32 * tm - 1) / (32 * tm);
+                }
+            if (cost != least) continue;
+            const int64_t lds = pb128 <= kLdsBytes ? patch_lds(tm, 1, (int)pb128, p.tab_bytes) : kLdsBytes;
+            const int64_t per_cu = tm >= 6 ? 1 : std::max<int64_t>(1, std::min<int64_t>(2, kLdsBytes / lds));
+            const int64_t wgs = mt * ((p.NPQ + 127) / 128);
+            const int64_t t = (wgs + 256 * per_cu - 1) / (256 * per_cu) * (kPatchFixed + tm);
+            if (best_t < 0 || t < best_t) best_t = t, best_tm = tm;
+        }
         p.TM = best_tm;
-        p.tab_bytes = ((max_ldk + 2 * kPatchSlice) * 4 + 15) / 16 * 16;  // two slices past the last
         auto fits = [&](int tn, int *patch_bytes) {
             const int rows = patch_rows(p.NPQ, p.P, p.Q, Hp, p.gs, p.gC, 128 * tn);
             int64_t pb = 0;
@@ -1573,6 +1599,8 @@ extern "C" int structadmm_conv_fwd(const sa_conv_desc *desc, hipStream_t stream)
     if (pa.ngroups > 0) {
         int rc = SA_OK;
         switch (p.TM * 10 + p.TN) {
+            case 61: rc = launch_patch<6, 1>(pa, p.lds, stream); break;
+            case 62: rc = launch_patch<6, 2>(pa, p.lds, stream); break;
             case 41: rc = launch_patch<4, 1>(pa, p.lds, stream); break;
             case 42: rc = launch_patch<4, 2>(pa, p.lds, stream); break;
             case 31: rc = launch_patch<3, 1>(pa, p.lds, stream); break;
