@@ -56,6 +56,9 @@ def parse():
                         "MIOpen, density sweep, achievable peaks) and write the report to JSON")
     p.add_argument("--tables", metavar="JSON", default=None,
                    help="only the batch-1 replay of the pruned AlexNet layers of Tables 1-2 (CONV speedups)")
+    p.add_argument("--admm", metavar="WORKLOAD", default=None,
+                   help="only the ADMM step (fused projection, gradient, SGD steps) of one workload, "
+                        "one call and replicated; prints one JSON line")
     p.add_argument("--sparse", metavar="JSON", default=None,
                    help="only the CSR CONV of non-structured pruning: density sweep of the [256,256,3,3] "
                         "layer and batch-1 AlexNet conv2-5 at the sparsities of Tables 4-5")
@@ -728,6 +731,15 @@ def main():
         return
     if args.sparse:
         sparse(args.sparse)
+        return
+    if args.admm:
+        import torch
+        import paper_1807_11091_amd as sa
+        from workloads import WORKLOADS
+        if not torch.cuda.is_available():
+            raise SystemExit("bench.py needs a GPU")
+        sa.lib()
+        print(json.dumps({"workload": args.admm, **suite_admm(torch, sa, WORKLOADS[args.admm], 0)}))
         return
     if args.suite:
         suite(args.suite)
