@@ -886,6 +886,7 @@ struct S2dArgs {
     int32_t N, H, W, Cx, s, pad, Hs, Ws, Cs, Creal;  // Creal = s*s*Cx, Cs = Creal rounded up to 8
     int32_t chunks;                           // N*Hs*Ws*Cs / 8 (< 2^27: the image is below 2 GiB)
     uint32_t x_bytes;                         // bytes of X (below 2 GiB)
+    int32_t runs;                             // k_s2d_rows: copy whole runs (see there)
     FastDiv divCs8, divWs, divHs, divCx, divS;
 };
 
@@ -969,8 +970,37 @@ __global__ __launch_bounds__(256) void k_s2d_rows(S2dArgs a) {
     }
     __syncthreads();
     const uint16_t *rowbuf = reinterpret_cast<const uint16_t *>(smem) + (int)((b0 - a0) >> 1);
-    const int cs8 = a.Cs / 8;
     uint16_t *dst = a.Xs + (int64_t)ni * a.Ws * a.Cs;
+    if (a.runs) {
+        // Cs = s*s*Cx and s*Cx*2 bytes a multiple of 8: output pixel j holds,
+        // for each input row ra of the block, the s*Cx consecutive inputs
+        // X[h0 + ra][j*s - pad ..][0 .. Cx) as one run of consecutive channels,
+        // 8-byte aligned in the output; one thread per (j, ra) run
+        const int run = a.s * a.Cx;
+        for (int t = threadIdx.x; t < a.Ws * a.s; t += 256) {
+            const int j = (int)fdiv((uint32_t)t, a.divS), ra = t - j * a.s;
+            const int w0 = j * a.s - a.pad;
+            const bool row_in = (unsigned)(h0 + ra) < (unsigned)a.H;
+            const uint16_t *src = rowbuf + ra * rowlen + w0 * a.Cx;
+            uint2 *out = reinterpret_cast<uint2 *>(dst + (int64_t)j * a.Cs + ra * run);
+            const bool full = row_in && w0 >= 0 && w0 + a.s <= a.W;  // no zero padding in the run
+            for (int q = 0; q < run; q += 4) {
+                uint32_t v[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    if (full) {
+                        v[e] = src[q + e];
+                    } else {  // a run at the image border: element by element
+                        const int w = w0 + (q + e) / a.Cx;
+                        v[e] = row_in && (unsigned)w < (unsigned)a.W ? src[q + e] : 0u;
+                    }
+                }
+                out[q / 4] = make_uint2(v[0] | (v[1] << 16), v[2] | (v[3] << 16));
+            }
+        }
+        return;
+    }
+    const int cs8 = a.Cs / 8;
     for (int e = threadIdx.x; e < a.Ws * cs8; e += 256) {
         const int j = (int)fdiv((uint32_t)e, a.divCs8);
         const int c0 = (e - j * cs8) * 8;
@@ -1482,6 +1512,7 @@ extern "C" int structadmm_conv_fwd(const sa_conv_desc *desc, hipStream_t stream)
         sa2.divHs = make_fastdiv((uint32_t)p.gH);
         sa2.divCx = make_fastdiv((uint32_t)d.Cx);
         sa2.divS = make_fastdiv((uint32_t)p.s2d);
+        sa2.runs = sa2.Cs == sa2.Creal && (p.s2d * d.Cx * 2) % 8 == 0;
         sa2.x_bytes = x_bytes;
         const size_t rowbytes = (size_t)p.s2d * d.W * d.Cx * 2 + 32;  // the s rows plus alignment slack
         if (rowbytes <= (size_t)kS2dRowLds) {
