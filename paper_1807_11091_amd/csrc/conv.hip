@@ -531,8 +531,7 @@ struct PatchGroup {
     const int32_t *col_ch;   // group base
     const int32_t *col_tap;  // group base
     int32_t M, K, ldk, o_off, ch_lo, nch, pix_bytes, mtiles, begin;
-    int32_t dch, dw, dpr;    // fill item step of one workgroup (256 chunks) in (channel chunk, column, row)
-    FastDiv divNch, divRow;  // 16-byte chunks per pixel, chunks per padded input row
+    FastDiv divNch;          // 16-byte chunks per pixel
 };
 struct PatchArgs {
     const uint16_t *X;
@@ -616,10 +615,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(TM >= 6 ? 1
     const int g0 = i0 * a.Hp + (r0 - i0 * a.P) * a.stride;
     const int g1 = i1 * a.Hp + (r1 - i1 * a.P) * a.stride + a.C;  // exclusive
     const int nch = G.nch, pixb = G.pix_bytes;
-    // source order (padded row, padded column, chunk): consecutive threads read
-    // consecutive input bytes; columns land at their de-interleaved position
-    const int rowchunks = a.Wp * nch;
-    const int total = (g1 - g0) * rowchunks;
     const __amdgpu_buffer_rsrc_t xrs = rsrc(a.X, a.x_bytes);
 
     // 2. column table: (kernel row, kernel column, channel) -> byte offset.
@@ -653,65 +648,81 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(TM >= 6 ? 1
         }
     }
 
-    // 1. the copy, in source order (padded row, padded column, chunk): item
-    //    tid, then steps of NT items (one carry at most per coordinate)
-    int pr = (int)fdiv((uint32_t)tid, G.divRow);
-    const int rem = tid - pr * rowchunks;
-    int wpad = (int)fdiv((uint32_t)rem, G.divNch);
-    int ch = rem - wpad * nch;
-    constexpr int kFill = 32;  // 16-byte loads in flight per thread
-    for (int base = tid; base < total; base += NT * kFill) {
-        uint4 v[kFill];
-        int dst[kFill];
+    // 1. the copy.  Every padded row is split the same way over the threads:
+    //    item e of a row is chunk c of padded column 4*b + (e mod 4), with
+    //    (b, c) = divmod(e / 4, nch), so the 64 lanes of a wavefront hold 16
+    //    consecutive chunks of 4 neighbouring columns (256-byte runs of the
+    //    input), and with an odd number of words per pixel their 4-byte LDS
+    //    writes fall on distinct banks.  A thread's items of a row (two per
+    //    pass) keep their source and LDS offsets across rows; the row's own
+    //    terms (image, input row, zero halo) are the same for every thread.
+    const int nrows = g1 - g0;
+    const int rowitems = 4 * nch * ((a.Wp + 3) >> 2);
+    const int J = (rowitems + NT - 1) / NT;  // items of a row per thread
+    const int rowb = a.Wpp * pixb;           // LDS bytes per padded row
+    const uint32_t rowsrc = (uint32_t)a.W * (uint32_t)a.Cx * 2u;
+    constexpr int kRows = 16;  // rows per batch: up to 2 * kRows 16-byte loads in flight per thread
+    for (int j0 = 0; j0 < J; j0 += 2) {
+        const bool two = j0 + 1 < J;
+        uint32_t so[2];  // source offset within the input row; past the buffer for the zero halo
+        int cpo[2];      // LDS offset within the padded row; -1: no item
 #pragma unroll
-        for (int u = 0; u < kFill; ++u) {
-            dst[u] = -1;
-            v[u] = make_uint4(0, 0, 0, 0);
-            if (base + u * NT < total) {
-                const int jw = a.stride == 1 ? wpad : (int)fdiv((uint32_t)wpad, a.divS);
-                const int cp = (wpad - jw * a.stride) * a.Ws + jw;
-                const int gr = g0 + pr;
-                const int img = (int)fdiv((uint32_t)gr, a.divHp);
-                const int h = gr - img * a.Hp - a.pad, w = wpad - a.pad;
-                dst[u] = (pr * a.Wpp + cp) * pixb + ch * 16;
-                if (img < a.N && (unsigned)h < (unsigned)a.H && (unsigned)w < (unsigned)a.W)
-                    v[u] = bload16(xrs, ((((uint32_t)(img * a.H + h) * a.W + w) * a.Cx + G.ch_lo) + ch * 8) * 2u);
-            }
-            ch += G.dch;
-            const int c1 = ch >= nch;
-            ch -= c1 ? nch : 0;
-            wpad += G.dw + c1;
-            const int c2 = wpad >= a.Wp;
-            wpad -= c2 ? a.Wp : 0;
-            pr += G.dpr + c2;
-        }
-        if (base == tid) {  // while the first loads are in flight: the table
-#pragma unroll
-            for (int q = 0; q < kTabRegs; ++q) {
-                const int k = tid + q * NT;
-                if (k < ntab) {
-                    if (k < G.K) tab_entry(k, ttap[q], tch[q]);
-                    else tab[k] = 0;  // columns past K: zeroed after the gather
+        for (int jj = 0; jj < 2; ++jj) {
+            const int e = tid + (j0 + jj) * NT;
+            so[jj] = kInvalidOffset;
+            cpo[jj] = -1;
+            if (j0 + jj < J && e < rowitems) {
+                const int q = e >> 2;
+                const int b = (int)fdiv((uint32_t)q, G.divNch);
+                const int c = q - b * nch;
+                const int wpad = 4 * b + (e & 3);
+                if (wpad < a.Wp) {
+                    const int jw = (int)fdiv((uint32_t)wpad, a.divS);
+                    cpo[jj] = ((wpad - jw * a.stride) * a.Ws + jw) * pixb + c * 16;
+                    const int w = wpad - a.pad;
+                    if ((unsigned)w < (unsigned)a.W) so[jj] = ((uint32_t)w * (uint32_t)a.Cx + G.ch_lo + c * 8) * 2u;
                 }
             }
         }
+        for (int pr0 = 0; pr0 < nrows; pr0 += kRows) {
+            uint4 v[kRows][2];
 #pragma unroll
-        for (int u = 0; u < kFill; ++u) {
-            if (dst[u] < 0) continue;
-            uint32_t *d32 = reinterpret_cast<uint32_t *>(patch + dst[u]);
-            d32[0] = v[u].x;
-            d32[1] = v[u].y;
-            d32[2] = v[u].z;
-            d32[3] = v[u].w;
-        }
-    }
-    if (total <= tid) {  // a thread without copy items still writes its table entries
+            for (int r = 0; r < kRows; ++r) {
+                const int pr = pr0 + r;
+                const int gr = g0 + pr;
+                const int img = (int)fdiv((uint32_t)gr, a.divHp);
+                const int h = gr - img * a.Hp - a.pad;
+                const bool in = pr < nrows && img < a.N && (unsigned)h < (unsigned)a.H;
+                const uint32_t sb = (uint32_t)(img * a.H + h) * rowsrc;  // below 2^31 when in
 #pragma unroll
-        for (int q = 0; q < kTabRegs; ++q) {
-            const int k = tid + q * NT;
-            if (k < ntab) {
-                if (k < G.K) tab_entry(k, ttap[q], tch[q]);
-                else tab[k] = 0;
+                for (int jj = 0; jj < 2; ++jj) {
+                    v[r][jj] = make_uint4(0, 0, 0, 0);
+                    if (in && (jj == 0 || two)) v[r][jj] = bload16(xrs, sb + so[jj]);
+                }
+            }
+            if (j0 == 0 && pr0 == 0) {  // while the first loads are in flight: the table
+#pragma unroll
+                for (int q = 0; q < kTabRegs; ++q) {
+                    const int k = tid + q * NT;
+                    if (k < ntab) {
+                        if (k < G.K) tab_entry(k, ttap[q], tch[q]);
+                        else tab[k] = 0;  // columns past K: zeroed after the gather
+                    }
+                }
+            }
+#pragma unroll
+            for (int r = 0; r < kRows; ++r) {
+                const int pr = pr0 + r;
+                if (pr >= nrows) continue;
+#pragma unroll
+                for (int jj = 0; jj < 2; ++jj) {
+                    if (cpo[jj] < 0) continue;
+                    uint32_t *d32 = reinterpret_cast<uint32_t *>(patch + pr * rowb + cpo[jj]);
+                    d32[0] = v[r][jj].x;
+                    d32[1] = v[r][jj].y;
+                    d32[2] = v[r][jj].z;
+                    d32[3] = v[r][jj].w;
+                }
             }
         }
     }
@@ -1569,10 +1580,6 @@ extern "C" int structadmm_conv_fwd(const sa_conv_desc *desc, hipStream_t stream)
             G.nch = p.nch[g];
             G.pix_bytes = p.pix_bytes[g];
             G.divNch = make_fastdiv((uint32_t)G.nch);
-            G.divRow = make_fastdiv((uint32_t)(pa.Wp * G.nch));
-            G.dch = 256 % G.nch;  // k_conv_patch runs 256 threads
-            G.dw = 256 / G.nch % pa.Wp;
-            G.dpr = 256 / G.nch / pa.Wp;
             continue;
         }
         const bool vec = p.path[g] == kDirect;
