@@ -945,7 +945,8 @@ __global__ __launch_bounds__(256) void k_s2d(S2dArgs a) {
 // the range fits kS2dRowLds (the kernel above covers the rest).
 constexpr int kS2dRowLds = 64 * 1024;
 
-__global__ __launch_bounds__(256) void k_s2d_rows(S2dArgs a) {
+template <int NT>
+__global__ __launch_bounds__(NT) void k_s2d_rows(S2dArgs a) {
     extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
     const int ni = blockIdx.x;  // (n, i)
     const int n = (int)fdiv((uint32_t)ni, a.divHs);
@@ -956,11 +957,11 @@ __global__ __launch_bounds__(256) void k_s2d_rows(S2dArgs a) {
     const int64_t a0 = b0 & ~(int64_t)15;
     const int nchunk = (int)((b0 - a0 + (int64_t)a.s * rowlen * 2 + 15) >> 4);
     const __amdgpu_buffer_rsrc_t xrs = rsrc(a.X, a.x_bytes);
-    for (int base = 0; base < nchunk; base += 4 * 256) {
+    for (int base = 0; base < nchunk; base += 4 * NT) {
         uint4 v[4];
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-            const int ch = base + u * 256 + (int)threadIdx.x;
+            const int ch = base + u * NT + (int)threadIdx.x;
             const int64_t off = a0 + (int64_t)ch * 16;
             v[u] = bload16(xrs, (ch < nchunk && off >= 0 && off + 16 <= (int64_t)a.x_bytes) ? (uint32_t)off : kInvalidOffset);
             // the chunk that holds the input's last bytes (a buffer load reads
@@ -975,7 +976,7 @@ __global__ __launch_bounds__(256) void k_s2d_rows(S2dArgs a) {
         }
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-            const int ch = base + u * 256 + (int)threadIdx.x;
+            const int ch = base + u * NT + (int)threadIdx.x;
             if (ch < nchunk) reinterpret_cast<uint4 *>(smem)[ch] = v[u];
         }
     }
@@ -988,7 +989,7 @@ __global__ __launch_bounds__(256) void k_s2d_rows(S2dArgs a) {
         // X[h0 + ra][j*s - pad ..][0 .. Cx) as one run of consecutive channels,
         // 8-byte aligned in the output; one thread per (j, ra) run
         const int run = a.s * a.Cx;
-        for (int t = threadIdx.x; t < a.Ws * a.s; t += 256) {
+        for (int t = threadIdx.x; t < a.Ws * a.s; t += NT) {
             const int j = (int)fdiv((uint32_t)t, a.divS), ra = t - j * a.s;
             const int w0 = j * a.s - a.pad;
             const bool row_in = (unsigned)(h0 + ra) < (unsigned)a.H;
@@ -1012,7 +1013,7 @@ __global__ __launch_bounds__(256) void k_s2d_rows(S2dArgs a) {
         return;
     }
     const int cs8 = a.Cs / 8;
-    for (int e = threadIdx.x; e < a.Ws * cs8; e += 256) {
+    for (int e = threadIdx.x; e < a.Ws * cs8; e += NT) {
         const int j = (int)fdiv((uint32_t)e, a.divCs8);
         const int c0 = (e - j * cs8) * 8;
         int blk = (int)fdiv((uint32_t)c0, a.divCx);
@@ -1527,8 +1528,9 @@ extern "C" int structadmm_conv_fwd(const sa_conv_desc *desc, hipStream_t stream)
         sa2.x_bytes = x_bytes;
         const size_t rowbytes = (size_t)p.s2d * d.W * d.Cx * 2 + 32;  // the s rows plus alignment slack
         if (rowbytes <= (size_t)kS2dRowLds) {
-            if (int rc = allow_full_lds(reinterpret_cast<const void *>(k_s2d_rows))) return rc;
-            hipLaunchKernelGGL(k_s2d_rows, dim3(d.N * p.gH), dim3(256), rowbytes, stream, sa2);
+            // 128 threads: up to 16 workgroups per CU, so that enough rows are in flight
+            if (int rc = allow_full_lds(reinterpret_cast<const void *>(k_s2d_rows<128>))) return rc;
+            hipLaunchKernelGGL(k_s2d_rows<128>, dim3(d.N * p.gH), dim3(128), rowbytes, stream, sa2);
         } else {
             hipLaunchKernelGGL(k_s2d, dim3((unsigned)std::min(16384, (sa2.chunks + 255) / 256)), dim3(256), 0, stream,
                                sa2);
