@@ -548,19 +548,19 @@ struct PatchArgs {
     PatchGroup g[SA_MAX_CONV_GROUPS];
 };
 
-template <int TM, int TN>
+template <int TM, int TN, int NW>
 struct PatchCfg {
-    static constexpr int NT = 256;
-    static constexpr int BNB = 32 * TM;   // filters per tile
-    static constexpr int BMB = 128 * TN;  // pixels per tile
+    static constexpr int NT = 64 * NW;         // NW wavefronts
+    static constexpr int BNB = 32 * TM;        // filters per tile
+    static constexpr int BMB = 32 * NW * TN;   // pixels per tile
     static constexpr int AR = (BNB * (kPatchSlice / 8) + NT - 1) / NT;  // 16-B weight chunks per thread
     static constexpr int a_bytes = 2 * BNB * kPatchRowA * 2;
     static constexpr int c_bytes = BMB * (BNB + 8) * 2;
 };
 
-template <int TM, int TN>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(TM >= 6 ? 1 : 2))) void k_conv_patch(PatchArgs a) {
-    using Cfg = PatchCfg<TM, TN>;
+template <int TM, int TN, int NW>
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(TM >= 6 && NW <= 4 ? 1 : 2))) void k_conv_patch(PatchArgs a) {
+    using Cfg = PatchCfg<TM, TN, NW>;
     constexpr int NT = Cfg::NT, BNB = Cfg::BNB, BMB = Cfg::BMB, AR = Cfg::AR;
     constexpr int CPS = kPatchSlice / 8;  // 16-B chunks per weight row of a slice
 
@@ -1195,9 +1195,9 @@ int gather_group(GatherArgs g, int ch_span, hipStream_t stream) {
 // ---------------------------------------------------------------- planning
 enum GroupPath { kSkip, kDirect, kPatch, kGather };
 
-template <int TM, int TN>
+template <int TM, int TN, int NW = 4>
 int launch_patch(PatchArgs a, int lds, hipStream_t stream) {
-    using Cfg = PatchCfg<TM, TN>;
+    using Cfg = PatchCfg<TM, TN, NW>;
     const int ntiles = (a.NPQ + Cfg::BMB - 1) / Cfg::BMB;
     int begin = 0;
     for (int i = 0; i < a.ngroups; ++i) {
@@ -1206,7 +1206,7 @@ int launch_patch(PatchArgs a, int lds, hipStream_t stream) {
         begin += a.g[i].mtiles * ntiles;
     }
     a.nblocks = begin;
-    auto kern = k_conv_patch<TM, TN>;
+    auto kern = k_conv_patch<TM, TN, NW>;
     if (int rc = allow_full_lds(reinterpret_cast<const void *>(kern))) return rc;
     hipLaunchKernelGGL(kern, dim3(a.nblocks), dim3(Cfg::NT), (size_t)lds, stream, a);
     return check_hip(hipGetLastError(), "k_conv_patch");
@@ -1216,7 +1216,7 @@ struct ConvPlan {
     int P, Q, NPQ, Cy;
     int path[SA_MAX_CONV_GROUPS];
     int pix_bytes[SA_MAX_CONV_GROUPS], nch[SA_MAX_CONV_GROUPS], ch_lo8[SA_MAX_CONV_GROUPS];
-    int TM, TN, patch_bytes, tab_bytes, lds;  // k_conv_patch launch (when any group takes it)
+    int TM, TN, NW, patch_bytes, tab_bytes, lds;  // k_conv_patch launch (when any group takes it; NW wavefronts)
     // split K (launches that would fill few CUs): chunks, and the binary32
     // partial sums [ksplit][part_stride] at byte part_off of the scratch
     int ksplit;
@@ -1232,9 +1232,9 @@ struct ConvPlan {
 constexpr int kPatchTMs[5] = {6, 4, 3, 2, 1};
 constexpr int kPatchFixed = 9;  // per-workgroup footprint copy, in 32-filter-block units
 
-int patch_lds(int TM, int TN, int patch_bytes, int tab_bytes) {
+int patch_lds(int TM, int TN, int patch_bytes, int tab_bytes, int NW = 4) {
     const int a_bytes = 2 * 32 * TM * kPatchRowA * 2;
-    const int c_bytes = 128 * TN * (32 * TM + 8) * 2;
+    const int c_bytes = 32 * NW * TN * (32 * TM + 8) * 2;
     return std::max(patch_bytes + tab_bytes + a_bytes, c_bytes);
 }
 
@@ -1292,6 +1292,7 @@ int conv_plan(const sa_conv_desc &d, ConvPlan *pl) {
         return fail(SA_E_UNSUPPORTED, "conv: input of 2 GiB or more");
     ConvPlan &p = *pl;
     memset(&p, 0, sizeof p);
+    p.NW = 4;
     p.P = (int)P;
     p.Q = (int)Q;
     p.NPQ = (int)NPQ;
@@ -1425,6 +1426,28 @@ int conv_plan(const sa_conv_desc &d, ConvPlan *pl) {
         }
         if (p.TN > 0) {
             p.lds = patch_lds(p.TM, p.TN, p.patch_bytes, p.tab_bytes);
+            // six wavefronts (192-pixel tiles) when that saves rounds of workgroups
+            // over the 256 CUs: a launch of one workgroup per CU whose last round
+            // is partly filled (AlexNet conv4/conv5: 338 tiles) can take one round
+            // fewer, each workgroup about 1.5 times as long
+            if (p.TN == 1 && (p.TM == 6 || p.TM == 4)) {
+                const int rows6 = patch_rows(p.NPQ, p.P, p.Q, Hp, p.gs, p.gC, 192);
+                int64_t pb6 = 0;
+                for (int g = 0; g < s.groups; ++g)
+                    if (p.path[g] == kPatch) pb6 = std::max<int64_t>(pb6, ((int64_t)rows6 * Wpp * p.pix_bytes[g] + 15) / 16 * 16);
+                const int64_t lds6 = pb6 <= kLdsBytes ? patch_lds(p.TM, 1, (int)pb6, p.tab_bytes, 6) : (int64_t)kLdsBytes + 1;
+                if (lds6 <= kLdsBytes) {
+                    const int64_t per4 = p.TM >= 6 ? 1 : std::max<int64_t>(1, std::min<int64_t>(2, kLdsBytes / p.lds));
+                    const int64_t per6 = std::max<int64_t>(1, std::min<int64_t>(2, kLdsBytes / lds6));
+                    const int64_t r4 = (mt * ((p.NPQ + 127) / 128) + 256 * per4 - 1) / (256 * per4);
+                    const int64_t r6 = (mt * ((p.NPQ + 191) / 192) + 256 * per6 - 1) / (256 * per6);
+                    if (r6 * 3 < r4 * 2) {
+                        p.NW = 6;
+                        p.patch_bytes = (int)pb6;
+                        p.lds = (int)lds6;
+                    }
+                }
+            }
         } else {
             for (int g = 0; g < s.groups; ++g)
                 if (p.path[g] == kPatch) p.path[g] = kGather;
@@ -1638,17 +1661,19 @@ extern "C" int structadmm_conv_fwd(const sa_conv_desc *desc, hipStream_t stream)
     if (int rc = run_conv(direct, stream)) return rc;
     if (pa.ngroups > 0) {
         int rc = SA_OK;
-        switch (p.TM * 10 + p.TN) {
-            case 61: rc = launch_patch<6, 1>(pa, p.lds, stream); break;
-            case 62: rc = launch_patch<6, 2>(pa, p.lds, stream); break;
-            case 41: rc = launch_patch<4, 1>(pa, p.lds, stream); break;
-            case 42: rc = launch_patch<4, 2>(pa, p.lds, stream); break;
-            case 31: rc = launch_patch<3, 1>(pa, p.lds, stream); break;
-            case 32: rc = launch_patch<3, 2>(pa, p.lds, stream); break;
-            case 21: rc = launch_patch<2, 1>(pa, p.lds, stream); break;
-            case 22: rc = launch_patch<2, 2>(pa, p.lds, stream); break;
-            case 11: rc = launch_patch<1, 1>(pa, p.lds, stream); break;
-            case 12: rc = launch_patch<1, 2>(pa, p.lds, stream); break;
+        switch (p.TM * 100 + p.TN * 10 + p.NW) {
+            case 616: rc = launch_patch<6, 1, 6>(pa, p.lds, stream); break;
+            case 416: rc = launch_patch<4, 1, 6>(pa, p.lds, stream); break;
+            case 614: rc = launch_patch<6, 1>(pa, p.lds, stream); break;
+            case 624: rc = launch_patch<6, 2>(pa, p.lds, stream); break;
+            case 414: rc = launch_patch<4, 1>(pa, p.lds, stream); break;
+            case 424: rc = launch_patch<4, 2>(pa, p.lds, stream); break;
+            case 314: rc = launch_patch<3, 1>(pa, p.lds, stream); break;
+            case 324: rc = launch_patch<3, 2>(pa, p.lds, stream); break;
+            case 214: rc = launch_patch<2, 1>(pa, p.lds, stream); break;
+            case 224: rc = launch_patch<2, 2>(pa, p.lds, stream); break;
+            case 114: rc = launch_patch<1, 1>(pa, p.lds, stream); break;
+            case 124: rc = launch_patch<1, 2>(pa, p.lds, stream); break;
             default: return fail(SA_E_ARG, "conv: no tile shape for the gathered groups");
         }
         if (rc) return rc;
