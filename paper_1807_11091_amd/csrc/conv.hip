@@ -510,7 +510,8 @@ __global__ __launch_bounds__(256) void k_im2col_global(GatherArgs a) {
 
 // ---------------------------------------------------------------- k_conv_patch
 // Gathered groups without a scratch pass.  A workgroup owns the output tile
-// (32*TM filters) x (128*TN pixels) of one conv group:
+// (32*TM filters) x (32*NW*TN pixels) of one conv group, NW wavefronts (4, or
+// 6 when that saves a round of workgroups over the CUs):
 //   1. the input footprint of its pixels (the group's channel span, zero
 //      halo) is copied once into LDS; for stride s > 1 the padded columns are
 //      stored de-interleaved (column w at (w mod s) * Ws + w div s), so the
@@ -520,7 +521,7 @@ __global__ __launch_bounds__(256) void k_im2col_global(GatherArgs a) {
 //   3. each wavefront owns 32*TN pixels and gathers its MFMA B fragments
 //      straight from the copy into registers (lane = pixel, 8 columns per
 //      lane), while the weight slices (A) are staged through LDS, two
-//      buffers of 32 columns, shared by the four wavefronts.
+//      buffers of 32 columns, shared by the wavefronts.
 // Only ceil(K/16) column steps are run; columns past K in the last step are
 // zeroed in registers, so padding never multiplies a value from the input.
 constexpr int kPatchSlice = 32;                // columns per staged weight slice
