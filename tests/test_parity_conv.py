@@ -143,6 +143,9 @@ SMALL = [
     (2, 32, 8, 8, 50, 3, 3, 1, 1, 2, sa.FILTER, 0.62),
     # input rows too wide for an LDS copy of the footprint: two-phase gather
     (1, 64, 3, 2100, 40, 3, 3, 1, 1, 1, sa.SHAPE, 0.3),
+    # six-wavefront tiles: 529 tiles of 128 pixels take two rounds at two
+    # workgroups per CU, 353 of 192 pixels one (tiles span image boundaries)
+    (400, 16, 13, 13, 128, 3, 3, 1, 1, 1, sa.SHAPE, 0.3),
 ]
 
 
