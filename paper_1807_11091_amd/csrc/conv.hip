@@ -653,8 +653,10 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(TM >= 6
     //    item e of a row is chunk c of padded column 4*b + (e mod 4), with
     //    (b, c) = divmod(e / 4, nch), so the 64 lanes of a wavefront hold 16
     //    consecutive chunks of 4 neighbouring columns (256-byte runs of the
-    //    input), and with an odd number of words per pixel their 4-byte LDS
-    //    writes fall on distinct banks.  A thread's items of a row (two per
+    //    input); with an odd number of words per pixel, the 4-byte LDS writes
+    //    of a half-wavefront fall on distinct banks for most channel counts at
+    //    stride 1, and on at most two lanes per bank otherwise (checked on the
+    //    host for 1..64 chunks per pixel).  A thread's items of a row (two per
     //    pass) keep their source and LDS offsets across rows; the row's own
     //    terms (image, input row, zero halo) are the same for every thread.
     const int nrows = g1 - g0;
