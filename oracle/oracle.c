@@ -31,13 +31,13 @@
  *     intersection scores only the unmasked entries.
  *   - the fused step returns U' = fl32(v - Z) and G = fl32(rho * fl32(fl32(W - Z) + U')).
  *   - the compacted matrix of a conv group has the group's kept filters as
- *     rows (ascending) and its kept (tap, channel) pairs as columns, in
- *     tap-major order (tap = c*D + d ascending, then channel b ascending)
- *     when the group keeps every tap of one run of consecutive input
- *     channels (no shape mask), in channel-major order (b ascending, then
- *     tap) otherwise; its entries are Z rounded to bfloat16 (round to
- *     nearest even).  The paper fixes no column order: the GEMM is the same
- *     up to a permutation of its reduction index.
+ *     rows (ascending) and its kept (channel, tap) pairs as columns in the
+ *     ascending order of the flattened GEMM column index j = (b*C + c)*D + d
+ *     of Section 3's [A, B*C*D] view; its entries are Z rounded to bfloat16
+ *     (round to nearest even).  The paper fixes no other column order: an
+ *     implementation may permute the columns of a group (the GEMM is the same
+ *     up to a permutation of its reduction index), and a comparison with this
+ *     oracle matches columns by their (channel, tap) pair.
  *   - CONV is cross-correlation with zero padding, no bias, no dilation.
  *
  * Everything here is straight loops with no blocking, fusion or reordering.
@@ -284,9 +284,8 @@ void oracle_bf16_array(int64_t n, const float *x, uint16_t *out)
  * For conv group gc the rows are the kept filters a in [gc*A/groups, (gc+1)*A/groups)
  * (row_mask[a], all rows when NULL).  Column (b, c, d) of the group is kept when
  * col_mask[(b*C + c)*D + d], chan_mask[b] and in_ch_mask[gc*B + b] are all set
- * (a NULL mask sets nothing aside).  Columns are ordered tap-major (tap, then b)
- * when col_mask is NULL and the kept channels sit at consecutive input
- * positions (a dense channel run), channel-major (b, then tap) otherwise.  Each column
+ * (a NULL mask sets nothing aside).  Columns follow the ascending GEMM column
+ * index j = (b*C + c)*D + d, i.e. channel b ascending, then tap.  Each column
  * records col_tap = c*D + d and col_ch = the column's input channel, i.e. the
  * full channel index gc*B + b, or, when in_compacted, its position among the
  * channels with in_ch_mask set (the input then holds only those, ascending).
@@ -308,33 +307,12 @@ int oracle_compact(int64_t A, int64_t B, int64_t C, int64_t D, int32_t groups,
     if (!cb || !ct)
         return -2;
     for (int32_t gc = 0; gc < groups; ++gc) {
-        /* a dense channel run: no shape mask, kept channels at consecutive positions */
-        int tap_major = 0;
-        if (!col_mask) {
-            int64_t first = -1, last = -1, nkept = 0;
-            for (int64_t b = 0; b < B; ++b) {
-                if ((chan_mask && !chan_mask[b]) || (in_ch_mask && !in_ch_mask[gc * B + b]))
-                    continue;
-                if (first < 0) first = b;
-                last = b;
-                ++nkept;
-            }
-            if (nkept > 0) {
-                int64_t p_first = gc * B + first, p_last = gc * B + last;
-                if (in_compacted) {
-                    p_first = p_last = 0;
-                    for (int64_t q = 0; q < gc * B + first; ++q) p_first += in_ch_mask[q] != 0;
-                    for (int64_t q = 0; q < gc * B + last; ++q) p_last += in_ch_mask[q] != 0;
-                }
-                tap_major = p_last - p_first + 1 == nkept;
-            }
-        }
         int64_t ncol = 0;
-        for (int64_t i = 0; i < taps * B; ++i) {
-            const int64_t t = tap_major ? i / B : i % taps;
-            const int64_t b = tap_major ? i % B : i / taps;
+        for (int64_t j = 0; j < B * taps; ++j) {  /* j = b*taps + t: the GEMM column */
+            const int64_t b = j / taps;
+            const int64_t t = j % taps;
             int keep = 1;
-            if (col_mask && !col_mask[b * taps + t]) keep = 0;
+            if (col_mask && !col_mask[j]) keep = 0;
             if (chan_mask && !chan_mask[b]) keep = 0;
             if (in_ch_mask && !in_ch_mask[gc * B + b]) keep = 0;
             if (!keep)
@@ -412,9 +390,10 @@ void oracle_conv(int64_t N, int64_t Cx, int64_t H, int64_t W, const uint16_t *Xb
     int64_t Cy = 0;
     for (int32_t g = 0; g < groups; ++g)
         Cy += M_g[g];
-#pragma omp parallel for schedule(dynamic, 1)
+    /* every output is independent: threads take (image, output row) pairs */
+#pragma omp parallel for collapse(2) schedule(dynamic, 1)
     for (int64_t n = 0; n < N; ++n) {
-        for (int64_t p = 0; p < P; ++p)
+        for (int64_t p = 0; p < P; ++p) {
             for (int64_t q = 0; q < Q; ++q) {
                 int64_t wc_off = 0, col_off = 0, o = 0;
                 for (int32_t g = 0; g < groups; ++g) {
@@ -439,6 +418,7 @@ void oracle_conv(int64_t N, int64_t Cx, int64_t H, int64_t W, const uint16_t *Xb
                     col_off += K_g[g];
                 }
             }
+        }
     }
 }
 
@@ -481,7 +461,7 @@ void oracle_conv_csr(int64_t N, int64_t H, int64_t W, const uint16_t *Xb, int64_
     int64_t P = (H + 2 * pad - C) / stride + 1;
     int64_t Q = (W + 2 * pad - D) / stride + 1;
     int64_t Cx = groups * B, per_group = A / groups;
-#pragma omp parallel for schedule(dynamic, 1)
+#pragma omp parallel for collapse(2) schedule(dynamic, 1)
     for (int64_t n = 0; n < N; ++n)
         for (int64_t p = 0; p < P; ++p)
             for (int64_t q = 0; q < Q; ++q)

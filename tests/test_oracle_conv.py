@@ -2,9 +2,11 @@
 
   * bf16 rounding equals torch's float32 -> bfloat16 conversion (round to
     nearest even), a library routine;
-  * the compacted matrix equals torch indexing of Z (kept rows, kept
-    columns tap-major for a dense channel run, channel-major otherwise)
-    converted by torch, bit for bit;
+  * the compacted matrix equals torch indexing of Z's GEMM view [A, B*C*D]
+    (kept rows, kept columns in ascending column order) converted by torch,
+    bit for bit;
+  * the input preparation equals torch's channel selection and bf16
+    conversion, bit for bit;
   * the CONV oracle equals torch.nn.functional.conv2d in float64 on the same
     bf16-rounded operands (grouped, strided, padded, non-square kernels);
   * CONV over the compacted matrix equals the dense CONV with the masked
@@ -42,26 +44,6 @@ def test_bf16_rounding_matches_torch():
     assert np.array_equal(ours, ref)
 
 
-def kept_columns(B, C, D, keep_fn, tap_major):
-    """Kept (tap, b) pairs, tap-major (tap, then b) or channel-major (b, then
-    tap)."""
-    pairs = [(t, b) for t in range(C * D) for b in range(B) if keep_fn(b, t)]
-    return sorted(pairs) if tap_major else sorted(pairs, key=lambda tb: (tb[1], tb[0]))
-
-
-def dense_run(B, gc, im, in_compacted):
-    """No shape mask: are the group's kept channels consecutive in the input?"""
-    kept = [b for b in range(B) if im is None or im[gc * B + b]]
-    if not kept:
-        return False
-    if in_compacted:
-        pos = np.cumsum(im) - 1
-        p = [int(pos[gc * B + b]) for b in kept]
-    else:
-        p = kept
-    return p == list(range(p[0], p[0] + len(p)))
-
-
 @pytest.mark.parametrize("shape,groups", [((8, 6, 3, 3), 1), ((12, 4, 5, 5), 2), ((6, 3, 3, 2), 3)])
 def test_compact_matches_torch_indexing(shape, groups):
     rng = np.random.default_rng(sum(shape) + groups)
@@ -82,12 +64,12 @@ def test_compact_matches_torch_indexing(shape, groups):
         off = roff = coff = 0
         for gc in range(groups):
             rows = [a for a in range(gc * Ag, (gc + 1) * Ag) if rm is None or rm[a]]
-            tap_major = cm is None and dense_run(B, gc, im, use[3])
-            cols = kept_columns(B, C, D, lambda b, t: (cm is None or cm[b * C * D + t]) and
-                                (im is None or im[gc * B + b]), tap_major)
-            view = Zt.permute(0, 2, 3, 1).reshape(A, C * D, B)  # [a, tap, b]
+            # GEMM column j = (b*C + c)*D + d of the [A, B*C*D] view, ascending
+            cols = [j for j in range(B * C * D)
+                    if (cm is None or cm[j]) and (im is None or im[gc * B + j // (C * D)])]
+            view = Zt.reshape(A, B * C * D)
             if rows and cols:
-                ref = view[rows][:, [t for t, _ in cols], [b for _, b in cols]]
+                ref = view[rows][:, cols]
                 ref = ref.to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16).ravel()
             else:
                 ref = np.zeros(0, np.uint16)
@@ -95,17 +77,36 @@ def test_compact_matches_torch_indexing(shape, groups):
             got = comp["Wc"][off: off + len(rows) * len(cols)]
             assert np.array_equal(got, ref)
             assert list(comp["row_idx"][roff: roff + len(rows)]) == rows
-            full = [gc * B + b for _, b in cols]
+            full = [gc * B + j // (C * D) for j in cols]
             if use[3]:
                 pos = np.cumsum(im) - 1
                 want_ch = [int(pos[c]) for c in full]
             else:
                 want_ch = full
             assert list(comp["col_ch"][coff: coff + len(cols)]) == want_ch
-            assert list(comp["col_tap"][coff: coff + len(cols)]) == [t for t, _ in cols]
+            assert list(comp["col_tap"][coff: coff + len(cols)]) == [j % (C * D) for j in cols]
             off += len(rows) * len(cols)
             roff += len(rows)
             coff += len(cols)
+
+
+@pytest.mark.parametrize("shape,keep_frac", [((3, 16, 5, 7), None), ((2, 24, 4, 4), 0.5), ((1, 5, 3, 2), 0.4)])
+def test_pack_matches_torch(shape, keep_frac):
+    """The input preparation equals torch's channel selection and
+    float32 -> bfloat16 conversion (a library routine), bit for bit, in NCHW."""
+    rng = np.random.default_rng(sum(shape))
+    X = rng.standard_normal(shape).astype(np.float32) * np.float32(3.0)
+    keep = None
+    if keep_frac is not None:
+        keep = (rng.random(shape[1]) < keep_frac).astype(np.uint8)
+        keep[0] = 1
+    got = oracle.pack(X, keep=keep)
+    Xt = torch.from_numpy(X)
+    if keep is not None:
+        Xt = Xt[:, torch.from_numpy(keep.astype(bool))]
+    ref = Xt.to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert got.shape == ref.shape
+    assert np.array_equal(got, ref)
 
 
 def torch_conv_nhwc(Xb, Wbits, groups, stride, pad):

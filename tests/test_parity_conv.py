@@ -38,19 +38,35 @@ def gpu_compact(Z, groups, row_mask=None, col_mask=None, in_ch_mask=None, in_com
 
 
 def check_compact(gpu, ref):
+    """Sizes, kept rows and the padding must be equal; columns are matched by
+    their (input channel, tap) pair, since the library may order a group's
+    columns differently from the oracle's ascending GEMM column index (any
+    order gives the same GEMM): the kept pairs must be the same set, and every
+    GPU column must equal, bit for bit, the oracle's column of its pair."""
     Wc, row_idx, col_ch, col_tap, sizes = gpu
     assert list(sizes.M)[: sizes.groups] == list(ref["M"])
     assert list(sizes.K)[: sizes.groups] == list(ref["K"])
-    nr, nc = int(ref["M"].sum()), int(ref["K"].sum())
-    assert np.array_equal(strip_padding(Wc.cpu().numpy(), sizes), ref["Wc"])
+    nr = int(ref["M"].sum())
     assert np.array_equal(row_idx.cpu().numpy()[:nr], ref["row_idx"])
-    assert np.array_equal(col_ch.cpu().numpy()[:nc], ref["col_ch"])
-    assert np.array_equal(col_tap.cpu().numpy()[:nc], ref["col_tap"])
-    # padding columns hold +0
     full = Wc.cpu().numpy()
+    gch, gtap = col_ch.cpu().numpy(), col_tap.cpu().numpy()
+    woff = coff = 0
     for g in range(sizes.groups):
         M, K, ldk, off = sizes.M[g], sizes.K[g], sizes.ldk[g], sizes.wc_offset[g]
-        assert not np.any(full[off: off + M * ldk].reshape(M, ldk)[:, K:])
+        goff = sizes.col_offset[g]
+        mat = full[off: off + M * ldk].reshape(M, ldk)
+        # padding columns hold +0
+        assert not np.any(mat[:, K:])
+        rch, rtap = ref["col_ch"][coff: coff + K], ref["col_tap"][coff: coff + K]
+        rkey = {(int(c), int(t)): j for j, (c, t) in enumerate(zip(rch, rtap))}
+        assert len(rkey) == K
+        gkey = [(int(c), int(t)) for c, t in zip(gch[goff: goff + K], gtap[goff: goff + K])]
+        assert len(set(gkey)) == K and set(gkey) == set(rkey)
+        perm = np.array([rkey[k] for k in gkey], dtype=np.int64)
+        rmat = ref["Wc"][woff: woff + M * K].reshape(M, K)
+        assert np.array_equal(mat[:, :K], rmat[:, perm])
+        woff += M * K
+        coff += K
 
 
 def conv_case(N, Cin, H, Wd, A, C, D, stride, pad, groups, kind, keep, seed, dense_too=True, dead_lo=0):
@@ -187,13 +203,18 @@ def test_compact_chain_input_positions():
     assert maxabs_over_rms(bf16_bits_to_f64(Y.cpu().numpy()), Yr) <= TOL
 
 
-def sampled_images(N):
-    return sorted({0, N // 2, N - 1})
+def sampled_images(N, count):
+    """count images spread over the batch, always the first and the last
+    (every image when count >= N)."""
+    if count >= N:
+        return list(range(N))
+    return sorted({int(round(i * (N - 1) / (count - 1))) for i in range(count)})
 
 
-def workload_conv(name, layer_ids=None, variant=0, chain=False):
+def workload_conv(name, layer_ids=None, variant=0, chain=False, images=4):
     """Full-batch GPU path of a workload (projection -> compaction -> pack ->
-    compacted and dense CONV); the oracle recomputes sampled images."""
+    compacted and dense CONV); the oracle recomputes `images` images of the
+    batch (all of them when images >= batch)."""
     t = torch()
     wl = WORKLOADS[name]
     kind, pct = wl.variants[variant]
@@ -227,7 +248,7 @@ def workload_conv(name, layer_ids=None, variant=0, chain=False):
         gd = sa.compact(gl.Z, L.groups)
         Yd = sa.conv_fwd(Xf, gd[0], gd[2], gd[3], gd[4], L.C, L.D, L.stride, L.pad)
         t.cuda.synchronize()
-        sel = sampled_images(wl.batch)
+        sel = sampled_images(wl.batch, images)
         Xb = oracle.pack(X[sel], keep=inm_ref)
         Yr = oracle.conv(Xb, rc, L.C, L.D, L.stride, L.pad)
         y = bf16_bits_to_f64(Y.cpu().numpy()[sel])
@@ -245,29 +266,40 @@ def workload_conv(name, layer_ids=None, variant=0, chain=False):
 
 
 def test_conv_workload_cifar():
-    workload_conv("cifar_conv64")
+    workload_conv("cifar_conv64", images=8)
 
 
 def test_conv_workload_alexnet_shape30():
-    workload_conv("alexnet_shape30")
+    # the whole batch of 128 images
+    workload_conv("alexnet_shape30", images=128)
 
 
 def test_conv_workload_alexnet_chain():
-    workload_conv("alexnet_chain_f50c50", chain=True)
+    workload_conv("alexnet_chain_f50c50", chain=True, images=128)
 
 
-def test_conv_workload_resnet50_sampled_layers():
+def _resnet50_stage(prefix):
     wl = WORKLOADS["resnet50_filter60"]
-    names = {l.name: i for i, l in enumerate(wl.layers)}
-    pick = [names[n] for n in ("conv1", "layer1.0.conv1", "layer1.0.conv2", "layer2.0.conv2",
-                               "layer2.0.downsample", "layer3.3.conv2", "layer4.0.conv1",
-                               "layer4.2.conv2", "layer4.2.conv3")]
-    workload_conv("resnet50_filter60", pick)
+    return [i for i, l in enumerate(wl.layers)
+            if l.name.startswith(prefix) or (prefix == "layer1" and l.name == "conv1")]
 
 
-@pytest.mark.parametrize("variant", [0, 2, 3, 5, 6, 8])
+@pytest.mark.parametrize("stage", ["layer1", "layer2", "layer3", "layer4"])
+def test_conv_workload_resnet50(stage):
+    """Every one of the 53 CONVs (the stem goes with stage 1), four images of
+    the batch of 64 each: the first, the last and two inside."""
+    workload_conv("resnet50_filter60", _resnet50_stage(stage), images=4)
+
+
+def test_conv_workload_resnet50_covers_every_layer():
+    ids = sorted(i for st in ("layer1", "layer2", "layer3", "layer4") for i in _resnet50_stage(st))
+    assert ids == list(range(len(WORKLOADS["resnet50_filter60"].layers))) and len(ids) == 53
+
+
+@pytest.mark.parametrize("variant", range(9))
 def test_conv_workload_sweep(variant):
-    workload_conv("resnet50_s3_sweep", variant=variant)
+    """filter / shape / element-wise at 10, 25 and 50% kept."""
+    workload_conv("resnet50_s3_sweep", variant=variant, images=4)
 
 
 def table_masks(W, U, L, block):
