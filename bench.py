@@ -1,25 +1,29 @@
 #!/usr/bin/env python3
 """Benchmark of the StructADMM hot path on one MI355X.
 
-Workload: AlexNet conv1-5 at batch 128, filter-shape-wise pruning keeping 30%
-of the (c, kh, kw) columns of every layer (synthetic weights and inputs of
-the paper's AlexNet shapes; no dataset, no trained weights).
+Workload: the 53 convolutions of ResNet-50 v1.5 at 224x224, batch 64,
+filter-wise pruning keeping 60% of the filters of every layer (synthetic
+weights and inputs of the paper's ResNet-50 shapes; no dataset, no trained
+weights).  The AlexNet conv1-5 workload (batch 128, filter-shape-wise 30%)
+is measured in the same run with fewer steps and reported under its own key.
 
 One step = one pass of the whole path over one batch:
-  1. structadmm_project     fused Z-update + dual update + regulariser gradient, 5 layers in one call
-  2. structadmm_dual_update per-SGD-step gradient rho (W - Z + U) of the 5 layers
+  1. structadmm_project     fused Z-update + dual update + regulariser gradient, all layers in one call
+  2. structadmm_dual_update per-SGD-step gradient rho (W - Z + U) of all layers
   3. per layer: structadmm_compact (pruned and dense matrices), then structadmm_pack_nhwc of
      every layer's input
   4. structadmm_conv_fwd of every layer over its compacted matrix, then over the dense one
 Inputs are resident in HBM before the timed region.
 
-Output: one JSON line.  value = compacted-CONV TFLOP/s over the step's five
+Output: one JSON line.  value = compacted-CONV TFLOP/s over the step's
 compacted convolutions (algorithmic flops 2*N*P*Q*sum_g M_g*K_g / their
 HIP-event time); speedup_vs_dense = dense CONV time / compacted CONV time;
 admm_gbps = algorithmic bytes of steps 1-2 / their time.  Each CONV is bracketed
-by HIP events on the stream it runs on; the CONVs are enqueued back to back
-(the compactions, which return sizes to the host, come first), so the events
-measure the kernels rather than host gaps.
+by HIP events on the stream it runs on; a spin kernel ahead of each timed
+block lets the host enqueue the block before the GPU reaches it, so the events
+measure the kernels rather than host gaps.  ms_per_step is the wall time of a
+step: the GPU time of its parts, the host-side synchronisations of the
+compactions, and the spins (reported separately as spin_ms_per_step).
 """
 from __future__ import annotations
 
@@ -36,12 +40,14 @@ sys.path.insert(0, ROOT)
 
 METRIC = "compacted-conv TFLOP/s & speedup vs dense; ADMM projection+update HBM GB/s"
 FILTER_KIND, SHAPE_KIND = 0, 2  # sparsity-set kinds (the C ABI's enum)
-WORKLOAD = "alexnet_shape30"
+WORKLOAD = "resnet50_filter60"
+SECOND_WORKLOAD = "alexnet_shape30"
 HBM_PEAK_GBS = 8000.0
 BF16_PEAK_TFLOPS = 2500.0
-# spins ahead of the ADMM block and of the CONV block of a step (its wall time includes both);
-# the host takes ~40 us to enqueue one CONV with its two events
-LEAD_US, LEAD_CONV_US = 300, 1000
+# spin ahead of the ADMM block of a step; the spin ahead of the pack + CONV
+# block is sized from the host's measured enqueue time of that block
+LEAD_US = 300
+LEAD_CONV_MAX_US = 40000
 
 
 def parse():
@@ -140,6 +146,7 @@ def run_step(torch, sa, wl, layers, ws, cws, ev, record):
                                dtype=torch.uint16, device="cuda")
             o.flops_c = 2 * wl.batch * L.P * L.Q * sum(sizes.M[g] * sizes.K[g] for g in range(sizes.groups))
             o.flops_d = 2 * wl.batch * L.P * L.Q * sum(sized.M[g] * sized.K[g] for g in range(sized.groups))
+            o.sizes_c = sizes
         # scratch for groups whose im2col rows are gathered first; the kept
         # columns move between ADMM steps, so it is sized for every step (outside
         # the CONV events) and grown when a step needs more
@@ -152,8 +159,11 @@ def run_step(torch, sa, wl, layers, ws, cws, ev, record):
     # them while the host enqueues the first CONV
     if ev.get("lead_conv"):
         torch.cuda._sleep(ev["lead_conv"])
+    t_enq = time.perf_counter()
+    mark("pack0")
     for o in layers:
         sa.pack_nhwc(o.X, out=o.Xp)
+    mark("pack1")
     for i, (o, (c, d)) in enumerate(zip(layers, comp)):
         L = o.cfg
         mark(f"c{i}a")
@@ -164,6 +174,7 @@ def run_step(torch, sa, wl, layers, ws, cws, ev, record):
         mark(f"d{i}a")
         sa.conv_fwd(o.Xp, d[0], d[2], d[3], d[4], L.C, L.D, L.stride, L.pad, Y=o.Yd, ws=o.cvws)
         mark(f"d{i}b")
+    ev["enqueue_s"] = time.perf_counter() - t_enq
     return marks
 
 
@@ -180,8 +191,9 @@ def lead_cycles(torch, us):
 
 def cpu_baseline(wl, seconds):
     """The oracle on the host cores over a bounded sample of the same workload:
-    the fused ADMM step of all five layers and the compacted CONV of as many
-    images as fit the time budget (binary64 loops, OpenMP over images)."""
+    the fused ADMM step of every layer (one thread) and the compacted CONV of
+    as many images as fit the time budget (binary64 loops, OpenMP over
+    (image, output row) pairs)."""
     import oracle
     from workloads import input_nchw, layer_tensors
     kind, pct = wl.variants[0]
@@ -193,9 +205,10 @@ def cpu_baseline(wl, seconds):
         t0 = time.perf_counter()
         r = oracle.project(W, U, kind, k, L.groups, rho=wl.rho, fused=True)
         t_admm += time.perf_counter() - t0
-        rc = oracle.compact(r["Z"], L.groups, col_mask=r["mask"])
+        rc = oracle.compact(r["Z"], L.groups, row_mask=r["mask"] if kind == FILTER_KIND else None,
+                            col_mask=r["mask"] if kind == SHAPE_KIND else None)
         prep.append((L, rc))
-    # one image first, then as many as fit the budget
+
     def conv_images(nimg):
         flops, t = 0, 0.0
         for li, (L, rc) in enumerate(prep):
@@ -207,17 +220,19 @@ def cpu_baseline(wl, seconds):
             flops += 2 * nimg * L.P * L.Q * int(np.sum(rc["M"].astype(np.int64) * rc["K"]))
         return flops, t
     threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
-    # calibrate on one image per thread (the oracle runs images in parallel)
-    n0 = min(wl.batch, threads)
-    f, t = conv_images(n0)
-    nimg = int(min(wl.batch, max(n0, (seconds / max(t, 1e-6)) * n0 // threads * threads)))
-    if nimg > n0:
+    # calibrate on one image (the oracle threads over its output rows), then
+    # as many images as fit the budget
+    f, t = conv_images(1)
+    nimg = int(min(wl.batch, max(1, seconds / max(t, 1e-6))))
+    if nimg > 1:
         f, t = conv_images(nimg)
+    n = sum(L.n for L in wl.layers)
     return {"value": f / t / 1e12, "unit": "TFLOP/s", "cores": min(threads, os.cpu_count() or threads),
             "kind": "oracle",
-            "sample": f"compacted CONV of conv1-5 on {nimg} of {wl.batch} images "
-                      f"({f / 1e9:.1f} GFLOP in {t:.1f} s); fused ADMM step of all 5 layers took "
-                      f"{t_admm * 1e3:.0f} ms on one core"}
+            "sample": f"compacted CONV of all {len(wl.layers)} layers on {nimg} of {wl.batch} images "
+                      f"({f / 1e9:.1f} GFLOP in {t:.1f} s); fused ADMM step of all {len(wl.layers)} layers "
+                      f"({n} weights) took {t_admm * 1e3:.0f} ms on one core",
+            "admm_fused_GBps_1_core": round(20 * n / t_admm / 1e9, 3)}
 
 
 def copy_probe(mib):
@@ -233,12 +248,12 @@ def copy_probe(mib):
     print(json.dumps({"copy_probe_bytes": n, "copies": 5}))
 
 
-def traffic_per_launch():
-    """HBM bytes per k_conv_patch launch from the committed counter summary,
-    if it was taken on the current CONV source (else None)."""
+def traffic_per_launch(kernel, workload, source="conv.hip"):
+    """HBM bytes per launch of `kernel` on `workload` from the committed
+    counter summary, if it was taken on the current source (else None)."""
     import hashlib
-    summ = os.path.join(ROOT, "profiles", "k_conv_patch_alexnet_shape30_traffic.md")
-    src = os.path.join(ROOT, "paper_1807_11091_amd", "csrc", "conv.hip")
+    summ = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_traffic.md")
+    src = os.path.join(ROOT, "paper_1807_11091_amd", "csrc", source)
     if not os.path.exists(summ):
         return None
     fields = {}
@@ -247,7 +262,7 @@ def traffic_per_launch():
             k, v = line[2:].split(":", 1)
             fields[k.strip()] = v.strip().strip("`")
     digest = hashlib.sha256(open(src, "rb").read()).hexdigest()
-    if fields.get("conv.hip sha256") != digest or "bytes per launch" not in fields:
+    if fields.get(f"{source} sha256") != digest or "bytes per launch" not in fields:
         return None
     return int(fields["bytes per launch"])
 
@@ -768,7 +783,8 @@ def main():
         suite(args.suite)
         return
     if args.gpus != 1:
-        print(json.dumps({"error": "this build measures one GPU only; run with --gpus 1"}))
+        print(json.dumps({"error": "this build measures one GPU only (one MI355X); "
+                                   "multi-GPU runs are not part of it: run with --gpus 1"}))
         sys.exit(2)
     import torch
     import paper_1807_11091_amd as sa
@@ -777,22 +793,89 @@ def main():
     if not torch.cuda.is_available():
         raise SystemExit("bench.py needs a GPU")
     sa.lib()  # fails loudly if the HIP library is missing
+    main_res = measure(torch, sa, WORKLOADS[WORKLOAD], args.steps, args.warmup)
+    second = measure(torch, sa, WORKLOADS[SECOND_WORKLOAD], max(3, args.steps // 4), max(1, args.warmup))
+    warm = admm_warm(torch, sa, WORKLOADS[WORKLOAD])
     wl = WORKLOADS[WORKLOAD]
+    out = {
+        "metric": METRIC,
+        "value": main_res["compact_tflops"],
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": main_res["ms_per_step"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": WORKLOAD, "layers": "ResNet-50 v1.5, all 53 convolutions, 224x224",
+                   "batch": wl.batch, "sparsity": "filter-wise, keep 60% of the filters of every layer",
+                   "parallelism": "single GPU"},
+        "speedup_vs_dense": main_res["speedup_vs_dense"],
+        "dense_conv_tflops": main_res["dense_tflops"],
+        "compact_conv_us": main_res["compact_us"],
+        "dense_conv_us": main_res["dense_us"],
+        "admm_gbps": main_res["admm_gbps"],
+        "admm_us": main_res["admm_us"],
+        "admm_note": "fused projection (20 B/weight) + per-SGD-step gradient (16 B/weight) of all layers, "
+                     "one call each, timed inside the step after the previous step's CONVs streamed GBs "
+                     "through the caches (cold); admm_warm_* = the same two calls back to back",
+        "admm_warm_gbps": warm["step_gbps"],
+        "admm_warm_us": warm["step_us"],
+        "spin_ms_per_step": main_res["spin_ms_per_step"],
+        "gpu_ms_per_step": main_res["gpu_ms_per_step"],
+        "per_layer": main_res["per_layer"],
+        "roofline": main_res["roofline"],
+        SECOND_WORKLOAD: {k: second[k] for k in ("compact_tflops", "dense_tflops", "speedup_vs_dense",
+                                                 "compact_us", "dense_us", "admm_gbps", "admm_us",
+                                                 "ms_per_step", "roofline")},
+    }
+    if not args.no_cpu_baseline:
+        progress("oracle on the host cores")
+        out["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
+    print(json.dumps(out))
+
+
+# bytes one launch of the direct / footprint CONV must move at least: the input
+# channels it references, the compacted weights and the output (bf16)
+def layer_bytes(o):
+    L = o.cfg
+    N, H, W, Cx = o.Xp.shape
+    m = sum(o.sizes_c.M[g] for g in range(o.sizes_c.groups))
+    kk = sum(o.sizes_c.M[g] * o.sizes_c.K[g] for g in range(o.sizes_c.groups))
+    return 2 * N * H * W * Cx + 2 * kk + 2 * N * L.P * L.Q * m
+
+
+def progress(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def measure(torch, sa, wl, steps, warmup):
+    """Timed steps of one workload; returns the figures of its bench line."""
+    progress(f"{wl.name}: generating inputs")
     layers = setup(torch, sa, wl)
+    progress(f"{wl.name}: {len(layers)} layers resident, warm-up")
     ws = torch.empty(max(256, sa.project_workspace([o.proj for o in layers])), dtype=torch.uint8, device="cuda")
     cws = torch.empty(sa.COMPACT_WS_BYTES, dtype=torch.uint8, device="cuda")
     ev = {"pdescs": sa._descs([o.proj for o in layers]),
           "ddescs": sa.dual_descs([(o.W, o.Z, o.U, wl.rho, o.G2, False) for o in layers]),
-          "lead": lead_cycles(torch, LEAD_US), "lead_conv": lead_cycles(torch, LEAD_CONV_US)}
-
-    # at least one untimed step: it sizes the output and scratch buffers
-    for _ in range(max(1, args.warmup)):
-        run_step(torch, sa, wl, layers, ws, cws, ev, record=False)
+          "lead": lead_cycles(torch, LEAD_US), "lead_conv": 0}
+    # untimed steps: size the output and scratch buffers, then the spin ahead
+    # of the pack + CONV block from the host's enqueue time of that block
+    for _ in range(max(1, warmup)):
+        run_step(torch, sa, wl, layers, ws, cws, ev, record=True)
+        torch.cuda.synchronize()
+        lead_us = min(LEAD_CONV_MAX_US, 1.3 * ev["enqueue_s"] * 1e6 + 200)
+        ev["lead_conv"] = lead_cycles(torch, lead_us)
+    spin_ms = (LEAD_US + lead_us) * 1e-3
     torch.cuda.synchronize()
+    progress(f"{wl.name}: timing {steps} steps")
 
     t0 = time.perf_counter()
     all_marks = []
-    for _ in range(args.steps):
+    for _ in range(steps):
         all_marks.append(run_step(torch, sa, wl, layers, ws, cws, ev, record=True))
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
@@ -800,53 +883,70 @@ def main():
     def span(m, a, b):
         return sum(x.elapsed_time(y) for x, y in zip(m[a], m[b]))  # ms
 
-    t_admm = sum(span(m, "admm0", "admm1") for m in all_marks) / args.steps
-    t_c = [sum(span(m, f"c{i}a", f"c{i}b") for m in all_marks) / args.steps for i in range(len(layers))]
-    t_d = [sum(span(m, f"d{i}a", f"d{i}b") for m in all_marks) / args.steps for i in range(len(layers))]
+    t_admm = sum(span(m, "admm0", "admm1") for m in all_marks) / steps
+    t_pack = sum(span(m, "pack0", "pack1") for m in all_marks) / steps
+    t_c = [sum(span(m, f"c{i}a", f"c{i}b") for m in all_marks) / steps for i in range(len(layers))]
+    t_d = [sum(span(m, f"d{i}a", f"d{i}b") for m in all_marks) / steps for i in range(len(layers))]
     flops_c = sum(o.flops_c for o in layers)
     flops_d = sum(o.flops_d for o in layers)
     n_el = sum(o.cfg.n for o in layers)
     admm_bytes = 20 * n_el + 16 * n_el  # fused step (W,U read; Z,U,G written) + gradient (W,Z,U read; G written)
-    tflops_c = flops_c / (sum(t_c) * 1e-3) / 1e12
-    tflops_d = flops_d / (sum(t_d) * 1e-3) / 1e12
-    # dominant kernel of the compacted path: k_conv_patch, one launch per
-    # shape-pruned layer whose input channels are 8-aligned (CONV2-5)
-    patch = [i for i, o in enumerate(layers) if o.Xp.shape[3] % 8 == 0]
-    patch_ms = sum(t_c[i] for i in patch)
-    patch_tflops = sum(layers[i].flops_c for i in patch) / (patch_ms * 1e-3) / 1e12
-    out = {
-        "metric": METRIC,
-        "value": round(tflops_c, 3),
-        "unit": "TFLOP/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": round(wall * 1e3 / args.steps, 4),
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "bf16",
-        "data": "synthetic",
-        "config": {"workload": WORKLOAD, "layers": "AlexNet conv1-5", "batch": wl.batch,
-                   "sparsity": "filter-shape-wise, keep 30% of columns", "parallelism": "single GPU"},
+    # the dominant kernel of the compacted path: the kernel that runs the
+    # layers whose input channels are 8-aligned (all but a few-channel stem)
+    kern = {sa.FILTER: "k_conv", sa.SHAPE: "k_conv_patch"}[layers[0].kind]
+    dom = [i for i, o in enumerate(layers) if o.Xp.shape[3] % 8 == 0]
+    dom_ms = sum(t_c[i] for i in dom)
+    dom_flops = sum(layers[i].flops_c for i in dom)
+    dom_tflops = dom_flops / (dom_ms * 1e-3) / 1e12
+    # per-layer roofline min(MFMA, AI * HBM) time over the measured time
+    roof_ms = sum(max(layers[i].flops_c / (BF16_PEAK_TFLOPS * 1e12), layer_bytes(layers[i]) / (HBM_PEAK_GBS * 1e9))
+                  for i in dom) * 1e3
+    per_layer = [{"layer": o.cfg.name, "compact_us": round(tc * 1e3, 1), "dense_us": round(td * 1e3, 1),
+                  "compact_tflops": round(o.flops_c / (tc * 1e-3) / 1e12, 1),
+                  "dense_tflops": round(o.flops_d / (td * 1e-3) / 1e12, 1),
+                  "speedup": round(td / tc, 2)}
+                 for o, tc, td in zip(layers, t_c, t_d)]
+    res = {
+        "compact_tflops": round(flops_c / (sum(t_c) * 1e-3) / 1e12, 3),
+        "dense_tflops": round(flops_d / (sum(t_d) * 1e-3) / 1e12, 3),
         "speedup_vs_dense": round(sum(t_d) / sum(t_c), 3),
-        "dense_conv_tflops": round(tflops_d, 3),
+        "compact_us": round(sum(t_c) * 1e3, 1),
+        "dense_us": round(sum(t_d) * 1e3, 1),
         "admm_gbps": round(admm_bytes / (t_admm * 1e-3) / 1e9, 1),
         "admm_us": round(t_admm * 1e3, 2),
-        "per_layer": [{"layer": o.cfg.name, "compact_us": round(tc * 1e3, 1), "dense_us": round(td * 1e3, 1),
-                       "compact_tflops": round(o.flops_c / (tc * 1e-3) / 1e12, 1),
-                       "dense_tflops": round(o.flops_d / (td * 1e-3) / 1e12, 1),
-                       "speedup": round(td / tc, 2)}
-                      for o, tc, td in zip(layers, t_c, t_d)],
-        "roofline": {"kernel": "k_conv_patch (compacted " + "/".join(layers[i].cfg.name for i in patch) + ")",
-                     "bound": "mfma", "achieved": round(patch_tflops, 2), "peak": BF16_PEAK_TFLOPS,
-                     "unit": "TFLOP/s", "frac": round(patch_tflops / BF16_PEAK_TFLOPS, 4),
-                     "avg_launch_us": round(patch_ms * 1e3 / len(patch), 2), "launches_per_step": len(patch),
-                     "traffic": traffic_per_launch()},
+        "pack_us": round(t_pack * 1e3, 1),
+        "ms_per_step": round(wall * 1e3 / steps, 4),
+        "spin_ms_per_step": round(spin_ms, 3),
+        "gpu_ms_per_step": round(t_admm + t_pack + sum(t_c) + sum(t_d), 4),
+        "per_layer": per_layer,
+        "roofline": {"kernel": f"{kern} (compacted CONVs of {len(dom)} of {len(layers)} layers)",
+                     "bound": "mfma", "achieved": round(dom_tflops, 2), "peak": BF16_PEAK_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(dom_tflops / BF16_PEAK_TFLOPS, 4),
+                     "avg_launch_us": round(dom_ms * 1e3 / len(dom), 2), "launches_per_step": len(dom),
+                     "flops_per_launch": round(dom_flops / len(dom)),
+                     "frac_of_layer_roofline": round(roof_ms / dom_ms, 4),
+                     "traffic": traffic_per_launch(kern, wl.name)},
     }
-    if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
-    print(json.dumps(out))
+    del layers
+    torch.cuda.empty_cache()
+    return res
+
+
+def admm_warm(torch, sa, wl):
+    """The two ADMM calls of a step back to back (warm caches)."""
+    layers, grads = _admm_layers(torch, sa, wl, 0, 1)
+    ws = torch.empty(max(256, sa.project_workspace(layers)), dtype=torch.uint8, device="cuda")
+    pd, dd = sa._descs(layers), sa.dual_descs(grads)
+
+    def step():
+        sa.project(layers, ws, descs=pd)
+        sa.dual_update(None, descs=dd)
+    t = _time(torch, step, reps=10)
+    n = sum(L.n for L in wl.layers)
+    res = {"step_us": round(t["median_ms"] * 1e3, 2), "step_gbps": round(36 * n / t["median_ms"] / 1e6, 1)}
+    del layers, grads, ws
+    torch.cuda.empty_cache()
+    return res
 
 
 if __name__ == "__main__":

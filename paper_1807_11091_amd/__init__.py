@@ -161,6 +161,19 @@ def _stream(stream) -> Optional[int]:
     return stream if isinstance(stream, int) else stream.cuda_stream
 
 
+def _keep_for_stream(stream, *tensors):
+    """Temporaries this module allocates come from torch's caching allocator on
+    the current stream; when the launch goes to another torch stream, mark them
+    in use there, so their memory is not handed out again before that stream's
+    work has finished (a raw stream handle gets no such tracking: the caller
+    must keep such calls on the current stream or pass its own buffers)."""
+    if stream is None or isinstance(stream, int):
+        return
+    for t in tensors:
+        if t is not None:
+            t.record_stream(stream)
+
+
 @dataclass
 class ProjectLayer:
     """One layer of a projection call: tensors are torch device tensors."""
@@ -254,6 +267,7 @@ def compact(Z, groups: int = 1, row_mask=None, col_mask=None, chan_mask=None, in
                        _ptr(col_tap), _ptr(ws))
     sizes = CompactSizes()
     _check(lib().structadmm_compact(ctypes.byref(desc), ctypes.byref(sizes), _stream(stream)), "structadmm_compact")
+    _keep_for_stream(stream, ws, *(() if out is not None else (Wc, row_idx, col_ch, col_tap)))
     return Wc, row_idx, col_ch, col_tap, sizes
 
 
@@ -266,6 +280,8 @@ def pack_nhwc(X, keep=None, Cx: Optional[int] = None, out=None, stream=None):
     Xp = out if out is not None else torch.empty((N, H, W, Cx), dtype=torch.uint16, device=X.device)
     _check(lib().structadmm_pack_nhwc(_ptr(X), N, Cin, H, W, _ptr(keep), Cx, _ptr(Xp), _stream(stream)),
            "structadmm_pack_nhwc")
+    if out is None:
+        _keep_for_stream(stream, Xp)
     return Xp
 
 
@@ -294,16 +310,20 @@ def conv_fwd(Xp, Wc, col_ch, col_tap, sizes: CompactSizes, C: int, D: int, strid
     """structadmm_conv_fwd; Xp bf16 NHWC (uint16), returns Y bf16 NHWC (uint16).
     ``ws``: uint8 device scratch of conv_workspace() bytes (allocated here when None)."""
     import torch
+    temps = []
     if desc is None:
         N, H, W, Cx = Xp.shape
         if Y is None:
             Y = torch.empty(conv_out_shape(N, H, W, C, D, stride, pad, sizes), dtype=torch.uint16,
                             device=Xp.device)
+            temps.append(Y)
         if ws is None:
             need = conv_workspace(Xp, sizes, C, D, stride, pad)
             ws = torch.empty(need, dtype=torch.uint8, device=Xp.device) if need else None
+            temps.append(ws)
         desc = conv_desc(Xp, Wc, col_ch, col_tap, sizes, C, D, stride, pad, Y, ws)
     _check(lib().structadmm_conv_fwd(ctypes.byref(desc), _stream(stream)), "structadmm_conv_fwd")
+    _keep_for_stream(stream, *temps)
     return Y
 
 
@@ -324,6 +344,7 @@ def csr(Z, kept_idx, nnz: Optional[int] = None, row_ptr=None, col=None, val=None
     d = CsrDesc(A, B, C, D, nnz, _ptr(Z), _ptr(kept_idx) if nnz else None, _ptr(row_ptr),
                 _ptr(col) if nnz else None, _ptr(val) if nnz else None)
     _check(lib().structadmm_csr(ctypes.byref(d), _stream(stream)), "structadmm_csr")
+    _keep_for_stream(stream, row_ptr, col, val)
     return row_ptr, col, val
 
 
@@ -349,6 +370,7 @@ def conv_sparse_fwd(Xp, row_ptr, col, val, shape, groups: int, stride: int, pad:
     [N, P, Q, A] (uint16).  reuse_ws: ws holds the padded entries an earlier
     call with the same CSR and geometry built."""
     import torch
+    temps = []
     if desc is None:
         N, H, W, Cx = Xp.shape
         A, B, C, D = shape
@@ -356,11 +378,14 @@ def conv_sparse_fwd(Xp, row_ptr, col, val, shape, groups: int, stride: int, pad:
             P = (H + 2 * pad - C) // stride + 1
             Q = (W + 2 * pad - D) // stride + 1
             Y = torch.empty((N, P, Q, A), dtype=torch.uint16, device=Xp.device)
+            temps.append(Y)
         if ws is None:
             need = conv_sparse_workspace(Xp, shape, groups, stride, pad, nnz)
             ws = torch.empty(max(need, 256), dtype=torch.uint8, device=Xp.device)
+            temps.append(ws)
         desc = sparse_conv_desc(Xp, row_ptr, col, val, shape, groups, stride, pad, nnz, Y, ws, reuse_ws)
     _check(lib().structadmm_conv_sparse_fwd(ctypes.byref(desc), _stream(stream)), "structadmm_conv_sparse_fwd")
+    _keep_for_stream(stream, *temps)
     return Y
 
 

@@ -367,3 +367,26 @@ def test_conv_is_deterministic():
     Y2 = sa.conv_fwd(Xp, Wc, cc, ct, sizes, 3, 3, 1, 1)
     t.cuda.synchronize()
     assert t.equal(Y1, Y2)
+
+
+def test_conv_on_a_non_current_stream():
+    """Compaction, pack and CONV enqueued on a torch stream other than the
+    current one, with the binding allocating the outputs and scratch: results
+    equal those of the current stream, bit for bit."""
+    t = torch()
+    rng = np.random.default_rng(12)
+    X = to_dev(rng.standard_normal((3, 3, 30, 28)).astype(np.float32))  # stem-like: space-to-depth scratch
+    Z = to_dev((0.05 * rng.standard_normal((40, 3, 7, 7))).astype(np.float32))
+    ref_c = sa.compact(Z, 1)
+    ref = sa.conv_fwd(sa.pack_nhwc(X), ref_c[0], ref_c[2], ref_c[3], ref_c[4], 7, 7, 2, 3)
+    t.cuda.synchronize()
+    s = t.cuda.Stream()
+    s.wait_stream(t.cuda.current_stream())
+    got_c = sa.compact(Z, 1, stream=s)
+    Xp = sa.pack_nhwc(X, stream=s)
+    Y = sa.conv_fwd(Xp, got_c[0], got_c[2], got_c[3], got_c[4], 7, 7, 2, 3, stream=s)
+    # unrelated work on the current stream may reuse freed blocks meanwhile
+    junk = [t.full((1 << 20,), 7, dtype=t.uint8, device=DEV) for _ in range(4)]
+    s.synchronize()
+    assert t.equal(Y, ref)
+    del junk
