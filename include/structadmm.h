@@ -123,6 +123,21 @@ size_t structadmm_project_workspace(const sa_project_desc *layers, int n_layers)
 int structadmm_project(const sa_project_desc *layers, int n_layers, void *ws, size_t ws_bytes,
                        hipStream_t stream);
 
+/* Largest scratch structadmm_project_noalloc can use (bytes). */
+#define SA_PROJECT_NOALLOC_BYTES (16u << 20)
+
+/* structadmm_project without a caller workspace and without any device
+ * allocation: for callers that cannot allocate (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc).  Same layers, same
+ * results as structadmm_project; its scratch is a fixed array of
+ * SA_PROJECT_NOALLOC_BYTES held by the library on each GPU it runs on (the
+ * GPU current at the call) until the process ends.  Returns SA_E_WORKSPACE,
+ * before anything is enqueued, when the layers need more scratch than that
+ * (structadmm_project_workspace() > SA_PROJECT_NOALLOC_BYTES).  Every call on
+ * one GPU shares that GPU's array: calls that may overlap on one GPU (other
+ * streams, other threads) race and must be ordered by the caller. */
+int structadmm_project_noalloc(const sa_project_desc *layers, int n_layers, hipStream_t stream);
+
 /* ---- dual update / gradient: structadmm_dual_update ------------------ */
 /*
  * U <- fl32(fl32(U + W) - Z) (Section 4, below eq. (3)) when update_dual != 0,

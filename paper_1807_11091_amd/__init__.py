@@ -117,6 +117,8 @@ def lib():
         L.structadmm_project_workspace.restype = ctypes.c_size_t
         L.structadmm_project.argtypes = [ctypes.POINTER(ProjectDesc), ctypes.c_int, _vp, ctypes.c_size_t, _vp]
         L.structadmm_project.restype = ctypes.c_int
+        L.structadmm_project_noalloc.argtypes = [ctypes.POINTER(ProjectDesc), ctypes.c_int, _vp]
+        L.structadmm_project_noalloc.restype = ctypes.c_int
         L.structadmm_dual_update.argtypes = [ctypes.POINTER(DualDesc), ctypes.c_int, _vp]
         L.structadmm_dual_update.restype = ctypes.c_int
         L.structadmm_sgd_step.argtypes = [ctypes.POINTER(SgdDesc), ctypes.c_int, _vp]
@@ -213,6 +215,17 @@ def project(layers: Sequence[ProjectLayer], ws=None, stream=None, descs=None):
     d = descs if descs is not None else _descs(layers)
     nbytes = 0 if ws is None else ws.numel() * ws.element_size()
     _check(lib().structadmm_project(d, len(layers), _ptr(ws), nbytes, _stream(stream)), "structadmm_project")
+
+
+# scratch the library holds per GPU for project_noalloc (bytes)
+PROJECT_NOALLOC_BYTES = 16 << 20
+
+
+def project_noalloc(layers: Sequence[ProjectLayer], stream=None, descs=None):
+    """structadmm_project_noalloc: the projection with no workspace argument
+    and no device allocation (the library's fixed per-GPU scratch)."""
+    d = descs if descs is not None else _descs(layers)
+    _check(lib().structadmm_project_noalloc(d, len(d), _stream(stream)), "structadmm_project_noalloc")
 
 
 def dual_descs(items) -> "ctypes.Array":

@@ -19,6 +19,7 @@
 #include <algorithm>
 #include <cstdint>
 #include <cstring>
+#include <mutex>
 #include <vector>
 
 #include "sa_device.h"
@@ -983,9 +984,70 @@ extern "C" size_t structadmm_project_workspace(const sa_project_desc *layers, in
     return off;
 }
 
+namespace sa {
+namespace {
+
+// Scratch of structadmm_project_noalloc: one copy per GPU, in the code
+// object's device memory, held until the process ends.  Host code never uses
+// the symbol itself as an address: the device address of each GPU's copy
+// comes from hipGetSymbolAddress with that GPU current.
+__device__ __align__(256) uint8_t scratch[SA_PROJECT_NOALLOC_BYTES];
+
+constexpr int kMaxDevices = 64;
+
+// Device address of the current GPU's scratch (nullptr and an error set on failure).
+void *noalloc_scratch() {
+    static std::mutex mu;
+    static void *ptr[kMaxDevices] = {};
+    int dev = 0;
+    if (check_hip(hipGetDevice(&dev), "project_noalloc: current device")) return nullptr;
+    if (dev < 0 || dev >= kMaxDevices) {
+        fail(SA_E_UNSUPPORTED, "project_noalloc: device index %d beyond %d", dev, kMaxDevices);
+        return nullptr;
+    }
+    std::lock_guard<std::mutex> lock(mu);
+    if (!ptr[dev]) {
+        void *p = nullptr;
+        if (check_hip(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)), "project_noalloc: scratch address")) return nullptr;
+        ptr[dev] = p;
+    }
+    return ptr[dev];
+}
+
+int project_impl(const sa_project_desc *layers, int n_layers, void *ws, size_t ws_bytes, hipStream_t stream);
+
+}  // namespace
+}  // namespace sa
+
 extern "C" int structadmm_project(const sa_project_desc *layers, int n_layers, void *ws,
                                   size_t ws_bytes, hipStream_t stream) {
     clear_error();
+    return project_impl(layers, n_layers, ws, ws_bytes, stream);
+}
+
+extern "C" int structadmm_project_noalloc(const sa_project_desc *layers, int n_layers, hipStream_t stream) {
+    clear_error();
+    if (!layers || n_layers <= 0) return fail(SA_E_ARG, "project: layers must be a non-empty array");
+    size_t need = 0;
+    for (int i = 0; i < n_layers; ++i) {
+        if (int rc = validate_project(layers[i], i)) return rc;
+        LayerPlan p;
+        plan_layer(layers[i], need, p);
+        need = p.end;
+    }
+    if (need > (size_t)SA_PROJECT_NOALLOC_BYTES)
+        return fail(SA_E_WORKSPACE, "project_noalloc: these layers need %zu bytes of scratch, more than the %zu "
+                    "the library holds (use structadmm_project with a workspace)", need,
+                    (size_t)SA_PROJECT_NOALLOC_BYTES);
+    void *ws = need > 0 ? noalloc_scratch() : nullptr;
+    if (need > 0 && !ws) return SA_E_HIP;
+    return project_impl(layers, n_layers, ws, SA_PROJECT_NOALLOC_BYTES, stream);
+}
+
+namespace sa {
+namespace {
+
+int project_impl(const sa_project_desc *layers, int n_layers, void *ws, size_t ws_bytes, hipStream_t stream) {
     if (!layers || n_layers <= 0) return fail(SA_E_ARG, "project: layers must be a non-empty array");
     std::vector<LayerPlan> plan(n_layers);
     size_t off = 0;
@@ -1222,6 +1284,9 @@ extern "C" int structadmm_project(const sa_project_desc *layers, int n_layers, v
     }
     return SA_OK;
 }
+
+}  // namespace
+}  // namespace sa
 
 extern "C" int structadmm_dual_update(const sa_dual_desc *layers, int n_layers, hipStream_t stream) {
     clear_error();
