@@ -297,6 +297,28 @@ size_t structadmm_conv_workspace(const sa_conv_desc *desc);
 
 int structadmm_conv_fwd(const sa_conv_desc *desc, hipStream_t stream);
 
+/* Which kernels structadmm_conv_fwd takes for a descriptor (Section 3: the
+ * compacted CONV is a GEMM over the kept rows and columns; the library picks
+ * a kernel per conv group from the column set and the sizes).  Host only: no
+ * GPU work, the device pointers are not read.  Same validation and error
+ * codes as structadmm_conv_fwd; on success *info is filled. */
+#define SA_CONV_NONE 0       /* group without output channels                          */
+#define SA_CONV_DIRECT 1     /* every tap of a channel run, LDS-staged 32/64/128-filter tiles */
+#define SA_CONV_DIRECT_IG 2  /* every tap of a channel run, 16-filter-granular tiles       */
+#define SA_CONV_FOOTPRINT 3  /* any columns, input footprint of the pixel tile in LDS      */
+#define SA_CONV_GATHER 4     /* any columns, im2col rows gathered to scratch first         */
+typedef struct sa_conv_plan_info {
+    int32_t groups;
+    int32_t path[SA_MAX_CONV_GROUPS]; /* SA_CONV_* per conv group                         */
+    int32_t ksplit;                   /* > 1: columns split over workgroups (small batch) */
+    int32_t space_to_depth;           /* stride of the space-to-depth image, 0 = none     */
+    int32_t ig_tile[3];               /* SA_CONV_DIRECT_IG: MT, NF, WM = 16*MT*WM filters by
+                                         64*NF/WM pixels per workgroup                    */
+    int32_t footprint_tile[3];        /* SA_CONV_FOOTPRINT: TM, TN, NW = 32*TM filters by
+                                         32*NW*TN pixels per workgroup                    */
+} sa_conv_plan_info;
+int structadmm_conv_plan(const sa_conv_desc *desc, sa_conv_plan_info *info);
+
 /* ---- non-structured layers as CSR: structadmm_csr -------------------- */
 /*
  * The non-structured set of Section 3 keeps an arbitrary pattern of weights,

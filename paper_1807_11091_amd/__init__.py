@@ -85,6 +85,16 @@ class ConvDesc(ctypes.Structure):
                 ("col_tap", _vp), ("Y", _vp), ("ws", _vp), ("ws_bytes", ctypes.c_size_t)]
 
 
+class ConvPlanInfo(ctypes.Structure):
+    _fields_ = [("groups", ctypes.c_int32), ("path", ctypes.c_int32 * _G), ("ksplit", ctypes.c_int32),
+                ("space_to_depth", ctypes.c_int32), ("ig_tile", ctypes.c_int32 * 3),
+                ("footprint_tile", ctypes.c_int32 * 3)]
+
+
+# kernel paths of structadmm_conv_plan
+CONV_NONE, CONV_DIRECT, CONV_DIRECT_IG, CONV_FOOTPRINT, CONV_GATHER = 0, 1, 2, 3, 4
+
+
 class CsrDesc(ctypes.Structure):
     _fields_ = [("A", ctypes.c_int64), ("B", ctypes.c_int64), ("C", ctypes.c_int64), ("D", ctypes.c_int64),
                 ("nnz", ctypes.c_int64), ("Z", _vp), ("kept_idx", _vp), ("row_ptr", _vp), ("col", _vp),
@@ -130,6 +140,8 @@ def lib():
         L.structadmm_pack_nhwc.restype = ctypes.c_int
         L.structadmm_conv_fwd.argtypes = [ctypes.POINTER(ConvDesc), _vp]
         L.structadmm_conv_fwd.restype = ctypes.c_int
+        L.structadmm_conv_plan.argtypes = [ctypes.POINTER(ConvDesc), ctypes.POINTER(ConvPlanInfo)]
+        L.structadmm_conv_plan.restype = ctypes.c_int
         L.structadmm_conv_workspace.argtypes = [ctypes.POINTER(ConvDesc)]
         L.structadmm_conv_workspace.restype = ctypes.c_size_t
         L.structadmm_csr.argtypes = [ctypes.POINTER(CsrDesc), _vp]
@@ -316,6 +328,17 @@ def conv_workspace(Xp, sizes: CompactSizes, C: int, D: int, stride: int, pad: in
     N, H, W, Cx = Xp.shape
     d = ConvDesc(N, H, W, Cx, C, D, stride, pad, ctypes.pointer(sizes), 16, 16, 16, 16, 16, None, 0)
     return int(lib().structadmm_conv_workspace(ctypes.byref(d)))
+
+
+def conv_plan(Xp, sizes: CompactSizes, C: int, D: int, stride: int, pad: int) -> dict:
+    """structadmm_conv_plan: the kernels structadmm_conv_fwd takes (host only)."""
+    N, H, W, Cx = Xp.shape if not isinstance(Xp, tuple) else Xp
+    d = ConvDesc(N, H, W, Cx, C, D, stride, pad, ctypes.pointer(sizes), 16, 16, 16, 16, 16, None, 0)
+    info = ConvPlanInfo()
+    _check(lib().structadmm_conv_plan(ctypes.byref(d), ctypes.byref(info)), "structadmm_conv_plan")
+    g = info.groups
+    return {"path": list(info.path)[:g], "ksplit": info.ksplit, "space_to_depth": info.space_to_depth,
+            "ig_tile": tuple(info.ig_tile), "footprint_tile": tuple(info.footprint_tile)}
 
 
 def conv_fwd(Xp, Wc, col_ch, col_tap, sizes: CompactSizes, C: int, D: int, stride: int, pad: int,

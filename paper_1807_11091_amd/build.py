@@ -9,7 +9,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libstructadmm.so")
-SOURCES = ["sa_host.cpp", "admm.hip", "compact.hip", "conv.hip", "sparse.hip"]
+SOURCES = ["sa_host.cpp", "admm.hip", "compact.hip", "conv.hip", "conv_ig.hip", "sparse.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",

@@ -30,10 +30,14 @@
 #include <algorithm>
 #include <cstdint>
 #include <cstring>
+#include <map>
 #include <mutex>
 #include <set>
+#include <tuple>
 #include <utility>
 
+#include "conv_ig.h"
+#include "sa_conv_device.h"
 #include "sa_device.h"
 #include "sa_host.h"
 #include "structadmm.h"
@@ -49,86 +53,6 @@ typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 constexpr int kBK = 64;            // K slice per stage (= compacted row padding)
 constexpr int kRow = kBK + 8;      // LDS row of a staged operand tile (bf16 elements)
 constexpr int kLdsBytes = 160 * 1024;
-constexpr int kRsrcWord3 = 0x00020000;  // raw buffer resource: 32-bit data, range checked
-// Offset used for reads that must return zero: every buffer here is smaller
-// than 2 GiB, so offset + 16 stays past its range without 32-bit wrap-around.
-constexpr uint32_t kInvalidOffset = 0x80000000u;
-
-__device__ inline __amdgpu_buffer_rsrc_t rsrc(const void *base, uint32_t bytes) {
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes, kRsrcWord3);
-}
-
-__device__ inline uint4 bload16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
-    auto v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
-    return make_uint4(v[0], v[1], v[2], v[3]);
-}
-
-// Workgroups are dispatched to the 8 XCDs round-robin (id mod 8); each XCD has
-// its own L2.  Remap ids so that every XCD walks one contiguous range of tiles
-// (neighbouring tiles share input rows and weight slices): XCD x gets the
-// range of q+1 tiles when x < r, of q tiles otherwise (n = 8q + r).
-__device__ inline int xcd_remap(int bid, int n) {
-    const int xcd = bid & 7, local = bid >> 3, q = n >> 3, r = n & 7;
-    return xcd < r ? xcd * (q + 1) + local : r * (q + 1) + (xcd - r) * q + local;
-}
-
-// Stores n <= 8 consecutive bf16 outputs (a 16-byte aligned row of the LDS
-// output tile) with the widest stores the destination's alignment allows:
-// output rows of sum(M_g) channels are 16-byte aligned only when that sum is a
-// multiple of 8 (pruned layers keep any number of filters).
-__device__ inline void store_out8(uint16_t *dst, const uint16_t *src, int n) {
-    const uintptr_t ad = reinterpret_cast<uintptr_t>(dst);
-    if (n == 8 && (ad & 15) == 0) {
-        *reinterpret_cast<uint4 *>(dst) = *reinterpret_cast<const uint4 *>(src);
-        return;
-    }
-    if (n == 8 && (ad & 7) == 0) {
-        reinterpret_cast<uint2 *>(dst)[0] = reinterpret_cast<const uint2 *>(src)[0];
-        reinterpret_cast<uint2 *>(dst)[1] = reinterpret_cast<const uint2 *>(src)[1];
-        return;
-    }
-    int e = 0;
-    if (ad & 2) {  // one element to reach 4-byte alignment
-        dst[0] = src[0];
-        e = 1;
-    }
-    for (; e + 2 <= n; e += 2)
-        *reinterpret_cast<uint32_t *>(dst + e) = (uint32_t)src[e] | ((uint32_t)src[e + 1] << 16);
-    if (e < n) dst[e] = src[e];
-}
-
-// An output tile that holds whole output rows (one conv group owns every output
-// channel and one filter tile covers them) is one contiguous range of Y: it is
-// written with 16-byte stores whatever the row length, the elements read back
-// from the LDS tile (row pitch RP) one by one.  Y + n0 * Cy is 16-byte aligned
-// when Y is (n0 is a multiple of 8).
-template <int RP>
-__device__ inline void store_tile_rows(uint16_t *Y, const uint16_t *sC, int n0, int rows, int Cy,
-                                       const FastDiv &divCy, int tid, int nt) {
-    const int total = rows * Cy;
-    uint16_t *base = Y + (int64_t)n0 * Cy;
-    for (int c = tid; c * 8 < total; c += nt) {
-        const int e0 = c * 8;
-        int pl = (int)fdiv((uint32_t)e0, divCy);
-        int m = e0 - pl * Cy;
-        uint16_t v[8];
-#pragma unroll
-        for (int q = 0; q < 8; ++q) {
-            v[q] = e0 + q < total ? sC[pl * RP + m] : (uint16_t)0;
-            if (++m == Cy) {
-                m = 0;
-                ++pl;
-            }
-        }
-        if (e0 + 8 <= total) {
-            *reinterpret_cast<uint4 *>(base + e0) =
-                make_uint4(v[0] | ((uint32_t)v[1] << 16), v[2] | ((uint32_t)v[3] << 16),
-                           v[4] | ((uint32_t)v[5] << 16), v[6] | ((uint32_t)v[7] << 16));
-        } else {
-            for (int q = 0; e0 + q < total; ++q) base[e0 + q] = v[q];
-        }
-    }
-}
 
 // ---------------------------------------------------------------- k_conv
 // One conv group of a launch (every group of a layer runs in one launch).
@@ -1220,6 +1144,8 @@ struct ConvPlan {
     int path[SA_MAX_CONV_GROUPS];
     int pix_bytes[SA_MAX_CONV_GROUPS], nch[SA_MAX_CONV_GROUPS], ch_lo8[SA_MAX_CONV_GROUPS];
     int TM, TN, NW, patch_bytes, tab_bytes, lds;  // k_conv_patch launch (when any group takes it; NW wavefronts)
+    // the direct groups run on k_ig (16-row filter tiles) instead of k_conv
+    bool direct_ig;
     // split K (launches that would fill few CUs): chunks, and the binary32
     // partial sums [ksplit][part_stride] at byte part_off of the scratch
     int ksplit;
@@ -1233,6 +1159,56 @@ struct ConvPlan {
 };
 
 constexpr int kPatchTMs[5] = {6, 4, 3, 2, 1};
+
+const void *patch_kernel(int TM, int TN, int NW) {
+    switch (TM * 100 + TN * 10 + NW) {
+        case 616: return reinterpret_cast<const void *>(k_conv_patch<6, 1, 6>);
+        case 416: return reinterpret_cast<const void *>(k_conv_patch<4, 1, 6>);
+        case 614: return reinterpret_cast<const void *>(k_conv_patch<6, 1, 4>);
+        case 624: return reinterpret_cast<const void *>(k_conv_patch<6, 2, 4>);
+        case 414: return reinterpret_cast<const void *>(k_conv_patch<4, 1, 4>);
+        case 424: return reinterpret_cast<const void *>(k_conv_patch<4, 2, 4>);
+        case 314: return reinterpret_cast<const void *>(k_conv_patch<3, 1, 4>);
+        case 324: return reinterpret_cast<const void *>(k_conv_patch<3, 2, 4>);
+        case 214: return reinterpret_cast<const void *>(k_conv_patch<2, 1, 4>);
+        case 224: return reinterpret_cast<const void *>(k_conv_patch<2, 2, 4>);
+        case 114: return reinterpret_cast<const void *>(k_conv_patch<1, 1, 4>);
+        case 124: return reinterpret_cast<const void *>(k_conv_patch<1, 2, 4>);
+        default: return nullptr;
+    }
+}
+
+// Workgroups of the footprint kernel <TM, TN, NW> with `lds` bytes of LDS that
+// one CU holds at once (registers and LDS, as the runtime reports them),
+// capped at 2 (the per-workgroup time model below is fitted for at most two);
+// the LDS-only estimate when no GPU answers (a size query without a device).
+int patch_per_cu(int TM, int TN, int NW, int lds) {
+    const int by_lds = std::max(1, std::min(2, kLdsBytes / std::max(1, lds)));
+    const void *kern = patch_kernel(TM, TN, NW);
+    int dev = 0;
+    if (!kern || hipGetDevice(&dev) != hipSuccess) {
+        (void)hipGetLastError();
+        return by_lds;
+    }
+    static std::mutex mu;
+    static std::map<std::tuple<const void *, int, int>, int> cache;
+    {
+        std::lock_guard<std::mutex> lock(mu);
+        auto it = cache.find({kern, lds, dev});
+        if (it != cache.end()) return it->second;
+    }
+    int n = 0;
+    if (allow_full_lds(kern) != SA_OK ||
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kern, 64 * NW, lds) != hipSuccess || n <= 0) {
+        (void)hipGetLastError();
+        clear_error();
+        return by_lds;
+    }
+    n = std::min(n, 2);
+    std::lock_guard<std::mutex> lock(mu);
+    cache[{kern, lds, dev}] = n;
+    return n;
+}
 constexpr int kPatchFixed = 9;  // per-workgroup footprint copy, in 32-filter-block units
 
 int patch_lds(int TM, int TN, int patch_bytes, int tab_bytes, int NW = 4) {
@@ -1278,6 +1254,34 @@ void split_plan(const sa_compact_sizes &s, ConvPlan *pl) {
     p.part_stride = ((int64_t)p.NPQ * p.Cy + 3) / 4 * 4;
     p.part_off = (p.ws_need + 255) / 256 * 256;
     p.ws_need = p.part_off + ((size_t)p.ksplit * p.part_stride * 4 + 255) / 256 * 256;
+}
+
+// Kernel for the groups read straight from the NHWC input (measured on
+// gfx950 over the ResNet-50 and AlexNet layers): k_ig, whose filter tiles grow
+// in steps of 16, when the kept-filter counts are ragged enough that k_conv's
+// 32/64/128-filter tiles would pad the filter work by 15% or more and the
+// columns are few (at most 512 per group: 1x1 CONVs and small 3x3 ones, where
+// the work is bound by memory and the padding is pure loss); k_conv's larger
+// LDS-staged tiles otherwise.  Not for split K (batch 1).
+void direct_plan(const sa_compact_sizes &s, ConvPlan *pl) {
+    ConvPlan &p = *pl;
+    p.direct_ig = false;
+    if (p.ksplit > 1) return;
+    int Ms[SA_MAX_CONV_GROUPS], n = 0;
+    int64_t fine = 0;
+    for (int g = 0; g < s.groups; ++g) {
+        if (p.path[g] != kDirect) continue;
+        if (s.K[g] > 512) return;
+        Ms[n++] = s.M[g];
+        fine += (s.M[g] + 15) / 16 * 16;
+    }
+    if (n == 0) return;
+    int64_t blocks;
+    constexpr int kBN[4] = {128, 64, 128, 32};
+    const int BN = kBN[direct_pick(Ms, n, p.NPQ, &blocks)];
+    int64_t coarse = 0;
+    for (int i = 0; i < n; ++i) coarse += (int64_t)(Ms[i] + BN - 1) / BN * BN;
+    p.direct_ig = coarse * 100 >= fine * 115;
 }
 
 // Validates the descriptor (beyond validate_conv) and chooses, per conv group,
@@ -1396,7 +1400,7 @@ int conv_plan(const sa_conv_desc &d, ConvPlan *pl) {
                 }
             if (cost != least) continue;
             const int64_t lds = pb128 <= kLdsBytes ? patch_lds(tm, 1, (int)pb128, p.tab_bytes) : kLdsBytes;
-            const int64_t per_cu = tm >= 6 ? 1 : std::max<int64_t>(1, std::min<int64_t>(2, kLdsBytes / lds));
+            const int64_t per_cu = patch_per_cu(tm, 1, 4, (int)lds);
             const int64_t wgs = mt * ((p.NPQ + 127) / 128);
             const int64_t t = (wgs + 256 * per_cu - 1) / (256 * per_cu) * (kPatchFixed + tm);
             if (best_t < 0 || t < best_t) best_t = t, best_tm = tm;
@@ -1440,11 +1444,11 @@ int conv_plan(const sa_conv_desc &d, ConvPlan *pl) {
                     if (p.path[g] == kPatch) pb6 = std::max<int64_t>(pb6, ((int64_t)rows6 * Wpp * p.pix_bytes[g] + 15) / 16 * 16);
                 const int64_t lds6 = pb6 <= kLdsBytes ? patch_lds(p.TM, 1, (int)pb6, p.tab_bytes, 6) : (int64_t)kLdsBytes + 1;
                 if (lds6 <= kLdsBytes) {
-                    const int64_t per4 = p.TM >= 6 ? 1 : std::max<int64_t>(1, std::min<int64_t>(2, kLdsBytes / p.lds));
-                    const int64_t per6 = std::max<int64_t>(1, std::min<int64_t>(2, kLdsBytes / lds6));
+                    const int64_t per4 = patch_per_cu(p.TM, 1, 4, p.lds);
+                    const int64_t per6 = patch_per_cu(p.TM, 1, 6, (int)lds6);
                     const int64_t r4 = (mt * ((p.NPQ + 127) / 128) + 256 * per4 - 1) / (256 * per4);
                     const int64_t r6 = (mt * ((p.NPQ + 191) / 192) + 256 * per6 - 1) / (256 * per6);
-                    if (r6 * 3 < r4 * 2) {
+                    if (r6 * 3 <= r4 * 2) {  // a tie goes to six wavefronts (measured faster on the 13x13 layers)
                         p.NW = 6;
                         p.patch_bytes = (int)pb6;
                         p.lds = (int)lds6;
@@ -1468,6 +1472,7 @@ int conv_plan(const sa_conv_desc &d, ConvPlan *pl) {
         p.ws_need += ((size_t)bytes + 255) / 256 * 256;  // each gathered group has its own rows
     }
     split_plan(s, &p);
+    direct_plan(s, &p);
     return SA_OK;
 }
 
@@ -1484,6 +1489,43 @@ extern "C" size_t structadmm_conv_workspace(const sa_conv_desc *desc) {
         return 0;
     }
     return p.ws_need;
+}
+
+extern "C" int structadmm_conv_plan(const sa_conv_desc *desc, sa_conv_plan_info *info) {
+    clear_error();
+    if (!desc || !info) return fail(SA_E_ARG, "conv_plan: desc and info are required");
+    ConvPlan p;
+    if (int rc = conv_plan(*desc, &p)) return rc;
+    const sa_compact_sizes &s = *desc->sizes;
+    memset(info, 0, sizeof *info);
+    info->groups = s.groups;
+    info->ksplit = p.ksplit;
+    info->space_to_depth = p.s2d;
+    IgArgs ia;
+    memset(&ia, 0, sizeof ia);
+    ia.NPQ = p.NPQ;
+    for (int g = 0; g < s.groups; ++g) {
+        switch (p.path[g]) {
+            case kSkip: info->path[g] = SA_CONV_NONE; break;
+            case kDirect:
+                info->path[g] = p.direct_ig ? SA_CONV_DIRECT_IG : SA_CONV_DIRECT;
+                ia.g[ia.ngroups++].M = s.M[g];
+                break;
+            case kPatch: info->path[g] = SA_CONV_FOOTPRINT; break;
+            default: info->path[g] = SA_CONV_GATHER; break;
+        }
+    }
+    if (p.direct_ig && ia.ngroups > 0)
+        ig_tile_shape(ig_pick(ia), &info->ig_tile[0], &info->ig_tile[1], &info->ig_tile[2]);
+    bool patch = false;
+    for (int g = 0; g < s.groups; ++g) patch = patch || p.path[g] == kPatch;
+    if (patch) {
+        info->footprint_tile[0] = p.TM;
+        info->footprint_tile[1] = p.TN;
+        info->footprint_tile[2] = p.NW;
+    }
+    if (!patch) info->space_to_depth = 0;
+    return SA_OK;
 }
 
 extern "C" int structadmm_conv_fwd(const sa_conv_desc *desc, hipStream_t stream) {
@@ -1661,7 +1703,40 @@ extern "C" int structadmm_conv_fwd(const sa_conv_desc *desc, hipStream_t stream)
         G.run = s.ldk[g];
         G.run_base = 0;
     }
-    if (int rc = run_conv(direct, stream)) return rc;
+    if (p.direct_ig && direct.ngroups > 0) {
+        // ragged kept-filter counts over few columns: the 16-row MFMA kernel
+        IgArgs ia;
+        memset(&ia, 0, sizeof ia);
+        ia.X = d.X;
+        ia.Y = d.Y;
+        ia.x_bytes = x_bytes;
+        ia.yshift = (int)((reinterpret_cast<uintptr_t>(d.Y) >> 1) & 7);
+        ia.H = d.H;
+        ia.W = d.W;
+        ia.Cx = d.Cx;
+        ia.D = d.D;
+        ia.stride = d.stride;
+        ia.pad = d.pad;
+        ia.P = P;
+        ia.Q = Q;
+        ia.NPQ = NPQ;
+        ia.Cy = p.Cy;
+        ia.ngroups = direct.ngroups;
+        for (int i = 0; i < direct.ngroups; ++i) {
+            const ConvGroup &c = direct.g[i];
+            IgGroup &G = ia.g[i];
+            G.Wc = c.Wc;
+            G.M = c.M;
+            G.K = c.K;
+            G.ldk = c.ldk;
+            G.run = c.run;
+            G.run_base = c.run_base;
+            G.o_off = c.o_off;
+        }
+        if (int rc = ig_run(ia, -1, stream)) return rc;
+    } else if (int rc = run_conv(direct, stream)) {
+        return rc;
+    }
     if (pa.ngroups > 0) {
         int rc = SA_OK;
         switch (p.TM * 100 + p.TN * 10 + p.NW) {

@@ -69,7 +69,8 @@ def check_compact(gpu, ref):
         coff += K
 
 
-def conv_case(N, Cin, H, Wd, A, C, D, stride, pad, groups, kind, keep, seed, dense_too=True, dead_lo=0):
+def conv_case(N, Cin, H, Wd, A, C, D, stride, pad, groups, kind, keep, seed, dense_too=True, dead_lo=0,
+              expect=None):
     rng = np.random.default_rng(seed)
     B = Cin // groups
     shape = (A, B, C, D)
@@ -99,6 +100,11 @@ def conv_case(N, Cin, H, Wd, A, C, D, stride, pad, groups, kind, keep, seed, den
     Xp = sa.pack_nhwc(dX)
     Xb = oracle.pack(X)
     assert bitwise_equal(Xp.cpu().numpy(), Xb.transpose(0, 2, 3, 1))
+    if expect is not None:  # the kernel the case is meant to exercise
+        plan = sa.conv_plan(Xp, sizes, C, D, stride, pad)
+        for key, want in expect.items():
+            got = plan[key] if key != "path" else set(plan["path"]) - {sa.CONV_NONE}
+            assert got == want, (key, got, want, plan)
     Y = sa.conv_fwd(Xp, Wc, col_ch, col_tap, sizes, C, D, stride, pad)
     Yr = oracle.conv(Xb, rc, C, D, stride, pad)
     y = bf16_bits_to_f64(Y.cpu().numpy())
@@ -168,6 +174,63 @@ SMALL = [
 @pytest.mark.parametrize("case", SMALL, ids=[f"c{i}" for i in range(len(SMALL))])
 def test_conv_small(case):
     conv_case(*case, seed=hash(case) % 2**31)
+
+
+# cases pinned to a kernel and tile shape (the plan is asserted before the
+# parity check, so a change of the selection cannot silently move them)
+PLANNED = [
+    # ragged kept filters over few columns: the 16-row kernel (batches large
+    # enough that the launch is not split over its columns)
+    ((48, 64, 20, 20, 64, 1, 1, 1, 0, 1, sa.FILTER, 0.6), {"path": {sa.CONV_DIRECT_IG}, "ig_tile": (3, 2, 1)}),
+    ((70, 32, 15, 17, 80, 3, 3, 1, 1, 1, sa.FILTER, 0.48), {"path": {sa.CONV_DIRECT_IG}, "ig_tile": (3, 2, 1)}),
+    ((120, 64, 14, 14, 256, 1, 1, 2, 0, 1, sa.FILTER, 0.6), {"path": {sa.CONV_DIRECT_IG}, "ig_tile": (5, 2, 2)}),
+    ((102, 96, 9, 9, 100, 1, 1, 1, 0, 1, sa.FILTER, 0.77), {"path": {sa.CONV_DIRECT_IG}, "ig_tile": (5, 2, 1)}),
+    ((70, 256, 14, 14, 512, 1, 1, 1, 0, 1, sa.FILTER, 0.6), {"path": {sa.CONV_DIRECT}}),
+    # every tap of a channel run, aligned or wide: the LDS-staged kernel
+    ((114, 64, 12, 12, 128, 3, 3, 1, 1, 1, sa.FILTER, 1.0), {"path": {sa.CONV_DIRECT}}),
+    ((114, 64, 12, 12, 96, 3, 3, 1, 1, 1, sa.FILTER, 0.6), {"path": {sa.CONV_DIRECT}}),
+    # split over the columns at a small batch
+    ((1, 64, 12, 12, 96, 3, 3, 1, 1, 1, sa.FILTER, 0.6), {"path": {sa.CONV_DIRECT}, "ksplit": 4}),
+    # footprint kernel: six-wavefront tiles of 192 filters (AlexNet conv4 at
+    # batch 128: one workgroup per CU, 226 tiles of 192 pixels fill one round
+    # where 338 of 128 need two) and four-wavefront tiles (two per CU)
+    ((128, 384, 13, 13, 384, 3, 3, 1, 1, 2, sa.SHAPE, 0.3), {"path": {sa.CONV_FOOTPRINT}, "footprint_tile": (6, 1, 6)}),
+    ((400, 16, 13, 13, 128, 3, 3, 1, 1, 1, sa.SHAPE, 0.3), {"path": {sa.CONV_FOOTPRINT}, "footprint_tile": (4, 1, 4)}),
+    ((2, 32, 13, 13, 48, 3, 3, 1, 1, 2, sa.SHAPE, 0.3), {"path": {sa.CONV_FOOTPRINT}}),
+    # stem: space-to-depth image, then the footprint kernel
+    ((2, 3, 30, 28, 20, 7, 7, 2, 3, 1, sa.FILTER, 0.6), {"path": {sa.CONV_FOOTPRINT}, "space_to_depth": 2}),
+]
+
+
+@pytest.mark.parametrize("case,expect", PLANNED, ids=[f"p{i}" for i in range(len(PLANNED))])
+def test_conv_planned_kernel(case, expect):
+    conv_case(*case, seed=sum(case[:9]), dense_too=False, expect=expect)
+
+
+def test_conv_16row_tile_shapes():
+    """The 16-row kernel over 1x1 layers of 64 input channels at 40k pixels,
+    kept-filter counts that make its launcher take different tile shapes, all
+    against the oracle."""
+    seen = set()
+    for A, keep in ((64, 0.6), (128, 0.6), (256, 0.6), (512, 0.6), (160, 0.5), (1024, 0.6), (40, 0.5)):
+        rng = np.random.default_rng(A + int(100 * keep))
+        X = rng.standard_normal((50, 64, 28, 28)).astype(np.float32)
+        k = max(1, int(round(keep * A)))
+        mask = np.zeros(A, np.uint8)
+        mask[rng.choice(A, size=k, replace=False)] = 1
+        Z = (0.05 * rng.standard_normal((A, 64, 1, 1))).astype(np.float32)
+        Wc, ri, cc, ct, sizes = sa.compact(to_dev(Z), 1, row_mask=to_dev(mask))
+        Xp = sa.pack_nhwc(to_dev(X))
+        plan = sa.conv_plan(Xp, sizes, 1, 1, 1, 0)
+        if plan["path"] == [sa.CONV_DIRECT_IG]:
+            seen.add(plan["ig_tile"])
+        Y = sa.conv_fwd(Xp, Wc, cc, ct, sizes, 1, 1, 1, 0)
+        rc = oracle.compact(Z, 1, row_mask=mask)
+        sel = [0, 17, 49]  # three images of the batch
+        Yr = oracle.conv(oracle.pack(X[sel]), rc, 1, 1, 1, 0)
+        err = maxabs_over_rms(bf16_bits_to_f64(Y.cpu().numpy()[sel]), Yr)
+        assert err <= TOL, (A, keep, plan, err)
+    assert len(seen) >= 3, seen
 
 
 def test_conv_unaligned_channel_window():
