@@ -19,9 +19,10 @@ Output: one JSON line.  value = compacted-CONV TFLOP/s over the step's
 compacted convolutions (algorithmic flops 2*N*P*Q*sum_g M_g*K_g / their
 HIP-event time); speedup_vs_dense = dense CONV time / compacted CONV time;
 admm_gbps = algorithmic bytes of steps 1-2 / their time.  Each CONV is bracketed
-by HIP events on the stream it runs on; a spin kernel ahead of each timed
-block lets the host enqueue the block before the GPU reaches it, so the events
-measure the kernels rather than host gaps.  ms_per_step is the wall time of a
+by HIP events on the stream it runs on (recorded without a system-scope
+fence, which would write back and invalidate the caches at every event); a
+spin kernel ahead of each timed block lets the host enqueue the block before
+the GPU reaches it, so the events measure the kernels rather than host gaps.  ms_per_step is the wall time of a
 step: the GPU time of its parts, the host-side synchronisations of the
 compactions, and the spins (reported separately as spin_ms_per_step).
 """
@@ -77,6 +78,46 @@ class Layer:
     pass
 
 
+class TimingEvent:
+    """A HIP timing event recorded without the system-scope fence
+    (hipEventDisableSystemFence): torch's events write back and invalidate the
+    caches when recorded, which costs each bracketed kernel several
+    microseconds and starts it with cold caches.  Only timestamps are read, after a
+    device-wide synchronisation."""
+    _hip = None
+
+    def __init__(self):
+        import ctypes
+        if TimingEvent._hip is None:
+            lib = ctypes.CDLL("libamdhip64.so")  # the HIP runtime torch has loaded
+            lib.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint]
+            lib.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+            lib.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+            lib.hipEventDestroy.argtypes = [ctypes.c_void_p]
+            TimingEvent._hip = lib
+        self._ev = ctypes.c_void_p()
+        rc = TimingEvent._hip.hipEventCreateWithFlags(ctypes.byref(self._ev), 0x20000000)
+        if rc != 0:
+            raise RuntimeError(f"hipEventCreateWithFlags failed ({rc})")
+
+    def record(self, torch):
+        rc = TimingEvent._hip.hipEventRecord(self._ev, torch.cuda.current_stream().cuda_stream)
+        if rc != 0:
+            raise RuntimeError(f"hipEventRecord failed ({rc})")
+
+    def elapsed_time(self, other):
+        import ctypes
+        ms = ctypes.c_float()
+        rc = TimingEvent._hip.hipEventElapsedTime(ctypes.byref(ms), self._ev, other._ev)
+        if rc != 0:
+            raise RuntimeError(f"hipEventElapsedTime failed ({rc})")
+        return ms.value
+
+    def __del__(self):
+        if TimingEvent._hip is not None and self._ev:
+            TimingEvent._hip.hipEventDestroy(self._ev)
+
+
 def setup(torch, sa, wl):
     from workloads import input_nchw, layer_tensors
     dev = "cuda"
@@ -118,8 +159,8 @@ def run_step(torch, sa, wl, layers, ws, cws, ev, record):
 
     def mark(name):
         if record:
-            e = torch.cuda.Event(enable_timing=True)
-            e.record()
+            e = TimingEvent()
+            e.record(torch)
             marks.setdefault(name, []).append(e)
 
     # a short spin kernel ahead of each timed block lets the host enqueue the

@@ -87,7 +87,7 @@ class ConvDesc(ctypes.Structure):
 
 class ConvPlanInfo(ctypes.Structure):
     _fields_ = [("groups", ctypes.c_int32), ("path", ctypes.c_int32 * _G), ("ksplit", ctypes.c_int32),
-                ("space_to_depth", ctypes.c_int32), ("ig_tile", ctypes.c_int32 * 3),
+                ("space_to_depth", ctypes.c_int32), ("ig_tile", ctypes.c_int32 * 4),
                 ("footprint_tile", ctypes.c_int32 * 3)]
 
 

@@ -1259,19 +1259,21 @@ void split_plan(const sa_compact_sizes &s, ConvPlan *pl) {
 // Kernel for the groups read straight from the NHWC input (measured on
 // gfx950 over the ResNet-50 and AlexNet layers): k_ig, whose filter tiles grow
 // in steps of 16, when the kept-filter counts are ragged enough that k_conv's
-// 32/64/128-filter tiles would pad the filter work by 15% or more and the
-// columns are few (at most 512 per group: 1x1 CONVs and small 3x3 ones, where
-// the work is bound by memory and the padding is pure loss); k_conv's larger
-// LDS-staged tiles otherwise.  Not for split K (batch 1).
+// 32/64/128-filter tiles would pad the filter work by 15% or more, and either
+// the columns are few (at most 512 per group: 1x1 CONVs and small 3x3 ones,
+// bound by memory, where the padding is pure loss) or k_conv would have fewer
+// than 1024 tiles (late ResNet stages, where k_ig splits the columns over
+// the wavefronts of a workgroup); k_conv's larger LDS-staged tiles otherwise.
+// Not for split K over workgroups (batch 1).
 void direct_plan(const sa_compact_sizes &s, ConvPlan *pl) {
     ConvPlan &p = *pl;
     p.direct_ig = false;
     if (p.ksplit > 1) return;
-    int Ms[SA_MAX_CONV_GROUPS], n = 0;
+    int Ms[SA_MAX_CONV_GROUPS], n = 0, maxK = 0;
     int64_t fine = 0;
     for (int g = 0; g < s.groups; ++g) {
         if (p.path[g] != kDirect) continue;
-        if (s.K[g] > 512) return;
+        maxK = std::max(maxK, s.K[g]);
         Ms[n++] = s.M[g];
         fine += (s.M[g] + 15) / 16 * 16;
     }
@@ -1281,7 +1283,7 @@ void direct_plan(const sa_compact_sizes &s, ConvPlan *pl) {
     const int BN = kBN[direct_pick(Ms, n, p.NPQ, &blocks)];
     int64_t coarse = 0;
     for (int i = 0; i < n; ++i) coarse += (int64_t)(Ms[i] + BN - 1) / BN * BN;
-    p.direct_ig = coarse * 100 >= fine * 115;
+    p.direct_ig = coarse * 100 >= fine * 115 && (maxK <= 512 || blocks < 1024);
 }
 
 // Validates the descriptor (beyond validate_conv) and chooses, per conv group,
@@ -1515,8 +1517,13 @@ extern "C" int structadmm_conv_plan(const sa_conv_desc *desc, sa_conv_plan_info 
             default: info->path[g] = SA_CONV_GATHER; break;
         }
     }
-    if (p.direct_ig && ia.ngroups > 0)
-        ig_tile_shape(ig_pick(ia), &info->ig_tile[0], &info->ig_tile[1], &info->ig_tile[2]);
+    if (p.direct_ig && ia.ngroups > 0) {
+        for (int g = 0, i = 0; g < s.groups; ++g)
+            if (p.path[g] == kDirect) ia.g[i++].ldk = s.ldk[g];
+        const int t = ig_pick(ia);
+        ig_tile_shape(t, &info->ig_tile[0], &info->ig_tile[1], &info->ig_tile[2]);
+        info->ig_tile[3] = ig_split(ia, t);
+    }
     bool patch = false;
     for (int g = 0; g < s.groups; ++g) patch = patch || p.path[g] == kPatch;
     if (patch) {

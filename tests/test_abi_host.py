@@ -47,6 +47,8 @@ def _c_layout():
         "sa_compact_sizes": ("CompactSizes", ["M", "K", "ldk", "wc_offset", "row_offset", "run", "run_base",
                                               "ch_lo", "ch_span"]),
         "sa_conv_desc": ("ConvDesc", ["N", "pad", "sizes", "X", "Y", "ws", "ws_bytes"]),
+        "sa_conv_plan_info": ("ConvPlanInfo", ["groups", "path", "ksplit", "space_to_depth", "ig_tile",
+                                               "footprint_tile"]),
         "sa_csr_desc": ("CsrDesc", ["A", "D", "nnz", "Z", "kept_idx", "row_ptr", "col", "val"]),
         "sa_sparse_conv_desc": ("SparseConvDesc", ["N", "Cx", "A", "D", "groups", "stride", "pad", "nnz", "X",
                                                    "row_ptr", "col", "val", "Y", "ws", "ws_bytes",
@@ -214,6 +216,44 @@ def test_compact_and_conv_validation():
     s.ch_span[0] = 16
     wide = dict(W=4000, Cx=16)
     assert L.structadmm_conv_workspace(ctypes.byref(desc(**wide))) == 8 * 4000 * 64 * 2
+
+
+def test_conv_plan_host_only():
+    """structadmm_conv_plan on the host (no device pointer is read): the
+    kernel each kind of layer takes, and the descriptor checks."""
+    L = sa.lib()
+    s = sa.CompactSizes()
+    s.groups = 1
+
+    def plan(N, H, W, Cx, C, D, stride, pad, M, run=None, cols=None):
+        K = C * D * (Cx if run is None else run) if cols is None else cols
+        s.M[0], s.K[0], s.ldk[0] = M, K, (K + 63) // 64 * 64
+        s.run[0], s.run_base[0] = (0, 0) if run is None else (run, 0)
+        s.ch_lo[0], s.ch_span[0] = 0, Cx
+        d = sa.ConvDesc(N, H, W, Cx, C, D, stride, pad, ctypes.pointer(s), FAKE, FAKE, FAKE, FAKE, FAKE, None, 0)
+        info = sa.ConvPlanInfo()
+        rc = L.structadmm_conv_plan(ctypes.byref(d), ctypes.byref(info))
+        return rc, info
+
+    # 38 kept filters of a 1x1 layer over 64 channels, 56x56 at batch 64: the 16-row kernel
+    rc, info = plan(64, 56, 56, 64, 1, 1, 1, 0, 38, run=64)
+    assert rc == 0 and list(info.path)[:1] == [sa.CONV_DIRECT_IG] and info.ksplit == 1
+    assert tuple(info.ig_tile)[:3] == (3, 2, 1)
+    # every filter of a 3x3 layer: the LDS-staged kernel
+    rc, info = plan(64, 28, 28, 128, 3, 3, 1, 1, 128, run=128)
+    assert rc == 0 and list(info.path)[:1] == [sa.CONV_DIRECT]
+    # batch 1: split over the columns
+    rc, info = plan(1, 13, 13, 256, 3, 3, 1, 1, 384, run=256)
+    assert rc == 0 and info.ksplit > 1
+    # 3 input channels: the space-to-depth image and the footprint kernel
+    rc, info = plan(2, 30, 28, 3, 7, 7, 2, 3, 12, cols=147)
+    assert rc == 0 and list(info.path)[:1] == [sa.CONV_FOOTPRINT] and info.space_to_depth == 2
+    # arbitrary columns over 8-aligned channels: the footprint kernel
+    rc, info = plan(8, 13, 13, 64, 3, 3, 1, 1, 48, cols=100)
+    assert rc == 0 and list(info.path)[:1] == [sa.CONV_FOOTPRINT] and info.space_to_depth == 0
+    d = sa.ConvDesc(1, 8, 8, 8, 3, 3, 0, 1, ctypes.pointer(s), FAKE, FAKE, FAKE, FAKE, FAKE, None, 0)
+    assert L.structadmm_conv_plan(ctypes.byref(d), ctypes.byref(sa.ConvPlanInfo())) == -1  # stride 0
+    assert L.structadmm_conv_plan(ctypes.byref(d), None) == -1
 
 
 def test_csr_validation():

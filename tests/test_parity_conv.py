@@ -181,10 +181,10 @@ def test_conv_small(case):
 PLANNED = [
     # ragged kept filters over few columns: the 16-row kernel (batches large
     # enough that the launch is not split over its columns)
-    ((48, 64, 20, 20, 64, 1, 1, 1, 0, 1, sa.FILTER, 0.6), {"path": {sa.CONV_DIRECT_IG}, "ig_tile": (3, 2, 1)}),
-    ((70, 32, 15, 17, 80, 3, 3, 1, 1, 1, sa.FILTER, 0.48), {"path": {sa.CONV_DIRECT_IG}, "ig_tile": (3, 2, 1)}),
-    ((120, 64, 14, 14, 256, 1, 1, 2, 0, 1, sa.FILTER, 0.6), {"path": {sa.CONV_DIRECT_IG}, "ig_tile": (5, 2, 2)}),
-    ((102, 96, 9, 9, 100, 1, 1, 1, 0, 1, sa.FILTER, 0.77), {"path": {sa.CONV_DIRECT_IG}, "ig_tile": (5, 2, 1)}),
+    ((48, 64, 20, 20, 64, 1, 1, 1, 0, 1, sa.FILTER, 0.6), {"path": {sa.CONV_DIRECT_IG}, "ig_tile": (3, 2, 1, 1)}),
+    ((70, 32, 15, 17, 80, 3, 3, 1, 1, 1, sa.FILTER, 0.48), {"path": {sa.CONV_DIRECT_IG}, "ig_tile": (3, 2, 1, 2)}),
+    ((120, 64, 14, 14, 256, 1, 1, 2, 0, 1, sa.FILTER, 0.6), {"path": {sa.CONV_DIRECT_IG}, "ig_tile": (5, 2, 2, 1)}),
+    ((102, 96, 9, 9, 100, 1, 1, 1, 0, 1, sa.FILTER, 0.77), {"path": {sa.CONV_DIRECT_IG}, "ig_tile": (5, 2, 1, 1)}),
     ((70, 256, 14, 14, 512, 1, 1, 1, 0, 1, sa.FILTER, 0.6), {"path": {sa.CONV_DIRECT}}),
     # every tap of a channel run, aligned or wide: the LDS-staged kernel
     ((114, 64, 12, 12, 128, 3, 3, 1, 1, 1, sa.FILTER, 1.0), {"path": {sa.CONV_DIRECT}}),
