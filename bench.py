@@ -69,6 +69,14 @@ def parse():
     p.add_argument("--sparse", metavar="JSON", default=None,
                    help="only the CSR CONV of non-structured pruning: density sweep of the [256,256,3,3] "
                         "layer and batch-1 AlexNet conv2-5 at the sparsities of Tables 4-5")
+    p.add_argument("--conv-only", metavar="WORKLOAD", default=None,
+                   help="only the compacted CONVs of one workload, --reps times each, untimed (a short "
+                        "program for hardware-counter runs); prints one JSON line per layer")
+    p.add_argument("--kernel", default=None,
+                   help="with --conv-only: only the layers whose compacted CONV is this one kernel")
+    p.add_argument("--layers", default=None, help="with --conv-only: comma-separated layer indices")
+    p.add_argument("--dense", action="store_true", help="with --conv-only: the uncompacted matrices instead")
+    p.add_argument("--reps", type=int, default=5, help="with --conv-only: launches per layer")
     p.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                    help="only copy MIB MiB device-to-device 5 times (HBM counter calibration) and exit")
     return p.parse_args()
@@ -188,6 +196,7 @@ def run_step(torch, sa, wl, layers, ws, cws, ev, record):
             o.flops_c = 2 * wl.batch * L.P * L.Q * sum(sizes.M[g] * sizes.K[g] for g in range(sizes.groups))
             o.flops_d = 2 * wl.batch * L.P * L.Q * sum(sized.M[g] * sized.K[g] for g in range(sized.groups))
             o.sizes_c = sizes
+            o.plan_c = sa.conv_plan(o.Xp, sizes, L.C, L.D, L.stride, L.pad)
         # scratch for groups whose im2col rows are gathered first; the kept
         # columns move between ADMM steps, so it is sized for every step (outside
         # the CONV events) and grown when a step needs more
@@ -274,6 +283,51 @@ def cpu_baseline(wl, seconds):
                       f"({f / 1e9:.1f} GFLOP in {t:.1f} s); fused ADMM step of all {len(wl.layers)} layers "
                       f"({n} weights) took {t_admm * 1e3:.0f} ms on one core",
             "admm_fused_GBps_1_core": round(20 * n / t_admm / 1e9, 3)}
+
+
+def conv_only(args):
+    """The compacted (or dense) CONV of the selected layers, args.reps launches
+    each, layer after layer, with nothing timed: the program hardware-counter
+    runs profile.  Every launch of a layer runs the kernel(s) of its plan."""
+    import torch
+    import paper_1807_11091_amd as sa
+    from workloads import WORKLOADS
+    if not torch.cuda.is_available():
+        raise SystemExit("bench.py needs a GPU")
+    sa.lib()
+    wl = WORKLOADS[args.conv_only]
+    layers = setup(torch, sa, wl)
+    ws = torch.empty(max(256, sa.project_workspace([o.proj for o in layers])), dtype=torch.uint8, device="cuda")
+    cws = torch.empty(sa.COMPACT_WS_BYTES, dtype=torch.uint8, device="cuda")
+    sa.project([o.proj for o in layers], ws)
+    ids = range(len(layers)) if args.layers is None else [int(i) for i in args.layers.split(",")]
+    picked = []
+    for i in ids:
+        o, L = layers[i], layers[i].cfg
+        rows = o.mask if (o.kind == sa.FILTER and not args.dense) else None
+        cols = o.mask if (o.kind == sa.SHAPE and not args.dense) else None
+        c = sa.compact(o.Z, L.groups, row_mask=rows, col_mask=cols, ws=cws)
+        sizes = o.sizes_c = c[4]
+        plan = sa.conv_plan(o.Xp, sizes, L.C, L.D, L.stride, L.pad)
+        kern = kernel_of(sa, plan)
+        if args.kernel is not None and kern != args.kernel:
+            continue
+        sa.pack_nhwc(o.X, out=o.Xp)
+        Y = torch.empty(sa.conv_out_shape(*o.Xp.shape[:3], L.C, L.D, L.stride, L.pad, sizes),
+                        dtype=torch.uint16, device="cuda")
+        cv = torch.empty(max(256, sa.conv_workspace(o.Xp, sizes, L.C, L.D, L.stride, L.pad)),
+                         dtype=torch.uint8, device="cuda")
+        picked.append((i, o, L, c, Y, cv, plan, kern))
+    torch.cuda.synchronize()
+    for i, o, L, c, Y, cv, plan, kern in picked:
+        for _ in range(args.reps):
+            sa.conv_fwd(o.Xp, c[0], c[2], c[3], c[4], L.C, L.D, L.stride, L.pad, Y=Y, ws=cv)
+        torch.cuda.synchronize()
+        sizes = c[4]
+        fl = 2 * wl.batch * L.P * L.Q * sum(sizes.M[g] * sizes.K[g] for g in range(sizes.groups))
+        print(json.dumps({"layer": i, "name": L.name, "kernel": kern, "plan": plan, "flops": fl,
+                          "bytes": layer_bytes(o), "M": [sizes.M[g] for g in range(sizes.groups)],
+                          "K": [sizes.K[g] for g in range(sizes.groups)], "launches": args.reps}), flush=True)
 
 
 def copy_probe(mib):
@@ -823,6 +877,9 @@ def main():
     if args.suite:
         suite(args.suite)
         return
+    if args.conv_only:
+        conv_only(args)
+        return
     if args.gpus != 1:
         print(json.dumps({"error": "this build measures one GPU only (one MI355X); "
                                    "multi-GPU runs are not part of it: run with --gpus 1"}))
@@ -868,6 +925,7 @@ def main():
         "spin_ms_per_step": main_res["spin_ms_per_step"],
         "gpu_ms_per_step": main_res["gpu_ms_per_step"],
         "per_layer": main_res["per_layer"],
+        "compact_by_kernel": main_res["compact_by_kernel"],
         "roofline": main_res["roofline"],
         SECOND_WORKLOAD: {k: second[k] for k in ("compact_tflops", "dense_tflops", "speedup_vs_dense",
                                                  "compact_us", "dense_us", "admm_gbps", "admm_us",
@@ -891,6 +949,27 @@ def layer_bytes(o):
 
 def progress(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+# source file of each CONV kernel (its profile summaries hold that file's hash)
+KERNEL_SOURCE = {"k_conv": "conv.hip", "k_conv_patch": "conv.hip", "k_ig": "conv_ig.hip", "k_igk": "conv_ig.hip"}
+
+
+def kernel_of(sa, plan):
+    """The one kernel a compacted CONV launches, from the library's plan
+    (None when it launches more than one: space-to-depth image first, column
+    split with a summing pass, gathered im2col rows first, mixed groups)."""
+    paths = set(plan["path"]) - {sa.CONV_NONE}
+    if len(paths) != 1 or plan["ksplit"] > 1 or plan["space_to_depth"]:
+        return None
+    p = paths.pop()
+    if p == sa.CONV_DIRECT:
+        return "k_conv"
+    if p == sa.CONV_DIRECT_IG:
+        return "k_igk" if plan["ig_tile"][3] > 1 else "k_ig"
+    if p == sa.CONV_FOOTPRINT:
+        return "k_conv_patch"
+    return None
 
 
 def measure(torch, sa, wl, steps, warmup):
@@ -932,16 +1011,25 @@ def measure(torch, sa, wl, steps, warmup):
     flops_d = sum(o.flops_d for o in layers)
     n_el = sum(o.cfg.n for o in layers)
     admm_bytes = 20 * n_el + 16 * n_el  # fused step (W,U read; Z,U,G written) + gradient (W,Z,U read; G written)
-    # the dominant kernel of the compacted path: the kernel that runs the
-    # layers whose input channels are 8-aligned (all but a few-channel stem)
-    kern = {sa.FILTER: "k_conv", sa.SHAPE: "k_conv_patch"}[layers[0].kind]
-    dom = [i for i, o in enumerate(layers) if o.Xp.shape[3] % 8 == 0]
+    # the dominant kernel of the compacted path: the kernel (from the library's
+    # plan of each layer) whose launches take the most time in the step; a
+    # layer whose CONV runs more than one kernel is not counted for any
+    fam = [kernel_of(sa, o.plan_c) for o in layers]
+    by = {}
+    for i, f in enumerate(fam):
+        if f is not None:
+            by.setdefault(f, []).append(i)
+    kern = max(by, key=lambda f: sum(t_c[i] for i in by[f]))
+    dom = by[kern]
     dom_ms = sum(t_c[i] for i in dom)
     dom_flops = sum(layers[i].flops_c for i in dom)
     dom_tflops = dom_flops / (dom_ms * 1e-3) / 1e12
     # per-layer roofline min(MFMA, AI * HBM) time over the measured time
     roof_ms = sum(max(layers[i].flops_c / (BF16_PEAK_TFLOPS * 1e12), layer_bytes(layers[i]) / (HBM_PEAK_GBS * 1e9))
                   for i in dom) * 1e3
+    by_kernel = {f: {"layers": len(v), "us": round(sum(t_c[i] for i in v) * 1e3, 1),
+                     "tflops": round(sum(layers[i].flops_c for i in v) / (sum(t_c[i] for i in v) * 1e-3) / 1e12, 1)}
+                 for f, v in by.items()}
     per_layer = [{"layer": o.cfg.name, "compact_us": round(tc * 1e3, 1), "dense_us": round(td * 1e3, 1),
                   "compact_tflops": round(o.flops_c / (tc * 1e-3) / 1e12, 1),
                   "dense_tflops": round(o.flops_d / (td * 1e-3) / 1e12, 1),
@@ -960,13 +1048,14 @@ def measure(torch, sa, wl, steps, warmup):
         "spin_ms_per_step": round(spin_ms, 3),
         "gpu_ms_per_step": round(t_admm + t_pack + sum(t_c) + sum(t_d), 4),
         "per_layer": per_layer,
+        "compact_by_kernel": by_kernel,
         "roofline": {"kernel": f"{kern} (compacted CONVs of {len(dom)} of {len(layers)} layers)",
                      "bound": "mfma", "achieved": round(dom_tflops, 2), "peak": BF16_PEAK_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(dom_tflops / BF16_PEAK_TFLOPS, 4),
                      "avg_launch_us": round(dom_ms * 1e3 / len(dom), 2), "launches_per_step": len(dom),
                      "flops_per_launch": round(dom_flops / len(dom)),
                      "frac_of_layer_roofline": round(roof_ms / dom_ms, 4),
-                     "traffic": traffic_per_launch(kern, wl.name)},
+                     "traffic": traffic_per_launch(kern, wl.name, KERNEL_SOURCE[kern])},
     }
     del layers
     torch.cuda.empty_cache()

@@ -238,8 +238,6 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
         // LDS position of output (pl, m): whole rows keep Y's pitch Cy, other
         // rows sit at pl * CP + shift(pl), shift = Y's misalignment of the row
         const int pitch = whole ? a.Cy : CP;
-        const bool fast = whole ? (a.Cy & 3) == 0
-                                : ((a.Cy | G.o_off | P.m0 | a.yshift) & 7) == 0;  // every row 16-byte aligned
 #pragma unroll
         for (int j = 0; j < NF; ++j) {
             const int pl = (wn * NF + j) * 16 + (lane & 15);
@@ -252,14 +250,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
 #pragma unroll
                 for (int e = 0; e < 4; ++e) o[e] = f32_to_bf16_bits(acc[i][j][e]);  // round to nearest even
                 if (ml >= count) continue;  // filters past the group (padding rows)
-                if (fast) {
-                    *reinterpret_cast<uint2 *>(row + ml) =
-                        make_uint2(o[0] | ((uint32_t)o[1] << 16), o[2] | ((uint32_t)o[3] << 16));
-                } else {  // a quad may straddle the end of a row of Cy elements
-#pragma unroll
-                    for (int e = 0; e < 4; ++e)
-                        if (ml + e < count) row[ml + e] = o[e];
-                }
+                stage_quad(row + ml, o, count - ml);  // a quad may straddle the end of the group
             }
         }
         __syncthreads();
@@ -547,7 +538,6 @@ __global__ __launch_bounds__(256 * KG) void k_igk(IgArgs a) {
 #pragma unroll
                     for (int e = 0; e < 4; ++e) acc[i][j][e] += r[((i * NF + j) * 4 + e) * 64];
         }
-        const bool fast = whole ? (a.Cy & 3) == 0 : ((a.Cy | G.o_off | P.m0 | a.yshift) & 7) == 0;
 #pragma unroll
         for (int j = 0; j < NF; ++j) {
             const int pl = (wn * NF + j) * 16 + (lane & 15);
@@ -560,14 +550,7 @@ __global__ __launch_bounds__(256 * KG) void k_igk(IgArgs a) {
 #pragma unroll
                 for (int e = 0; e < 4; ++e) o[e] = f32_to_bf16_bits(acc[i][j][e]);
                 if (ml >= count) continue;
-                if (fast) {
-                    *reinterpret_cast<uint2 *>(row + ml) =
-                        make_uint2(o[0] | ((uint32_t)o[1] << 16), o[2] | ((uint32_t)o[3] << 16));
-                } else {
-#pragma unroll
-                    for (int e = 0; e < 4; ++e)
-                        if (ml + e < count) row[ml + e] = o[e];
-                }
+                stage_quad(row + ml, o, count - ml);
             }
         }
     }

@@ -34,6 +34,24 @@ __device__ inline int xcd_remap(int bid, int n) {
     return xcd < r ? xcd * (q + 1) + local : r * (q + 1) + (xcd - r) * q + local;
 }
 
+// Writes the first min(n, 4) of four consecutive bf16 outputs to the LDS
+// output tile at dst with the widest stores dst's alignment allows (output rows
+// of any length: a quad is 8-, 4- or 2-byte aligned).
+__device__ inline void stage_quad(uint16_t *dst, const uint16_t *o, int n) {
+    const uint32_t lo = o[0] | ((uint32_t)o[1] << 16), hi = o[2] | ((uint32_t)o[3] << 16);
+    const uintptr_t ad = reinterpret_cast<uintptr_t>(dst);
+    if (n >= 4 && (ad & 7) == 0) {
+        *reinterpret_cast<uint2 *>(dst) = make_uint2(lo, hi);
+    } else if (n >= 4 && (ad & 3) == 0) {
+        reinterpret_cast<uint32_t *>(dst)[0] = lo;
+        reinterpret_cast<uint32_t *>(dst)[1] = hi;
+    } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            if (e < n) dst[e] = o[e];
+    }
+}
+
 // Stores n <= 8 consecutive bf16 outputs (a 16-byte aligned row of the LDS
 // output tile) with the widest stores the destination's alignment allows:
 // output rows of sum(M_g) channels are 16-byte aligned only when that sum is a
