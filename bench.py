@@ -343,9 +343,10 @@ def copy_probe(mib):
     print(json.dumps({"copy_probe_bytes": n, "copies": 5}))
 
 
-def traffic_per_launch(kernel, workload, source="conv.hip"):
-    """HBM bytes per launch of `kernel` on `workload` from the committed
-    counter summary, if it was taken on the current source (else None)."""
+def traffic_per_launch(kernel, workload, source="conv.hip", field="bytes per launch"):
+    """HBM bytes per launch of `kernel` on `workload` (or another figure of
+    its committed counter summary: "kernel µs per launch"), if the summary was
+    taken on the current source (else None)."""
     import hashlib
     summ = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_traffic.md")
     src = os.path.join(ROOT, "paper_1807_11091_amd", "csrc", source)
@@ -357,9 +358,9 @@ def traffic_per_launch(kernel, workload, source="conv.hip"):
             k, v = line[2:].split(":", 1)
             fields[k.strip()] = v.strip().strip("`")
     digest = hashlib.sha256(open(src, "rb").read()).hexdigest()
-    if fields.get(f"{source} sha256") != digest or "bytes per launch" not in fields:
+    if fields.get(f"{source} sha256") != digest or field not in fields:
         return None
-    return int(fields["bytes per launch"])
+    return float(fields[field]) if "." in fields[field] else int(fields[field])
 
 
 # ---------------------------------------------------------------- suite
@@ -894,6 +895,8 @@ def main():
     main_res = measure(torch, sa, WORKLOADS[WORKLOAD], args.steps, args.warmup)
     second = measure(torch, sa, WORKLOADS[SECOND_WORKLOAD], max(3, args.steps // 4), max(1, args.warmup))
     warm = admm_warm(torch, sa, WORKLOADS[WORKLOAD])
+    progress("library GEMM reference")
+    gref = gemm_reference(torch, sa, WORKLOADS[WORKLOAD])
     wl = WORKLOADS[WORKLOAD]
     out = {
         "metric": METRIC,
@@ -922,6 +925,9 @@ def main():
                      "through the caches (cold); admm_warm_* = the same two calls back to back",
         "admm_warm_gbps": warm["step_gbps"],
         "admm_warm_us": warm["step_us"],
+        "library_gemm_reference": gref | {"note": "torch.matmul (hipBLASLt) bf16 on each layer's GEMM shape with "
+                                                  "the im2col matrix in memory (im2col not timed); context "
+                                                  "for the CONV rates, not part of the step"},
         "spin_ms_per_step": main_res["spin_ms_per_step"],
         "gpu_ms_per_step": main_res["gpu_ms_per_step"],
         "per_layer": main_res["per_layer"],
@@ -1055,11 +1061,39 @@ def measure(torch, sa, wl, steps, warmup):
                      "avg_launch_us": round(dom_ms * 1e3 / len(dom), 2), "launches_per_step": len(dom),
                      "flops_per_launch": round(dom_flops / len(dom)),
                      "frac_of_layer_roofline": round(roof_ms / dom_ms, 4),
-                     "traffic": traffic_per_launch(kern, wl.name, KERNEL_SOURCE[kern])},
+                     "traffic": traffic_per_launch(kern, wl.name, KERNEL_SOURCE[kern]),
+                     # the same launches' kernel time alone, from the committed rocprofv3
+                     # trace (avg_launch_us holds the gap between launches as well)
+                     "profile_kernel_us": traffic_per_launch(kern, wl.name, KERNEL_SOURCE[kern],
+                                                             "kernel µs per launch")},
     }
     del layers
     torch.cuda.empty_cache()
     return res
+
+
+def gemm_reference(torch, sa, wl):
+    """Context for the CONV figures: the vendor library's plain bf16 GEMM
+    (torch.matmul, i.e. hipBLASLt) on each layer's GEMM shape -- [N*P*Q, K]
+    times [K, M] with the im2col matrix already in memory (im2col not timed),
+    for the compacted (kept filters) and the dense matrix."""
+    kind, pct = wl.variants[0]
+    tot = {"compact": [0.0, 0.0], "dense": [0.0, 0.0]}
+    for li, L in enumerate(wl.layers):
+        npq = wl.batch * L.P * L.Q
+        m_c = wl.k_for(li, kind, pct) if kind == sa.FILTER else L.A
+        k_c = L.K if kind == sa.FILTER else wl.k_for(li, kind, pct)
+        for label, m, k in (("compact", m_c, k_c), ("dense", L.A, L.K)):
+            a = torch.randn(npq, k, device="cuda", dtype=torch.bfloat16)
+            b = torch.randn(m, k, device="cuda", dtype=torch.bfloat16)
+            bt = b.t()
+            t = _time(torch, lambda: torch.matmul(a, bt), reps=10, warm=3, trials=3)
+            tot[label][0] += 2.0 * npq * m * k
+            tot[label][1] += t["median_ms"] * 1e-3
+            del a, b, bt
+    torch.cuda.empty_cache()
+    return {f"{lab}_tflops": round(f / s_ / 1e12, 1) for lab, (f, s_) in tot.items()} | \
+        {f"{lab}_us": round(s_ * 1e6, 1) for lab, (f, s_) in tot.items()}
 
 
 def admm_warm(torch, sa, wl):

@@ -262,6 +262,11 @@ int structadmm_pack_nhwc(const float *X, int32_t N, int32_t Cin, int32_t H, int3
 
 /* ---- compacted CONV: structadmm_conv_fwd ----------------------------- */
 /*
+ * Section 3, "Combination of structured sparsities": the CONV lowered to a GEMM
+ * over the compacted weight matrix.  Pruning removes rows (filters) or
+ * columns (channels, filter shapes) of the [A, B*C*D] matrix; what remains is
+ * a smaller full GEMM with the same products and sums as the dense CONV with
+ * the pruned weights set to zero, on the kept output channels:
  * Y[n, p, q, o] = sum_j Wc_g[m, j] * X[n, p*stride - pad + c_j, q*stride - pad + d_j, col_ch[j]]
  * for conv group g, output channel o = sizes->row_offset[g] + m, (c_j, d_j) =
  * (col_tap[j] / D, col_tap[j] % D); zero outside the image (cross-correlation,
@@ -295,6 +300,11 @@ typedef struct sa_conv_desc {
  * Returns 0 for an invalid descriptor; structadmm_conv_fwd reports those. */
 size_t structadmm_conv_workspace(const sa_conv_desc *desc);
 
+/* Asynchronous on `stream`.  Returns SA_OK, or a negative code with the
+ * thread's message set (nothing enqueued): SA_E_ARG for shapes, sizes or
+ * pointers that do not fit the descriptor, SA_E_ALIGN for misaligned X / Y /
+ * scratch, SA_E_WORKSPACE when ws is smaller than structadmm_conv_workspace(),
+ * SA_E_UNSUPPORTED beyond the limits above, SA_E_HIP for a failed launch. */
 int structadmm_conv_fwd(const sa_conv_desc *desc, hipStream_t stream);
 
 /* Which kernels structadmm_conv_fwd takes for a descriptor (Section 3: the

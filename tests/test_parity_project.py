@@ -152,6 +152,44 @@ def test_project_alexnet_chain():
             assert np.count_nonzero(Z) > 0
 
 
+# (A, B, C, D, groups, kind, parent): the layer's input channels are the
+# parent layer's kept filters (parent A = groups * B), or unrestricted
+CHAIN_GRAPHS = {
+    # a branching chain of filter layers: two children of one mask, a
+    # grandchild, an independent layer between them, grouped convolutions
+    "branching": [(24, 6, 3, 3, 1, sa.FILTER, None), (16, 12, 3, 3, 2, sa.FILTER, 0),
+                  (20, 24, 1, 1, 1, sa.FILTER, 0), (12, 5, 3, 3, 1, sa.FILTER, None),
+                  (30, 8, 3, 3, 2, sa.FILTER, 1), (9, 30, 2, 3, 1, sa.FILTER, 4)],
+    # a chain with a channel-pruned child: projected level by level
+    "mixed": [(16, 4, 3, 3, 1, sa.FILTER, None), (12, 16, 3, 3, 1, sa.CHANNEL, 0),
+              (10, 12, 1, 1, 1, sa.FILTER, None), (8, 10, 3, 3, 1, sa.SHAPE, 2)],
+    # 40 layers in one chain: more layers than one chain-walk launch takes
+    "long": [(12, 3, 3, 3, 1, sa.FILTER, None)] + [(12, 12, 3, 3, 1, sa.FILTER, i) for i in range(39)],
+}
+
+
+@pytest.mark.parametrize("graph", sorted(CHAIN_GRAPHS))
+def test_project_chain_graphs(graph):
+    """Layers whose input channels are an earlier layer's kept filters, in
+    one call: masks, kept lists, Z, U, G and scores against the oracle run
+    layer by layer in dependency order."""
+    specs = CHAIN_GRAPHS[graph]
+    rng = np.random.default_rng(len(specs) * 7 + len(graph))
+    layers, refs = [], []
+    for i, (A, B, C, D, groups, kind, parent) in enumerate(specs):
+        W = (0.05 * rng.standard_normal((A, B, C, D))).astype(np.float32)
+        U = (0.01 * rng.standard_normal((A, B, C, D))).astype(np.float32)
+        G = n_groups(W.shape, kind)
+        k = max(1, G // 2 + (i % 3) - 1)
+        ref_in = refs[parent]["mask"] if parent is not None else None
+        gpu_in = layers[parent].mask if parent is not None else None
+        refs.append(oracle_ref(W, U, kind, k, groups, in_ch_mask=ref_in, rho=1e-3, fused=True))
+        layers.append(GpuLayer(W, U, kind, k, groups, in_ch_mask=gpu_in, rho=1e-3, fused=True))
+    got = run_project(layers)
+    for i, (g, r) in enumerate(zip(got, refs)):
+        check(g, r, specs[i][5], layers[i].k, True, f"{graph} layer {i}")
+
+
 @pytest.mark.parametrize("variant", range(9))
 def test_project_sweep_variants(variant):
     (wl, li, W, U, kind, k), = workload_layers("resnet50_s3_sweep", variant)
