@@ -944,13 +944,15 @@ def main():
 
 
 # bytes one launch of the direct / footprint CONV must move at least: the input
-# channels it references, the compacted weights and the output (bf16)
+# pixels its taps reach (every input channel; a strided kernel narrower than
+# its stride skips rows and columns), the compacted weights and the output (bf16)
 def layer_bytes(o):
     L = o.cfg
     N, H, W, Cx = o.Xp.shape
     m = sum(o.sizes_c.M[g] for g in range(o.sizes_c.groups))
     kk = sum(o.sizes_c.M[g] * o.sizes_c.K[g] for g in range(o.sizes_c.groups))
-    return 2 * N * H * W * Cx + 2 * kk + 2 * N * L.P * L.Q * m
+    rows, cols = min(H, L.P * L.C), min(W, L.Q * L.D)
+    return 2 * N * rows * cols * Cx + 2 * kk + 2 * N * L.P * L.Q * m
 
 
 def progress(msg):
@@ -1030,6 +1032,12 @@ def measure(torch, sa, wl, steps, warmup):
     dom_ms = sum(t_c[i] for i in dom)
     dom_flops = sum(layers[i].flops_c for i in dom)
     dom_tflops = dom_flops / (dom_ms * 1e-3) / 1e12
+    dom_bytes = sum(layer_bytes(layers[i]) for i in dom)
+    dom_gbps = dom_bytes / (dom_ms * 1e-3) / 1e9
+    # the kernel's bound: its launches' algorithmic flops per algorithmic byte
+    # against the ridge point of the two peaks (2.5 PFLOP/s / 8 TB/s = 312.5)
+    ridge = BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9)
+    hbm_bound = dom_flops / dom_bytes < ridge
     # per-layer roofline min(MFMA, AI * HBM) time over the measured time
     roof_ms = sum(max(layers[i].flops_c / (BF16_PEAK_TFLOPS * 1e12), layer_bytes(layers[i]) / (HBM_PEAK_GBS * 1e9))
                   for i in dom) * 1e3
@@ -1056,8 +1064,16 @@ def measure(torch, sa, wl, steps, warmup):
         "per_layer": per_layer,
         "compact_by_kernel": by_kernel,
         "roofline": {"kernel": f"{kern} (compacted CONVs of {len(dom)} of {len(layers)} layers)",
-                     "bound": "mfma", "achieved": round(dom_tflops, 2), "peak": BF16_PEAK_TFLOPS,
-                     "unit": "TFLOP/s", "frac": round(dom_tflops / BF16_PEAK_TFLOPS, 4),
+                     "bound": "hbm" if hbm_bound else "mfma",
+                     "achieved": round(dom_gbps, 1) if hbm_bound else round(dom_tflops, 2),
+                     "peak": HBM_PEAK_GBS if hbm_bound else BF16_PEAK_TFLOPS,
+                     "unit": "GB/s" if hbm_bound else "TFLOP/s",
+                     "frac": round(dom_gbps / HBM_PEAK_GBS if hbm_bound else dom_tflops / BF16_PEAK_TFLOPS, 4),
+                     "arithmetic_intensity_flop_per_byte": round(dom_flops / dom_bytes, 1),
+                     "ridge_flop_per_byte": round(ridge, 1),
+                     "achieved_tflops": round(dom_tflops, 2),
+                     "frac_of_bf16_peak": round(dom_tflops / BF16_PEAK_TFLOPS, 4),
+                     "algorithmic_bytes_per_launch": round(dom_bytes / len(dom)),
                      "avg_launch_us": round(dom_ms * 1e3 / len(dom), 2), "launches_per_step": len(dom),
                      "flops_per_launch": round(dom_flops / len(dom)),
                      "frac_of_layer_roofline": round(roof_ms / dom_ms, 4),
