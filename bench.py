@@ -18,13 +18,17 @@ Inputs are resident in HBM before the timed region.
 Output: one JSON line.  value = compacted-CONV TFLOP/s over the step's
 compacted convolutions (algorithmic flops 2*N*P*Q*sum_g M_g*K_g / their
 HIP-event time); speedup_vs_dense = dense CONV time / compacted CONV time;
-admm_gbps = algorithmic bytes of steps 1-2 / their time.  Each CONV is bracketed
-by HIP events on the stream it runs on (recorded without a system-scope
-fence, which would write back and invalidate the caches at every event); a
+admm_gbps = algorithmic bytes of steps 1-2 / their time.  HIP events on the
+stream the work runs on (recorded without a system-scope fence, which would
+write back and invalidate the caches at every event) bracket the ADMM calls,
+the packs, the block of 53 compacted CONVs and the block of 53 dense CONVs;
+a few extra steps bracket every CONV for the per-layer breakdown (each
+event pair adds its own gap, so those spans sum above the block spans).  A
 spin kernel ahead of each timed block lets the host enqueue the block before
-the GPU reaches it, so the events measure the kernels rather than host gaps.  ms_per_step is the wall time of a
-step: the GPU time of its parts, the host-side synchronisations of the
-compactions, and the spins (reported separately as spin_ms_per_step).
+the GPU reaches it, so the events measure the kernels rather than host
+gaps.  ms_per_step is the wall time of a step: the GPU time of its parts,
+the host-side synchronisations of the compactions, and the spins (reported
+separately as spin_ms_per_step).
 """
 from __future__ import annotations
 
@@ -162,11 +166,14 @@ def setup(torch, sa, wl):
 
 
 def run_step(torch, sa, wl, layers, ws, cws, ev, record):
-    """One pass of the hot path; returns per-part event pairs when record."""
+    """One pass of the hot path; returns event pairs around its parts:
+    record = "blocks" brackets the ADMM calls, the packs, all compacted CONVs
+    and all dense CONVs (the timed steps); "layers" brackets every CONV
+    (the per-layer breakdown); False records nothing."""
     marks = {}
 
-    def mark(name):
-        if record:
+    def mark(name, level="blocks"):
+        if record and (level == "blocks" or record == "layers"):
             e = TimingEvent()
             e.record(torch)
             marks.setdefault(name, []).append(e)
@@ -214,16 +221,20 @@ def run_step(torch, sa, wl, layers, ws, cws, ev, record):
     for o in layers:
         sa.pack_nhwc(o.X, out=o.Xp)
     mark("pack1")
+    mark("c_all0")
     for i, (o, (c, d)) in enumerate(zip(layers, comp)):
         L = o.cfg
-        mark(f"c{i}a")
+        mark(f"c{i}a", "layers")
         sa.conv_fwd(o.Xp, c[0], c[2], c[3], c[4], L.C, L.D, L.stride, L.pad, Y=o.Yc, ws=o.cvws)
-        mark(f"c{i}b")
+        mark(f"c{i}b", "layers")
+    mark("c_all1")
+    mark("d_all0")
     for i, (o, (c, d)) in enumerate(zip(layers, comp)):
         L = o.cfg
-        mark(f"d{i}a")
+        mark(f"d{i}a", "layers")
         sa.conv_fwd(o.Xp, d[0], d[2], d[3], d[4], L.C, L.D, L.stride, L.pad, Y=o.Yd, ws=o.cvws)
-        mark(f"d{i}b")
+        mark(f"d{i}b", "layers")
+    mark("d_all1")
     ev["enqueue_s"] = time.perf_counter() - t_enq
     return marks
 
@@ -918,6 +929,8 @@ def main():
         "dense_conv_tflops": main_res["dense_tflops"],
         "compact_conv_us": main_res["compact_us"],
         "dense_conv_us": main_res["dense_us"],
+        "compact_conv_us_layer_events": main_res["compact_us_layer_events"],
+        "dense_conv_us_layer_events": main_res["dense_us_layer_events"],
         "admm_gbps": main_res["admm_gbps"],
         "admm_us": main_res["admm_us"],
         "admm_note": "fused projection (20 B/weight) + per-SGD-step gradient (16 B/weight) of all layers, "
@@ -993,7 +1006,7 @@ def measure(torch, sa, wl, steps, warmup):
     # untimed steps: size the output and scratch buffers, then the spin ahead
     # of the pack + CONV block from the host's enqueue time of that block
     for _ in range(max(1, warmup)):
-        run_step(torch, sa, wl, layers, ws, cws, ev, record=True)
+        run_step(torch, sa, wl, layers, ws, cws, ev, record="blocks")
         torch.cuda.synchronize()
         lead_us = min(LEAD_CONV_MAX_US, 1.3 * ev["enqueue_s"] * 1e6 + 200)
         ev["lead_conv"] = lead_cycles(torch, lead_us)
@@ -1004,17 +1017,25 @@ def measure(torch, sa, wl, steps, warmup):
     t0 = time.perf_counter()
     all_marks = []
     for _ in range(steps):
-        all_marks.append(run_step(torch, sa, wl, layers, ws, cws, ev, record=True))
+        all_marks.append(run_step(torch, sa, wl, layers, ws, cws, ev, record="blocks"))
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    # the per-layer breakdown: the same steps with every CONV bracketed (each
+    # event pair adds its own gap, so these spans sum above the block spans)
+    nl = max(2, steps // 4)
+    progress(f"{wl.name}: {nl} steps with per-layer events")
+    layer_marks = [run_step(torch, sa, wl, layers, ws, cws, ev, record="layers") for _ in range(nl)]
+    torch.cuda.synchronize()
 
     def span(m, a, b):
         return sum(x.elapsed_time(y) for x, y in zip(m[a], m[b]))  # ms
 
     t_admm = sum(span(m, "admm0", "admm1") for m in all_marks) / steps
     t_pack = sum(span(m, "pack0", "pack1") for m in all_marks) / steps
-    t_c = [sum(span(m, f"c{i}a", f"c{i}b") for m in all_marks) / steps for i in range(len(layers))]
-    t_d = [sum(span(m, f"d{i}a", f"d{i}b") for m in all_marks) / steps for i in range(len(layers))]
+    t_cblk = sum(span(m, "c_all0", "c_all1") for m in all_marks) / steps
+    t_dblk = sum(span(m, "d_all0", "d_all1") for m in all_marks) / steps
+    t_c = [sum(span(m, f"c{i}a", f"c{i}b") for m in layer_marks) / nl for i in range(len(layers))]
+    t_d = [sum(span(m, f"d{i}a", f"d{i}b") for m in layer_marks) / nl for i in range(len(layers))]
     flops_c = sum(o.flops_c for o in layers)
     flops_d = sum(o.flops_d for o in layers)
     n_el = sum(o.cfg.n for o in layers)
@@ -1050,17 +1071,19 @@ def measure(torch, sa, wl, steps, warmup):
                   "speedup": round(td / tc, 2)}
                  for o, tc, td in zip(layers, t_c, t_d)]
     res = {
-        "compact_tflops": round(flops_c / (sum(t_c) * 1e-3) / 1e12, 3),
-        "dense_tflops": round(flops_d / (sum(t_d) * 1e-3) / 1e12, 3),
-        "speedup_vs_dense": round(sum(t_d) / sum(t_c), 3),
-        "compact_us": round(sum(t_c) * 1e3, 1),
-        "dense_us": round(sum(t_d) * 1e3, 1),
+        "compact_tflops": round(flops_c / (t_cblk * 1e-3) / 1e12, 3),
+        "dense_tflops": round(flops_d / (t_dblk * 1e-3) / 1e12, 3),
+        "speedup_vs_dense": round(t_dblk / t_cblk, 3),
+        "compact_us": round(t_cblk * 1e3, 1),
+        "dense_us": round(t_dblk * 1e3, 1),
+        "compact_us_layer_events": round(sum(t_c) * 1e3, 1),
+        "dense_us_layer_events": round(sum(t_d) * 1e3, 1),
         "admm_gbps": round(admm_bytes / (t_admm * 1e-3) / 1e9, 1),
         "admm_us": round(t_admm * 1e3, 2),
         "pack_us": round(t_pack * 1e3, 1),
         "ms_per_step": round(wall * 1e3 / steps, 4),
         "spin_ms_per_step": round(spin_ms, 3),
-        "gpu_ms_per_step": round(t_admm + t_pack + sum(t_c) + sum(t_d), 4),
+        "gpu_ms_per_step": round(t_admm + t_pack + t_cblk + t_dblk, 4),
         "per_layer": per_layer,
         "compact_by_kernel": by_kernel,
         "roofline": {"kernel": f"{kern} (compacted CONVs of {len(dom)} of {len(layers)} layers)",
