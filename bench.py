@@ -90,6 +90,12 @@ class Layer:
     pass
 
 
+def kept_k(sizes, g):
+    """Kept columns of conv group g (the compaction's alignment columns, +0,
+    are not algorithmic work)."""
+    return sizes.K[g] - sizes.kpad[g]
+
+
 class TimingEvent:
     """A HIP timing event recorded without the system-scope fence
     (hipEventDisableSystemFence): torch's events write back and invalidate the
@@ -200,8 +206,8 @@ def run_step(torch, sa, wl, layers, ws, cws, ev, record):
         if o.Yc is None:
             o.Yc = torch.empty(sa.conv_out_shape(*o.Xp.shape[:3], L.C, L.D, L.stride, L.pad, sizes),
                                dtype=torch.uint16, device="cuda")
-            o.flops_c = 2 * wl.batch * L.P * L.Q * sum(sizes.M[g] * sizes.K[g] for g in range(sizes.groups))
-            o.flops_d = 2 * wl.batch * L.P * L.Q * sum(sized.M[g] * sized.K[g] for g in range(sized.groups))
+            o.flops_c = 2 * wl.batch * L.P * L.Q * sum(sizes.M[g] * kept_k(sizes, g) for g in range(sizes.groups))
+            o.flops_d = 2 * wl.batch * L.P * L.Q * sum(sized.M[g] * kept_k(sized, g) for g in range(sized.groups))
             o.sizes_c = sizes
             o.plan_c = sa.conv_plan(o.Xp, sizes, L.C, L.D, L.stride, L.pad)
         # scratch for groups whose im2col rows are gathered first; the kept
@@ -335,10 +341,10 @@ def conv_only(args):
             sa.conv_fwd(o.Xp, c[0], c[2], c[3], c[4], L.C, L.D, L.stride, L.pad, Y=Y, ws=cv)
         torch.cuda.synchronize()
         sizes = c[4]
-        fl = 2 * wl.batch * L.P * L.Q * sum(sizes.M[g] * sizes.K[g] for g in range(sizes.groups))
+        fl = 2 * wl.batch * L.P * L.Q * sum(sizes.M[g] * kept_k(sizes, g) for g in range(sizes.groups))
         print(json.dumps({"layer": i, "name": L.name, "kernel": kern, "plan": plan, "flops": fl,
                           "bytes": layer_bytes(o), "M": [sizes.M[g] for g in range(sizes.groups)],
-                          "K": [sizes.K[g] for g in range(sizes.groups)], "launches": args.reps}), flush=True)
+                          "K": [kept_k(sizes, g) for g in range(sizes.groups)], "launches": args.reps}), flush=True)
 
 
 def copy_probe(mib):
@@ -474,7 +480,7 @@ def suite_tables(torch, sa):
                 torch.cuda.synchronize()
                 tm = _time(torch, conv)
             best = min(td["median_ms"], tm["median_ms"])
-            fc = 2 * L.P * L.Q * sum(sz.M[g] * sz.K[g] for g in range(sz.groups))
+            fc = 2 * L.P * L.Q * sum(sz.M[g] * kept_k(sz, g) for g in range(sz.groups))
             rows_out.append({"layer": L.name, "row_sparsity_pct": rs, "column_sparsity_pct": cs,
                              "kept_rows": [sz.M[g] for g in range(sz.groups)], "kept_cols": sz.K[0],
                              "compact_us": round(tc["median_ms"] * 1e3, 2), "dense_us": round(td["median_ms"] * 1e3, 2),
@@ -725,8 +731,8 @@ def suite_conv(torch, sa, wl, variant, layer_ids=None):
         xb = X.to(torch.bfloat16)
         wb = dZ.to(torch.bfloat16)
         tm = _time(torch, lambda: F.conv2d(xb, wb, stride=L.stride, padding=L.pad, groups=L.groups), reps=10)
-        fc = 2 * wl.batch * L.P * L.Q * sum(sz.M[g] * sz.K[g] for g in range(sz.groups))
-        fd = 2 * wl.batch * L.P * L.Q * sum(szd.M[g] * szd.K[g] for g in range(szd.groups))
+        fc = 2 * wl.batch * L.P * L.Q * sum(sz.M[g] * kept_k(sz, g) for g in range(sz.groups))
+        fd = 2 * wl.batch * L.P * L.Q * sum(szd.M[g] * kept_k(szd, g) for g in range(szd.groups))
         best_dense = min(td["median_ms"], tm["median_ms"])
         out.append({"layer": L.name, "compact_us": round(tc["median_ms"] * 1e3, 1),
                     "dense_us": round(td["median_ms"] * 1e3, 1), "miopen_dense_us": round(tm["median_ms"] * 1e3, 1),
@@ -963,7 +969,7 @@ def layer_bytes(o):
     L = o.cfg
     N, H, W, Cx = o.Xp.shape
     m = sum(o.sizes_c.M[g] for g in range(o.sizes_c.groups))
-    kk = sum(o.sizes_c.M[g] * o.sizes_c.K[g] for g in range(o.sizes_c.groups))
+    kk = sum(o.sizes_c.M[g] * kept_k(o.sizes_c, g) for g in range(o.sizes_c.groups))
     rows, cols = min(H, L.P * L.C), min(W, L.Q * L.D)
     return 2 * N * rows * cols * Cx + 2 * kk + 2 * N * L.P * L.Q * m
 

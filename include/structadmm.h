@@ -209,6 +209,15 @@ int structadmm_sgd_step(const sa_sgd_desc *layers, int n_layers, hipStream_t str
  * gc*B + b among the channels with in_ch_mask set (the input then holds only
  * those channels, ascending).  row_idx lists the kept filters (the output
  * channel order of structadmm_conv_fwd).
+ * Alignment columns: when the input is channel-compacted to a multiple of 8
+ * channels and a group keeps every tap of one run of consecutive input
+ * positions that does not start and end on a multiple of 8, the group's
+ * columns are widened to the enclosing 8-aligned window of positions when it
+ * is at most 1.5 times the run: the window's other positions (channels of a
+ * neighbouring group) become columns whose entries are +0 (kpad counts them),
+ * so the run is whole 16-byte vectors of every pixel and the CONV takes its
+ * direct kernels.  Their products are +0 for finite inputs, so the CONV's
+ * result is that of the kept columns alone.
  * Masks are byte arrays (0 = pruned) such as structadmm_project's mask.
  * Synchronises with the host and fills *sizes.
  */
@@ -247,6 +256,9 @@ typedef struct sa_compact_sizes {
      * (ch_span = 0 when the group has no column). */
     int32_t ch_lo[SA_MAX_CONV_GROUPS];
     int32_t ch_span[SA_MAX_CONV_GROUPS];
+    /* Of the K[gc] columns, the number added for alignment (see below); the
+     * kept columns are K[gc] - kpad[gc]. */
+    int32_t kpad[SA_MAX_CONV_GROUPS];
 } sa_compact_sizes;
 
 int structadmm_compact(const sa_compact_desc *desc, sa_compact_sizes *sizes, hipStream_t stream);

@@ -69,13 +69,14 @@ class CompactSizes(ctypes.Structure):
                 ("ldk", ctypes.c_int32 * _G), ("wc_offset", ctypes.c_int64 * _G),
                 ("row_offset", ctypes.c_int32 * _G), ("col_offset", ctypes.c_int32 * _G),
                 ("run", ctypes.c_int32 * _G), ("run_base", ctypes.c_int32 * _G),
-                ("ch_lo", ctypes.c_int32 * _G), ("ch_span", ctypes.c_int32 * _G)]
+                ("ch_lo", ctypes.c_int32 * _G), ("ch_span", ctypes.c_int32 * _G),
+                ("kpad", ctypes.c_int32 * _G)]
 
     def as_dict(self):
         g = self.groups
         return {k: list(getattr(self, k))[:g] for k in
                 ("M", "K", "ldk", "wc_offset", "row_offset", "col_offset", "run", "run_base",
-                 "ch_lo", "ch_span")}
+                 "ch_lo", "ch_span", "kpad")}
 
 
 class ConvDesc(ctypes.Structure):

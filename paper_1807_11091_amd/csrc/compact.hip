@@ -26,7 +26,7 @@ struct CompArgs {
     const uint8_t *row_mask, *col_mask, *chan_mask, *in_ch_mask;
     uint16_t *Wc;
     int32_t *row_idx, *col_ch, *col_tap;
-    int32_t *counts;  // ws: [groups][kCS] = M, K, run, run_base, ch_lo, ch_span
+    int32_t *counts;  // ws: [groups][kCS] = M, K, run, run_base, ch_lo, ch_span, kpad, run offset in the window
     int32_t A, B, C, D, groups, in_compacted;
 };
 
@@ -49,7 +49,10 @@ __device__ inline int in_position(const CompArgs &a, int full) {
 
 // Per conv group: M (kept rows), K (kept columns), the span of input channels
 // the kept columns read and, when every tap keeps the same channels and their
-// input positions are consecutive, that channel run.
+// input positions are consecutive, that channel run -- for a channel-compacted
+// input of a multiple of 8 channels widened to its enclosing 8-aligned window
+// of positions when that is at most 1.5 times the run (the added positions
+// become +0 columns).
 __global__ __launch_bounds__(kCompThreads) void k_compact_count(CompArgs a) {
     __shared__ uint32_t tmp[kCompThreads / kWave + 1];
     __shared__ int s_first, s_last, s_cfirst, s_clast;
@@ -81,12 +84,17 @@ __global__ __launch_bounds__(kCompThreads) void k_compact_count(CompArgs a) {
             atomicMax(&s_last, b);
         }
     }
-    uint32_t tot_m, tot_k, tot_b;
+    // channels of the compacted input (every set bit of in_ch_mask)
+    uint32_t ncx_part = 0;
+    if (a.in_compacted)
+        for (int c = threadIdx.x; c < a.groups * a.B; c += kCompThreads) ncx_part += a.in_ch_mask[c] != 0;
+    uint32_t tot_m, tot_k, tot_b, ncx;
     block_excl_scan(m, tmp, &tot_m);
     block_excl_scan(kc, tmp, &tot_k);
     block_excl_scan(nb, tmp, &tot_b);
+    block_excl_scan(ncx_part, tmp, &ncx);
     if (threadIdx.x == 0) {
-        int run = 0, base = 0;
+        int run = 0, base = 0, kpad = 0, roff = 0;
         if (!a.col_mask && tot_b > 0) {
             int p0 = in_position(a, gc * a.B + s_first);
             int p1 = in_position(a, gc * a.B + s_last);
@@ -100,14 +108,32 @@ __global__ __launch_bounds__(kCompThreads) void k_compact_count(CompArgs a) {
             clo = in_position(a, gc * a.B + s_cfirst);
             cspan = in_position(a, gc * a.B + s_clast) - clo + 1;
         }
+        if (run > 0 && a.in_compacted && ((base | run) & 7)) {
+            const int lo = base & ~7, hi = (base + run + 7) & ~7;
+            if ((ncx & 7) == 0 && hi <= (int)ncx && 2 * (hi - lo) <= 3 * run) {
+                kpad = (hi - lo - run) * taps;
+                roff = base - lo;
+                tot_k += (uint32_t)kpad;
+                run = hi - lo;
+                base = lo;
+                clo = lo;
+                cspan = hi - lo;
+            }
+        }
         a.counts[kCS * gc + 0] = (int)tot_m;
         a.counts[kCS * gc + 1] = (int)tot_k;
         a.counts[kCS * gc + 2] = run;
         a.counts[kCS * gc + 3] = base;
         a.counts[kCS * gc + 4] = clo;
         a.counts[kCS * gc + 5] = cspan;
+        a.counts[kCS * gc + 6] = kpad;
+        a.counts[kCS * gc + 7] = roff;
     }
 }
+
+// Column-table entry of an alignment column: input position p, encoded
+// below zero until k_compact_inpos (which maps kept channels to positions).
+__device__ inline int32_t pad_code(int p) { return -p - 1; }
 
 // Column tables (full input channel for now) and kept rows, concatenated over groups.
 __global__ __launch_bounds__(kCompThreads) void k_compact_tables(CompArgs a) {
@@ -123,6 +149,21 @@ __global__ __launch_bounds__(kCompThreads) void k_compact_tables(CompArgs a) {
     // consecutive channels of one tap per load); any other column set
     // channel-major, so that every channel range is one range of columns
     const bool tap_major = a.counts[kCS * gc + 2] > 0;
+    // a widened run: kept channel r of tap t goes to column t * run + roff + r,
+    // the window's other positions to +0 alignment columns
+    const int kpad = a.counts[kCS * gc + 6];
+    const int wrun = a.counts[kCS * gc + 2], roff = a.counts[kCS * gc + 7];
+    const int krun = kpad > 0 ? wrun - kpad / taps : 0;  // kept channels per tap
+    if (kpad > 0) {
+        const int wbase = a.counts[kCS * gc + 3];
+        for (int idx = threadIdx.x; idx < taps * wrun; idx += kCompThreads) {
+            const int t = idx / wrun, q = idx - t * wrun;
+            if (q < roff || q >= roff + krun) {
+                a.col_ch[col_off + idx] = pad_code(wbase + q);
+                a.col_tap[col_off + idx] = t;
+            }
+        }
+    }
     uint32_t running = 0;
     const int64_t ncand = (int64_t)taps * a.B;
     for (int64_t base = 0; base < ncand; base += kCompThreads) {
@@ -142,8 +183,10 @@ __global__ __launch_bounds__(kCompThreads) void k_compact_tables(CompArgs a) {
         uint32_t tot;
         uint32_t pos = running + block_excl_scan(keep ? 1u : 0u, tmp, &tot);
         if (keep) {
-            a.col_ch[col_off + pos] = gc * a.B + b;
-            a.col_tap[col_off + pos] = t;
+            // tap-major with every tap keeping the same channels: pos = t * krun + rank
+            const int j = kpad > 0 ? t * wrun + roff + ((int)pos - t * krun) : (int)pos;
+            a.col_ch[col_off + j] = gc * a.B + b;
+            a.col_tap[col_off + j] = t;
         }
         running += tot;
     }
@@ -177,7 +220,7 @@ __global__ __launch_bounds__(256) void k_compact_gather(CompArgs a) {
     uint16_t *dst = a.Wc + wc_off + (int64_t)m * ldk;
     for (int j = threadIdx.x; j < ldk; j += blockDim.x) {
         uint16_t v = 0;
-        if (j < K) {
+        if (j < K && a.col_ch[col_off + j] >= 0) {  // alignment columns hold +0
             const int b = a.col_ch[col_off + j] - gc * a.B;
             const int t = a.col_tap[col_off + j];
             const int c = t / a.D, d = t - (t / a.D) * a.D;
@@ -204,7 +247,7 @@ __global__ __launch_bounds__(kCompThreads) void k_compact_inpos(CompArgs a, int 
     __syncthreads();
     for (int j = threadIdx.x; j < total_cols; j += kCompThreads) {
         const int full = a.col_ch[j];
-        a.col_ch[j] = (full >= 0 && full < nch) ? pos[full] : 0;
+        a.col_ch[j] = full < 0 ? -full - 1 : (full < nch ? pos[full] : 0);  // alignment columns: their position
     }
 }
 
@@ -356,6 +399,7 @@ extern "C" int structadmm_compact(const sa_compact_desc *desc, sa_compact_sizes 
         sizes->run_base[g] = counts[kCS * g + 3];
         sizes->ch_lo[g] = counts[kCS * g + 4];
         sizes->ch_span[g] = counts[kCS * g + 5];
+        sizes->kpad[g] = counts[kCS * g + 6];
         sizes->wc_offset[g] = wc_off;
         sizes->row_offset[g] = row_off;
         sizes->col_offset[g] = col_off;

@@ -21,14 +21,6 @@ pytestmark = pytest.mark.gpu
 TOL = 2e-2
 
 
-def strip_padding(Wc, sizes):
-    out = []
-    for g in range(sizes.groups):
-        M, K, ldk, off = sizes.M[g], sizes.K[g], sizes.ldk[g], sizes.wc_offset[g]
-        out.append(Wc[off: off + M * ldk].reshape(M, ldk)[:, :K].ravel())
-    return np.concatenate(out) if out else np.zeros(0, np.uint16)
-
-
 def gpu_compact(Z, groups, row_mask=None, col_mask=None, in_ch_mask=None, in_compacted=False):
     t = torch()
     Wc, row_idx, col_ch, col_tap, sizes = sa.compact(Z, groups, row_mask=row_mask, col_mask=col_mask,
@@ -42,10 +34,14 @@ def check_compact(gpu, ref):
     their (input channel, tap) pair, since the library may order a group's
     columns differently from the oracle's ascending GEMM column index (any
     order gives the same GEMM): the kept pairs must be the same set, and every
-    GPU column must equal, bit for bit, the oracle's column of its pair."""
+    GPU column must equal, bit for bit, the oracle's column of its pair.  The
+    library's alignment columns (kpad of a group, on a channel-compacted
+    input) are further pairs of the group's 8-aligned window whose entries are
+    all +0, so that they add nothing to the CONV."""
     Wc, row_idx, col_ch, col_tap, sizes = gpu
     assert list(sizes.M)[: sizes.groups] == list(ref["M"])
-    assert list(sizes.K)[: sizes.groups] == list(ref["K"])
+    kpad = list(sizes.kpad)[: sizes.groups]
+    assert [k - p for k, p in zip(list(sizes.K)[: sizes.groups], kpad)] == list(ref["K"])
     nr = int(ref["M"].sum())
     assert np.array_equal(row_idx.cpu().numpy()[:nr], ref["row_idx"])
     full = Wc.cpu().numpy()
@@ -53,20 +49,28 @@ def check_compact(gpu, ref):
     woff = coff = 0
     for g in range(sizes.groups):
         M, K, ldk, off = sizes.M[g], sizes.K[g], sizes.ldk[g], sizes.wc_offset[g]
-        goff = sizes.col_offset[g]
+        goff, Kr = sizes.col_offset[g], K - kpad[g]
         mat = full[off: off + M * ldk].reshape(M, ldk)
         # padding columns hold +0
         assert not np.any(mat[:, K:])
-        rch, rtap = ref["col_ch"][coff: coff + K], ref["col_tap"][coff: coff + K]
+        rch, rtap = ref["col_ch"][coff: coff + Kr], ref["col_tap"][coff: coff + Kr]
         rkey = {(int(c), int(t)): j for j, (c, t) in enumerate(zip(rch, rtap))}
-        assert len(rkey) == K
+        assert len(rkey) == Kr
         gkey = [(int(c), int(t)) for c, t in zip(gch[goff: goff + K], gtap[goff: goff + K])]
-        assert len(set(gkey)) == K and set(gkey) == set(rkey)
-        perm = np.array([rkey[k] for k in gkey], dtype=np.int64)
-        rmat = ref["Wc"][woff: woff + M * K].reshape(M, K)
-        assert np.array_equal(mat[:, :K], rmat[:, perm])
-        woff += M * K
-        coff += K
+        assert len(set(gkey)) == K and set(rkey) <= set(gkey)
+        kept = np.array([k in rkey for k in gkey], dtype=bool)
+        perm = np.array([rkey[k] for k in gkey if k in rkey], dtype=np.int64)
+        rmat = ref["Wc"][woff: woff + M * Kr].reshape(M, Kr)
+        assert np.array_equal(mat[:, :K][:, kept], rmat[:, perm])
+        if kpad[g]:
+            lo, run = sizes.run_base[g], sizes.run[g]
+            assert lo % 8 == 0 and run % 8 == 0 and K == run * (K // run)
+            extra = [k for k in gkey if k not in rkey]
+            assert all(lo <= c < lo + run for c, _ in extra)
+            assert {(c, t) for c in range(lo, lo + run) for t in range(K // run)} == set(gkey)
+            assert not np.any(mat[:, :K][:, ~kept])
+        woff += M * Kr
+        coff += Kr
 
 
 def conv_case(N, Cin, H, Wd, A, C, D, stride, pad, groups, kind, keep, seed, dense_too=True, dead_lo=0,
@@ -261,6 +265,46 @@ def test_compact_chain_input_positions():
     Xb = oracle.pack(X, keep=prev)
     assert bitwise_equal(Xp.cpu().numpy(), Xb.transpose(0, 2, 3, 1))
     Wc, ri, cc, ct, sizes = gc
+    Y = sa.conv_fwd(Xp, Wc, cc, ct, sizes, C, D, 1, 1)
+    Yr = oracle.conv(Xb, rc, C, D, 1, 1)
+    assert maxabs_over_rms(bf16_bits_to_f64(Y.cpu().numpy()), Yr) <= TOL
+
+
+@pytest.mark.parametrize("kept, kpad_expect", [
+    ((20, 20), (4, 4)),      # both groups widen to 8-aligned windows of 24 positions
+    ((20, 3, 17), (4, 0, 7)),  # group 1: a window of 8 over 3 kept is too wide
+    ((20, 3, 13), (0, 0, 0)),  # 36 input channels: no direct kernel, no widening
+    ((16, 8), (0, 0)),       # already aligned
+])
+def test_compact_alignment_columns(kept, kpad_expect):
+    """Alignment columns on a channel-compacted input: group g keeps the
+    channels kept[g] of the previous layer; the library widens unaligned runs
+    to 8-aligned windows (+0 columns, kpad_expect[g] positions per tap), and
+    the CONV over them is the CONV of the kept columns."""
+    rng = np.random.default_rng(sum(kept))
+    groups, B, A, C, D = len(kept), 32, 16 * len(kept), 3, 3
+    prev = np.zeros(groups * B, np.uint8)
+    for g, n in enumerate(kept):
+        prev[g * B + rng.choice(B, size=n, replace=False)] = 1
+    W = (0.05 * rng.standard_normal((A, B, C, D))).astype(np.float32)
+    U = np.zeros_like(W)
+    ref = oracle.project(W, U, sa.FILTER, 8 * groups, groups, in_ch_mask=prev)
+    L = GpuLayer(W, U, sa.FILTER, 8 * groups, groups, in_ch_mask=prev)
+    got = run_project([L])[0]
+    assert np.array_equal(got["mask"], ref["mask"])
+    gc = sa.compact(L.Z, groups, row_mask=L.mask, in_ch_mask=L.in_ch_mask, in_compacted=True)
+    rc = oracle.compact(ref["Z"], groups, row_mask=ref["mask"], in_ch_mask=prev, in_compacted=True)
+    check_compact(gc, rc)
+    Wc, ri, cc, ct, sizes = gc
+    assert [sizes.kpad[g] for g in range(groups)] == [p * C * D for p in kpad_expect]
+    X = rng.standard_normal((3, groups * B, 10, 11)).astype(np.float32)
+    Xp = sa.pack_nhwc(to_dev(X), keep=L.in_ch_mask)
+    plan = sa.conv_plan(Xp, sizes, C, D, 1, 1)
+    for g in range(groups):
+        aligned = sum(kept) % 8 == 0 and kept[g] % 8 == 0 and sum(kept[:g]) % 8 == 0
+        if sizes.M[g] > 0 and (kpad_expect[g] or aligned):
+            assert plan["path"][g] in (sa.CONV_DIRECT, sa.CONV_DIRECT_IG), (g, plan)
+    Xb = oracle.pack(X, keep=prev)
     Y = sa.conv_fwd(Xp, Wc, cc, ct, sizes, C, D, 1, 1)
     Yr = oracle.conv(Xb, rc, C, D, 1, 1)
     assert maxabs_over_rms(bf16_bits_to_f64(Y.cpu().numpy()), Yr) <= TOL
