@@ -166,7 +166,10 @@ def setup(torch, sa, wl):
         o.Yc = None
         o.cvws = None
         o.Yd = torch.empty((N, L.P, L.Q, L.A), dtype=torch.uint16, device=dev)
-        o.proj = sa.ProjectLayer(o.W, o.U, o.Z, o.mask, o.kept, kind, k, L.groups, None, None, wl.rho, o.G)
+        # the filter + channel chain: the input channels are the previous
+        # layer's kept filters
+        o.in_mask = layers[-1].mask if (wl.chain and layers) else None
+        o.proj = sa.ProjectLayer(o.W, o.U, o.Z, o.mask, o.kept, kind, k, L.groups, o.in_mask, None, wl.rho, o.G)
         layers.append(o)
     return layers
 
@@ -193,6 +196,8 @@ def run_step(torch, sa, wl, layers, ws, cws, ev, record):
     sa.project([o.proj for o in layers], ws, descs=ev["pdescs"])
     sa.dual_update(None, descs=ev["ddescs"])
     mark("admm1")
+    if any(o.in_mask is not None for o in layers):
+        raise SystemExit("the timed step runs workloads without a filter + channel chain (--suite times the chain)")
     # compaction synchronises with the host (it returns the sizes), so every
     # layer is compacted first and the CONVs are then enqueued back to back
     comp = []
@@ -323,13 +328,18 @@ def conv_only(args):
         o, L = layers[i], layers[i].cfg
         rows = o.mask if (o.kind == sa.FILTER and not args.dense) else None
         cols = o.mask if (o.kind == sa.SHAPE and not args.dense) else None
-        c = sa.compact(o.Z, L.groups, row_mask=rows, col_mask=cols, ws=cws)
+        inm = None if args.dense else o.in_mask
+        c = sa.compact(o.Z, L.groups, row_mask=rows, col_mask=cols, in_ch_mask=inm, in_compacted=inm is not None,
+                       ws=cws)
         sizes = o.sizes_c = c[4]
+        if inm is not None:  # the input holds the previous layer's kept filters only
+            o.Xp = sa.pack_nhwc(o.X, keep=inm)
+        else:
+            sa.pack_nhwc(o.X, out=o.Xp)
         plan = sa.conv_plan(o.Xp, sizes, L.C, L.D, L.stride, L.pad)
         kern = kernel_of(sa, plan)
         if args.kernel is not None and kern != args.kernel:
             continue
-        sa.pack_nhwc(o.X, out=o.Xp)
         Y = torch.empty(sa.conv_out_shape(*o.Xp.shape[:3], L.C, L.D, L.stride, L.pad, sizes),
                         dtype=torch.uint16, device="cuda")
         cv = torch.empty(max(256, sa.conv_workspace(o.Xp, sizes, L.C, L.D, L.stride, L.pad)),

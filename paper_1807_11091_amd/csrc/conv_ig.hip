@@ -722,8 +722,9 @@ int launch_tile(int t, const IgArgs &a, hipStream_t stream) {
 
 }  // namespace
 
-// Tile shape for a launch (measured on gfx950 over the ResNet-50 layers): the
-// least padded filter work first (rows pad to the tile's BM, within 4%).
+// Tile shape for a launch (measured on gfx950 over the ResNet-50 and AlexNet
+// layers): the least padded filter work first (rows pad to the tile's BM,
+// within 4%), not counting 32-filter tiles when a group keeps more filters.
 // Among those, a tile whose filter count covers every group's kept filters
 // (its output rows are whole: one contiguous range of Y), else the smallest
 // tile of at least 64 filters; two pixel fragments per wavefront, four
@@ -737,8 +738,10 @@ int ig_pick(const IgArgs &a) {
         const int BM = kTiles[t].WM * kTiles[t].MT * 16;
         int64_t w = 0;
         for (int i = 0; i < a.ngroups; ++i) w += (int64_t)(a.g[i].M + BM - 1) / BM * BM;
-        work[t] = w;
-        if (least < 0 || w < least) least = w;
+        // 32-filter tiles re-read every pixel's columns once per 32 filters:
+        // the slowest shape on every layer measured unless no group has more
+        work[t] = BM < 48 && maxM > BM ? -1 : w;
+        if (work[t] >= 0 && (least < 0 || w < least)) least = w;
     }
     auto score = [&](int t) {  // larger is better
         const Tile &T = kTiles[t];
@@ -751,7 +754,7 @@ int ig_pick(const IgArgs &a) {
     };
     int best = -1;
     for (int t = 0; t < kNumTiles; ++t) {
-        if (work[t] * 100 > least * 104) continue;
+        if (work[t] < 0 || work[t] * 100 > least * 104) continue;
         if (best < 0 || score(t) > score(best)) best = t;
     }
     return best;
