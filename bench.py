@@ -90,6 +90,14 @@ class Layer:
     pass
 
 
+def pitch8(sizes):
+    """Output row pitch of a compacted CONV: its kept filters rounded up to a
+    multiple of 8 channels, so that every output row starts on a 16-byte
+    boundary (the padding channels are not part of the result)."""
+    cy = sum(sizes.M[g] for g in range(sizes.groups))
+    return (cy + 7) // 8 * 8
+
+
 def kept_k(sizes, g):
     """Kept columns of conv group g (the compaction's alignment columns, +0,
     are not algorithmic work)."""
@@ -209,8 +217,8 @@ def run_step(torch, sa, wl, layers, ws, cws, ev, record):
         d = sa.compact(o.Z, L.groups, ws=cws, out=o.dense_out)
         sizes, sized = c[4], d[4]
         if o.Yc is None:
-            o.Yc = torch.empty(sa.conv_out_shape(*o.Xp.shape[:3], L.C, L.D, L.stride, L.pad, sizes),
-                               dtype=torch.uint16, device="cuda")
+            shape = sa.conv_out_shape(*o.Xp.shape[:3], L.C, L.D, L.stride, L.pad, sizes)
+            o.Yc = torch.empty(shape[:3] + (pitch8(sizes),), dtype=torch.uint16, device="cuda")
             o.flops_c = 2 * wl.batch * L.P * L.Q * sum(sizes.M[g] * kept_k(sizes, g) for g in range(sizes.groups))
             o.flops_d = 2 * wl.batch * L.P * L.Q * sum(sized.M[g] * kept_k(sized, g) for g in range(sized.groups))
             o.sizes_c = sizes
@@ -340,8 +348,8 @@ def conv_only(args):
         kern = kernel_of(sa, plan)
         if args.kernel is not None and kern != args.kernel:
             continue
-        Y = torch.empty(sa.conv_out_shape(*o.Xp.shape[:3], L.C, L.D, L.stride, L.pad, sizes),
-                        dtype=torch.uint16, device="cuda")
+        shape = sa.conv_out_shape(*o.Xp.shape[:3], L.C, L.D, L.stride, L.pad, sizes)
+        Y = torch.empty(shape[:3] + (pitch8(sizes),), dtype=torch.uint16, device="cuda")
         cv = torch.empty(max(256, sa.conv_workspace(o.Xp, sizes, L.C, L.D, L.stride, L.pad)),
                          dtype=torch.uint8, device="cuda")
         picked.append((i, o, L, c, Y, cv, plan, kern))
@@ -476,9 +484,9 @@ def suite_tables(torch, sa):
             need = max(sa.conv_workspace(Xp, sz, L.C, L.D, L.stride, L.pad),
                        sa.conv_workspace(Xp, szd, L.C, L.D, L.stride, L.pad), 256)
             cws = torch.empty(need, dtype=torch.uint8, device="cuda")
-            Yc = sa.conv_fwd(Xp, Wc, cc, ct, sz, L.C, L.D, L.stride, L.pad, ws=cws)
+            Yc = sa.conv_fwd(Xp, Wc, cc, ct, sz, L.C, L.D, L.stride, L.pad, ws=cws, ldy=pitch8(sz))
             Yd = sa.conv_fwd(Xp, Wd, ccd, ctd, szd, L.C, L.D, L.stride, L.pad, ws=cws)
-            dc = sa.conv_desc(Xp, Wc, cc, ct, sz, L.C, L.D, L.stride, L.pad, Yc, cws)
+            dc = sa.conv_desc(Xp, Wc, cc, ct, sz, L.C, L.D, L.stride, L.pad, Yc, cws, Yc.shape[-1])
             dd = sa.conv_desc(Xp, Wd, ccd, ctd, szd, L.C, L.D, L.stride, L.pad, Yd, cws)
             tc = _time_graph(torch, lambda: sa.conv_fwd(None, None, None, None, sz, 0, 0, 0, 0, desc=dc))
             td = _time_graph(torch, lambda: sa.conv_fwd(None, None, None, None, szd, 0, 0, 0, 0, desc=dd))
@@ -732,9 +740,9 @@ def suite_conv(torch, sa, wl, variant, layer_ids=None):
         need = max(sa.conv_workspace(Xc, sz, L.C, L.D, L.stride, L.pad),
                    sa.conv_workspace(Xf, szd, L.C, L.D, L.stride, L.pad), 256)
         cws = torch.empty(need, dtype=torch.uint8, device="cuda")
-        Yc = sa.conv_fwd(Xc, Wc, cc, ct, sz, L.C, L.D, L.stride, L.pad, ws=cws)
+        Yc = sa.conv_fwd(Xc, Wc, cc, ct, sz, L.C, L.D, L.stride, L.pad, ws=cws, ldy=pitch8(sz))
         Yd = sa.conv_fwd(Xf, Wd, ccd, ctd, szd, L.C, L.D, L.stride, L.pad, ws=cws)
-        dc, dd = sa.conv_desc(Xc, Wc, cc, ct, sz, L.C, L.D, L.stride, L.pad, Yc, cws), \
+        dc, dd = sa.conv_desc(Xc, Wc, cc, ct, sz, L.C, L.D, L.stride, L.pad, Yc, cws, Yc.shape[-1]), \
             sa.conv_desc(Xf, Wd, ccd, ctd, szd, L.C, L.D, L.stride, L.pad, Yd, cws)
         tc = _time(torch, lambda: sa.conv_fwd(None, None, None, None, sz, 0, 0, 0, 0, desc=dc), reps=10)
         td = _time(torch, lambda: sa.conv_fwd(None, None, None, None, szd, 0, 0, 0, 0, desc=dd), reps=10)

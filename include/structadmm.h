@@ -285,7 +285,13 @@ int structadmm_pack_nhwc(const float *X, int32_t N, int32_t Cin, int32_t H, int3
  * no bias, no dilation).  bfloat16 inputs, binary32 accumulation on the
  * matrix cores, bfloat16 output (nearest even).
  * X: bfloat16 NHWC [N, H, W, Cx], 16-byte aligned, smaller than 2 GiB.
- * Y: bfloat16 NHWC [N, P, Q, sum_g M_g], P = (H + 2*pad - C)/stride + 1, same for Q.
+ * Y: bfloat16 NHWC [N, P, Q, Cy], Cy = sum_g M_g, P = (H + 2*pad - C)/stride + 1,
+ * same for Q, 4-byte aligned; with ldy > 0 its N*P*Q rows are ldy >= Cy
+ * elements apart instead of Cy (a padded channel pitch: with ldy a multiple
+ * of 8 every row starts on a 16-byte boundary, so the output is written with
+ * 16-byte stores when Cy is not a multiple of 8).  Elements [Cy, ldy) of a row
+ * are not part of the result: the call leaves them unchanged or writes +0
+ * there.
  * sizes: host struct filled by structadmm_compact for the same Wc / tables.
  */
 typedef struct sa_conv_desc {
@@ -301,6 +307,7 @@ typedef struct sa_conv_desc {
     void *ws;                    /* device scratch of structadmm_conv_workspace() bytes,
                                     256-byte aligned (NULL when that size is 0) */
     size_t ws_bytes;
+    int32_t ldy;                 /* output row pitch in elements (0: Cy) */
 } sa_conv_desc;
 
 /* Scratch bytes structadmm_conv_fwd needs.  None when the input has a

@@ -12,7 +12,7 @@ Entry points (same names as the C ABI):
   sgd_step(items, stream=None)
   compact(Z, groups, ..., ws=None, stream=None) -> (Wc, row_idx, col_ch, col_tap, sizes)
   pack_nhwc(X, keep=None, Cx=None, stream=None)
-  conv_fwd(X, Wc, col_ch, col_tap, sizes, C, D, stride, pad, Y=None, stream=None)
+  conv_fwd(X, Wc, col_ch, col_tap, sizes, C, D, stride, pad, Y=None, stream=None, ldy=None)
   csr(Z, kept_idx, row_ptr=None, col=None, val=None, stream=None) -> (row_ptr, col, val)
   conv_sparse_workspace(Xp, shape, groups, stride, pad, nnz)
   conv_sparse_fwd(Xp, row_ptr, col, val, shape, groups, stride, pad, Y=None, ws=None, stream=None)
@@ -83,7 +83,8 @@ class ConvDesc(ctypes.Structure):
     _fields_ = [("N", ctypes.c_int32), ("H", ctypes.c_int32), ("W", ctypes.c_int32), ("Cx", ctypes.c_int32),
                 ("C", ctypes.c_int32), ("D", ctypes.c_int32), ("stride", ctypes.c_int32), ("pad", ctypes.c_int32),
                 ("sizes", ctypes.POINTER(CompactSizes)), ("X", _vp), ("Wc", _vp), ("col_ch", _vp),
-                ("col_tap", _vp), ("Y", _vp), ("ws", _vp), ("ws_bytes", ctypes.c_size_t)]
+                ("col_tap", _vp), ("Y", _vp), ("ws", _vp), ("ws_bytes", ctypes.c_size_t),
+                ("ldy", ctypes.c_int32)]
 
 
 class ConvPlanInfo(ctypes.Structure):
@@ -317,11 +318,11 @@ def conv_out_shape(N, H, W, C, D, stride, pad, sizes: CompactSizes):
     return (N, P, Q, int(sum(sizes.M[g] for g in range(sizes.groups))))
 
 
-def conv_desc(Xp, Wc, col_ch, col_tap, sizes: CompactSizes, C, D, stride, pad, Y, ws=None) -> ConvDesc:
+def conv_desc(Xp, Wc, col_ch, col_tap, sizes: CompactSizes, C, D, stride, pad, Y, ws=None, ldy=0) -> ConvDesc:
     N, H, W, Cx = Xp.shape
     nbytes = 0 if ws is None else ws.numel() * ws.element_size()
     return ConvDesc(N, H, W, Cx, C, D, stride, pad, ctypes.pointer(sizes), _ptr(Xp), _ptr(Wc),
-                    _ptr(col_ch), _ptr(col_tap), _ptr(Y), _ptr(ws), nbytes)
+                    _ptr(col_ch), _ptr(col_tap), _ptr(Y), _ptr(ws), nbytes, ldy)
 
 
 def conv_workspace(Xp, sizes: CompactSizes, C: int, D: int, stride: int, pad: int) -> int:
@@ -343,22 +344,32 @@ def conv_plan(Xp, sizes: CompactSizes, C: int, D: int, stride: int, pad: int) ->
 
 
 def conv_fwd(Xp, Wc, col_ch, col_tap, sizes: CompactSizes, C: int, D: int, stride: int, pad: int,
-             Y=None, ws=None, stream=None, desc: Optional[ConvDesc] = None):
+             Y=None, ws=None, stream=None, desc: Optional[ConvDesc] = None, ldy: Optional[int] = None):
     """structadmm_conv_fwd; Xp bf16 NHWC (uint16), returns Y bf16 NHWC (uint16).
-    ``ws``: uint8 device scratch of conv_workspace() bytes (allocated here when None)."""
+    ``ws``: uint8 device scratch of conv_workspace() bytes (allocated here when None).
+    ``ldy``: output row pitch in elements (>= the output channels Cy); by default
+    the last dimension of a given 4-d Y, else Cy.  Y is then [N, P, Q, ldy] whose
+    channels [Cy, ldy) are padding (left unchanged or set to +0)."""
     import torch
     temps = []
     if desc is None:
         N, H, W, Cx = Xp.shape
+        shape = conv_out_shape(N, H, W, C, D, stride, pad, sizes)
+        Cy = shape[-1]
+        if ldy is None:
+            ldy = Y.shape[-1] if (Y is not None and Y.dim() == 4) else Cy
+        if ldy < Cy:
+            raise StructAdmmError(f"conv_fwd: ldy={ldy} is below the {Cy} output channels")
         if Y is None:
-            Y = torch.empty(conv_out_shape(N, H, W, C, D, stride, pad, sizes), dtype=torch.uint16,
-                            device=Xp.device)
+            Y = torch.empty(shape[:3] + (ldy,), dtype=torch.uint16, device=Xp.device)
             temps.append(Y)
+        elif Y.numel() < shape[0] * shape[1] * shape[2] * ldy or Y.dtype != torch.uint16:
+            raise StructAdmmError(f"conv_fwd: Y must be uint16 with room for {shape[:3]} rows of {ldy}")
         if ws is None:
             need = conv_workspace(Xp, sizes, C, D, stride, pad)
             ws = torch.empty(need, dtype=torch.uint8, device=Xp.device) if need else None
             temps.append(ws)
-        desc = conv_desc(Xp, Wc, col_ch, col_tap, sizes, C, D, stride, pad, Y, ws)
+        desc = conv_desc(Xp, Wc, col_ch, col_tap, sizes, C, D, stride, pad, Y, ws, 0 if ldy == Cy else ldy)
     _check(lib().structadmm_conv_fwd(ctypes.byref(desc), _stream(stream)), "structadmm_conv_fwd")
     _keep_for_stream(stream, *temps)
     return Y

@@ -69,6 +69,7 @@ struct ConvArgs {
     int64_t part_stride;  // floats per chunk (N*P*Q*Cy rounded up to 4)
     int32_t ksplit, base_blocks;
     int32_t H, W, D, stride, pad, P, Q, NPQ, Cy;
+    int32_t ldy;  // Y's row pitch (>= Cy)
     int32_t ngroups, nblocks;
     FastDiv divPQ, divQ, divD, divCy;
     ConvGroup g[SA_MAX_CONV_GROUPS];
@@ -256,17 +257,21 @@ __global__ __launch_bounds__(64 * WN * WM) void k_conv(ConvArgs a) {
                 *reinterpret_cast<bf16x4 *>(&sC[pl * (BN + 8) + ml]) = o;
             }
     __syncthreads();
-    if (a.Cy % 8 != 0 && G.mtiles == 1 && G.M == a.Cy && ((uintptr_t)a.Y & 15) == 0) {  // whole, unaligned rows
+    if (a.Cy % 8 != 0 && a.ldy == a.Cy && G.mtiles == 1 && G.M == a.Cy && ((uintptr_t)a.Y & 15) == 0) {
+        // whole, unaligned rows
         store_tile_rows<BN + 8>(a.Y, sC, n0, min(BM, a.NPQ - n0), a.Cy, a.divCy, tid, NT);
         return;
     }
+    // the last channels of a row may run on into the row's padding (staged
+    // rows past the group's filters hold +0)
+    const int lim = G.o_off + G.M == a.Cy ? a.ldy - G.o_off : G.M;
     constexpr int CPR = BN / 8;  // 16-byte chunks per output row
     for (int c = tid; c < BM * CPR; c += NT) {
         const int pl = c / CPR, mc = c - pl * CPR;
         const int px = n0 + pl, m = m0 + mc * 8;
         if (px >= a.NPQ || m >= G.M) continue;
-        uint16_t *dst = a.Y + (int64_t)px * a.Cy + G.o_off + m;
-        store_out8(dst, &sC[pl * (BN + 8) + mc * 8], min(8, G.M - m));
+        uint16_t *dst = a.Y + (int64_t)px * a.ldy + G.o_off + m;
+        store_out8(dst, &sC[pl * (BN + 8) + mc * 8], min(8, lim - m));
     }
 }
 
@@ -463,6 +468,7 @@ struct PatchArgs {
     uint16_t *Y;
     uint32_t x_bytes;
     int32_t N, H, W, Cx, C, D, stride, pad, P, Q, NPQ, Cy;
+    int32_t ldy;  // Y's row pitch (>= Cy)
     int32_t Hp, Wp, Ws, Wpp;
     int32_t ngroups, nblocks, patch_bytes, tab_bytes;
     // space-to-depth input (s2d > 1): X holds s x s blocks of the padded input
@@ -768,28 +774,41 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(TM >= 6
                 *reinterpret_cast<bf16x4 *>(&sC[pl * (BNB + 8) + ml]) = o;
             }
     __syncthreads();
-    if (a.Cy % 8 != 0 && G.mtiles == 1 && G.M == a.Cy && ((uintptr_t)a.Y & 15) == 0) {  // whole, unaligned rows
+    if (a.Cy % 8 != 0 && a.ldy == a.Cy && G.mtiles == 1 && G.M == a.Cy && ((uintptr_t)a.Y & 15) == 0) {
+        // whole, unaligned rows
         store_tile_rows<BNB + 8>(a.Y, sC, n0, min(BMB, a.NPQ - n0), a.Cy, a.divCy, tid, NT);
         return;
     }
+    // the last channels of a row may run on into the row's padding (+0)
+    const int lim = G.o_off + G.M == a.Cy ? a.ldy - G.o_off : G.M;
     constexpr int CPR = BNB / 8;
     for (int c = tid; c < BMB * CPR; c += NT) {
         const int pl = c / CPR, mc = c - pl * CPR;
         const int px = n0 + pl, m = m0 + mc * 8;
         if (px >= a.NPQ || m >= G.M) continue;
-        uint16_t *dst = a.Y + (int64_t)px * a.Cy + G.o_off + m;
-        store_out8(dst, &sC[pl * (BNB + 8) + mc * 8], min(8, G.M - m));
+        uint16_t *dst = a.Y + (int64_t)px * a.ldy + G.o_off + m;
+        store_out8(dst, &sC[pl * (BNB + 8) + mc * 8], min(8, lim - m));
     }
 }
 
 // ---------------------------------------------------------------- k_splitk_sum
 // Split K: Y = bf16(sum over chunks c = 0, 1, ... of part[c]) in that order
 // (one fixed order: the result does not depend on which chunk finished
-// first).  Element f of a chunk is element f of Y = [N*P*Q][Cy].
+// first).  Element f = r * Cy + c of a chunk is output (row r, channel c),
+// at Y[r * ldy + c].
 __global__ __launch_bounds__(256) void k_splitk_sum(const float *part, int64_t stride, int ksplit, uint16_t *Y,
-                                                     int64_t total) {
+                                                     int64_t total, int Cy, int ldy) {
     const int64_t f = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 4;
     if (f >= total) return;
+    if (ldy != Cy) {  // padded rows: element by element
+        for (int64_t e = f; e < f + 4 && e < total; ++e) {
+            float acc = part[e];
+            for (int c = 1; c < ksplit; ++c) acc += part[c * stride + e];
+            const int64_t r = e / Cy;
+            Y[r * ldy + (e - r * Cy)] = f32_to_bf16_bits(acc);
+        }
+        return;
+    }
     if (f + 4 <= total) {
         float4 acc = *reinterpret_cast<const float4 *>(part + f);
 #pragma unroll 7
@@ -1561,6 +1580,7 @@ extern "C" int structadmm_conv_fwd(const sa_conv_desc *desc, hipStream_t stream)
     memset(&pa, 0, sizeof pa);
     direct.Y = gathered.Y = pa.Y = d.Y;
     direct.Cy = gathered.Cy = pa.Cy = p.Cy;
+    direct.ldy = gathered.ldy = pa.ldy = d.ldy ? d.ldy : p.Cy;
     direct.ksplit = gathered.ksplit = p.ksplit;
     if (p.ksplit > 1) {
         direct.part = gathered.part = reinterpret_cast<float *>(static_cast<uint8_t *>(d.ws) + p.part_off);
@@ -1728,6 +1748,7 @@ extern "C" int structadmm_conv_fwd(const sa_conv_desc *desc, hipStream_t stream)
         ia.Q = Q;
         ia.NPQ = NPQ;
         ia.Cy = p.Cy;
+        ia.ldy = d.ldy ? d.ldy : p.Cy;
         ia.ngroups = direct.ngroups;
         for (int i = 0; i < direct.ngroups; ++i) {
             const ConvGroup &c = direct.g[i];
@@ -1768,7 +1789,8 @@ extern "C" int structadmm_conv_fwd(const sa_conv_desc *desc, hipStream_t stream)
         const int64_t total = (int64_t)NPQ * p.Cy;
         const int64_t blocks = (total + 1023) / 1024;
         hipLaunchKernelGGL(k_splitk_sum, dim3((unsigned)blocks), dim3(256), 0, stream,
-                           static_cast<const float *>(direct.part), p.part_stride, p.ksplit, d.Y, total);
+                           static_cast<const float *>(direct.part), p.part_stride, p.ksplit, d.Y, total, p.Cy,
+                           direct.ldy);
         return check_hip(hipGetLastError(), "k_splitk_sum");
     }
     return SA_OK;

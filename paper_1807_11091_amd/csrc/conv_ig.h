@@ -25,10 +25,10 @@ struct IgGroup {
 
 struct IgArgs {
     const uint16_t *X;  // bf16 NHWC [N, H, W, Cx], 16-byte aligned
-    uint16_t *Y;        // bf16 NHWC [N, P, Q, Cy], 4-byte aligned
+    uint16_t *Y;        // bf16 NHWC rows of ldy >= Cy elements, 4-byte aligned
     uint32_t x_bytes;
     int32_t yshift;     // elements from the 16-byte boundary below Y to Y
-    int32_t H, W, Cx, D, stride, pad, P, Q, NPQ, Cy;
+    int32_t H, W, Cx, D, stride, pad, P, Q, NPQ, Cy, ldy;
     int32_t ngroups, ntiles;
     FastDiv divPQ, divQ, divD, divCy;
     IgGroup g[SA_MAX_CONV_GROUPS];

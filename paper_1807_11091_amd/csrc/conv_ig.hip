@@ -232,16 +232,18 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
         const TilePos P = tile_pos<BM, BP>(a, t);
         const IgGroup &G = a.g[P.gi];
         const int rows = min(BP, a.NPQ - P.p0);
-        const int count = min(BM, G.M - P.m0);
-        const bool whole = G.mtiles == 1 && G.M == a.Cy && a.yshift == 0;
-        const int64_t e_tile = (int64_t)P.p0 * a.Cy + G.o_off + P.m0;  // Y offset of the tile's (0, 0)
+        // count results per row, then (the last channels of a row) +0 up to
+        // the row's padded pitch
+        const int count = min(BM, (G.o_off + G.M == a.Cy ? a.ldy - G.o_off : G.M) - P.m0);
+        const bool whole = G.mtiles == 1 && G.M == a.Cy && a.yshift == 0 && a.ldy == a.Cy;
+        const int64_t e_tile = (int64_t)P.p0 * a.ldy + G.o_off + P.m0;  // Y offset of the tile's (0, 0)
         // LDS position of output (pl, m): whole rows keep Y's pitch Cy, other
         // rows sit at pl * CP + shift(pl), shift = Y's misalignment of the row
         const int pitch = whole ? a.Cy : CP;
 #pragma unroll
         for (int j = 0; j < NF; ++j) {
             const int pl = (wn * NF + j) * 16 + (lane & 15);
-            const int sh = whole ? 0 : (int)((e_tile + (int64_t)pl * a.Cy + a.yshift) & 7);
+            const int sh = whole ? 0 : (int)((e_tile + (int64_t)pl * a.ldy + a.yshift) & 7);
             uint16_t *row = sC + pl * pitch + sh;
 #pragma unroll
             for (int i = 0; i < MT; ++i) {
@@ -273,7 +275,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
         constexpr int CPR = BM / 8 + 2;  // chunks a shifted row segment can touch
         for (int c = tid; c < rows * CPR; c += kThreads) {
             const int pl = c / CPR, ci = c - pl * CPR;
-            const int64_t e0 = e_tile + (int64_t)pl * a.Cy;
+            const int64_t e0 = e_tile + (int64_t)pl * a.ldy;
             const int sh = (int)((e0 + a.yshift) & 7);
             const int lo = ci * 8 - sh;  // tile-row index of the chunk's first element
             if (lo >= count) continue;
@@ -523,9 +525,10 @@ __global__ __launch_bounds__(256 * KG) void k_igk(IgArgs a) {
     }
     __syncthreads();
     const int rows = min(BP, a.NPQ - P.p0);
-    const int count = min(BM, G.M - P.m0);
-    const bool whole = G.mtiles == 1 && G.M == a.Cy && a.yshift == 0;
-    const int64_t e_tile = (int64_t)P.p0 * a.Cy + G.o_off + P.m0;
+    // results, then +0 up to the padded pitch of a row's last channels
+    const int count = min(BM, (G.o_off + G.M == a.Cy ? a.ldy - G.o_off : G.M) - P.m0);
+    const bool whole = G.mtiles == 1 && G.M == a.Cy && a.yshift == 0 && a.ldy == a.Cy;
+    const int64_t e_tile = (int64_t)P.p0 * a.ldy + G.o_off + P.m0;
     const int pitch = whole ? a.Cy : CP;
     if (kg == 0) {
 #pragma unroll
@@ -541,7 +544,7 @@ __global__ __launch_bounds__(256 * KG) void k_igk(IgArgs a) {
 #pragma unroll
         for (int j = 0; j < NF; ++j) {
             const int pl = (wn * NF + j) * 16 + (lane & 15);
-            const int sh = whole ? 0 : (int)((e_tile + (int64_t)pl * a.Cy + a.yshift) & 7);
+            const int sh = whole ? 0 : (int)((e_tile + (int64_t)pl * a.ldy + a.yshift) & 7);
             uint16_t *row = sC + pl * pitch + sh;
 #pragma unroll
             for (int i = 0; i < MT; ++i) {
@@ -573,7 +576,7 @@ __global__ __launch_bounds__(256 * KG) void k_igk(IgArgs a) {
     constexpr int CPR = BM / 8 + 2;
     for (int c = tid; c < rows * CPR; c += Cfg::NT) {
         const int pl = c / CPR, ci = c - pl * CPR;
-        const int64_t e0 = e_tile + (int64_t)pl * a.Cy;
+        const int64_t e0 = e_tile + (int64_t)pl * a.ldy;
         const int sh = (int)((e0 + a.yshift) & 7);
         const int lo = ci * 8 - sh;
         if (lo >= count) continue;

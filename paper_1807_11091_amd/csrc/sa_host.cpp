@@ -141,6 +141,8 @@ int validate_conv(const sa_conv_desc &d) {
     }
     if (Cy <= 0)
         return fail(SA_E_ARG, "conv: no output channels");
+    if (d.ldy != 0 && d.ldy < Cy)
+        return fail(SA_E_ARG, "conv: ldy=%d is below the %lld output channels", d.ldy, (long long)Cy);
     if (!d.X || !d.Wc || !d.Y || !d.col_ch || !d.col_tap)
         return fail(SA_E_ARG, "conv: X, Wc, col_ch, col_tap and Y are required");
     if (!aligned(d.X, 16) || !aligned(d.Wc, 16) || !aligned(d.Y, 4))

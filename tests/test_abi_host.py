@@ -46,7 +46,7 @@ def _c_layout():
         "sa_compact_desc": ("CompactDesc", ["groups", "Z", "in_compacted", "Wc", "ws"]),
         "sa_compact_sizes": ("CompactSizes", ["M", "K", "ldk", "wc_offset", "row_offset", "run", "run_base",
                                               "ch_lo", "ch_span", "kpad"]),
-        "sa_conv_desc": ("ConvDesc", ["N", "pad", "sizes", "X", "Y", "ws", "ws_bytes"]),
+        "sa_conv_desc": ("ConvDesc", ["N", "pad", "sizes", "X", "Y", "ws", "ws_bytes", "ldy"]),
         "sa_conv_plan_info": ("ConvPlanInfo", ["groups", "path", "ksplit", "space_to_depth", "ig_tile",
                                                "footprint_tile"]),
         "sa_csr_desc": ("CsrDesc", ["A", "D", "nnz", "Z", "kept_idx", "row_ptr", "col", "val"]),

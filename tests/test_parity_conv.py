@@ -497,3 +497,67 @@ def test_conv_on_a_non_current_stream():
     s.synchronize()
     assert t.equal(Y, ref)
     del junk
+
+
+# (name, N, Cin, H, W, A, C, D, stride, pad, groups, kind, kept, what the plan must take)
+PITCH_CASES = [
+    ("direct_whole_rows", 32, 64, 64, 64, 64, 3, 3, 1, 1, 1, sa.FILTER, 38, "k_conv"),
+    ("direct_tiles", 32, 64, 64, 64, 256, 3, 3, 1, 1, 1, sa.FILTER, 154, "k_conv"),
+    ("ig_1x1", 8, 64, 28, 28, 64, 1, 1, 1, 0, 1, sa.FILTER, 38, "k_ig"),
+    ("igk", 16, 256, 28, 28, 256, 3, 3, 1, 1, 1, sa.FILTER, 154, "k_igk"),
+    ("footprint", 4, 64, 20, 20, 96, 3, 3, 1, 1, 1, sa.SHAPE, 173, "footprint"),
+    ("space_to_depth", 2, 3, 64, 64, 64, 7, 7, 2, 3, 1, sa.FILTER, 38, "s2d"),
+    ("split_k", 1, 512, 7, 7, 512, 3, 3, 1, 1, 1, sa.FILTER, 307, "split"),
+    ("grouped", 4, 96, 27, 27, 256, 5, 5, 1, 2, 2, sa.FILTER, 129, None),
+]
+
+
+@pytest.mark.parametrize("case", PITCH_CASES, ids=[c[0] for c in PITCH_CASES])
+@pytest.mark.parametrize("pitch", ["pad8", "odd"])
+def test_conv_output_pitch(case, pitch):
+    """Output rows ldy elements apart (ldy > Cy): every output equals, bit for
+    bit, the same CONV with rows of Cy; the row padding [Cy, ldy) is left
+    unchanged or +0, and nothing past the last row is written."""
+    t = torch()
+    name, N, Cin, H, Wd, A, C, D, stride, pad, groups, kind, kept, want = case
+    rng = np.random.default_rng(len(name) * 131 + (pitch == "odd"))
+    B = Cin // groups
+    W = (0.05 * rng.standard_normal((A, B, C, D))).astype(np.float32)
+    G = {sa.FILTER: A, sa.SHAPE: B * C * D}[kind]
+    mask = np.zeros(G, np.uint8)
+    mask[rng.choice(G, size=kept, replace=False)] = 1
+    if kind == sa.FILTER:
+        W[mask == 0] = 0
+        Wc, ri, cc, ct, sizes = sa.compact(to_dev(W), groups, row_mask=to_dev(mask))
+    else:
+        W.reshape(A, -1)[:, mask == 0] = 0
+        Wc, ri, cc, ct, sizes = sa.compact(to_dev(W), groups, col_mask=to_dev(mask))
+    Xp = sa.pack_nhwc(to_dev(rng.standard_normal((N, Cin, H, Wd)).astype(np.float32)))
+    plan = sa.conv_plan(Xp, sizes, C, D, stride, pad)
+    paths = set(plan["path"]) - {sa.CONV_NONE}
+    if want == "k_conv":
+        assert paths == {sa.CONV_DIRECT} and plan["ksplit"] == 1, plan
+    elif want in ("k_ig", "k_igk"):
+        assert paths == {sa.CONV_DIRECT_IG} and (plan["ig_tile"][3] > 1) == (want == "k_igk"), plan
+    elif want == "footprint":
+        assert paths == {sa.CONV_FOOTPRINT}, plan
+    elif want == "s2d":
+        assert plan["space_to_depth"] > 0, plan
+    elif want == "split":
+        assert plan["ksplit"] > 1, plan
+    Y0 = sa.conv_fwd(Xp, Wc, cc, ct, sizes, C, D, stride, pad)
+    Nn, P, Q, Cy = Y0.shape
+    ldy = (Cy + 8) // 8 * 8 if pitch == "pad8" else Cy + 5  # a multiple of 8 above Cy, or an odd pitch
+    assert ldy > Cy
+    SENT = 0x7FC1  # a bf16 NaN that no output takes
+    buf = t.full((Nn * P * Q * ldy + 64,), SENT, dtype=t.int32, device=DEV).to(t.uint16)
+    Y1 = buf[: Nn * P * Q * ldy].view(Nn, P, Q, ldy)
+    got = sa.conv_fwd(Xp, Wc, cc, ct, sizes, C, D, stride, pad, Y=Y1, ldy=ldy)
+    assert got.data_ptr() == Y1.data_ptr()
+    t.cuda.synchronize()
+    y0 = Y0.cpu().numpy()
+    y1 = Y1.cpu().numpy()
+    assert np.array_equal(y1[..., :Cy], y0), (name, pitch)
+    pads = y1[..., Cy:]
+    assert np.all((pads == SENT) | (pads == 0)), (name, pitch)
+    assert np.all(buf[Nn * P * Q * ldy:].cpu().numpy() == SENT)
