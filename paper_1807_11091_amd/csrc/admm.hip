@@ -4,7 +4,8 @@
 // retraining (k_sgd).
 //
 // Data flow of structadmm_project for one dependency level of layers:
-//   k_expand_allowed  (layers with an input-channel support) per-column support bytes
+//   k_expand_allowed  (channel, shape and element-wise layers with an input-channel
+//                     support) per-column support bytes; filter sets read the mask
 //   k_row_scores      filter sets: one wavefront per weight row, O_a in binary64
 //   k_col_partials    channel / shape sets: binary64 column sums per band of rows
 //   k_select          one workgroup per structured layer: final scores, radix
@@ -46,16 +47,17 @@ constexpr int kElemHistBlocks = 1024;
 struct RowLayer {
     const float *W;
     float *U;
-    float *Z;
-    float *G;
-    const uint8_t *rowkeep;  // [A] or null: every row kept
-    const uint8_t *colkeep;  // [groups*K] or null: every column kept
     const uint8_t *allowed;  // [groups*K] or null: every entry inside the support
+    const uint8_t *inmask;   // [groups*B] or null: filter sets read the support from the
+                             // input-channel mask itself (entry (a, j) is inside when
+                             // inmask[(a / Ag) * B + j / CD] is set)
     double *scores;          // [A] (row scores)
     double *rowpart;         // [A][nchunk] partial row sums when nchunk > 1
     int32_t A, K, Ag;        // rows, row length, rows per conv group
     int32_t R, nchunk;       // rows per wavefront item (short rows), 1024-weight chunks per row
     int32_t vec;             // K % 4 == 0: float4 path
+    int32_t B;               // input channels per conv group (inmask)
+    FastDiv divCD;           // taps per channel (inmask)
     float rho;
 };
 struct RowTab {
@@ -161,7 +163,7 @@ __device__ inline float masked(float v, uint8_t keep) { return keep ? v : 0.0f; 
 // Every wavefront takes one item: R = 4 rows when a row has at most 64 float4
 // (one per lane), 2 rows up to 128, else one 1024-weight chunk of a row, whose
 // partial sums k_select adds in chunk order.
-__device__ inline float4 row_v(const RowLayer &L, const uint8_t *al, int64_t base, int i) {
+__device__ inline float4 row_v(const RowLayer &L, const uint8_t *al, const uint8_t *im, int64_t base, int i) {
     float4 x = *reinterpret_cast<const float4 *>(L.W + base + 4 * (int64_t)i);
     float4 y = *reinterpret_cast<const float4 *>(L.U + base + 4 * (int64_t)i);
     float4 v = make_float4(x.x + y.x, x.y + y.y, x.z + y.z, x.w + y.w);
@@ -169,8 +171,15 @@ __device__ inline float4 row_v(const RowLayer &L, const uint8_t *al, int64_t bas
         uchar4 m = reinterpret_cast<const uchar4 *>(al)[i];
         v.x = masked(v.x, m.x); v.y = masked(v.y, m.y);
         v.z = masked(v.z, m.z); v.w = masked(v.w, m.w);
+    } else if (im) {  // the input channel of column j is j / CD
+        const uint32_t j = 4u * (uint32_t)i;
+        v.x = masked(v.x, im[fdiv(j, L.divCD)]); v.y = masked(v.y, im[fdiv(j + 1, L.divCD)]);
+        v.z = masked(v.z, im[fdiv(j + 2, L.divCD)]); v.w = masked(v.w, im[fdiv(j + 3, L.divCD)]);
     }
     return v;
+}
+__device__ inline const uint8_t *row_inmask(const RowLayer &L, int a) {
+    return L.inmask ? L.inmask + (int64_t)(a / L.Ag) * L.B : nullptr;
 }
 __device__ inline double sq4(float4 v) {
     double acc = (double)v.x * (double)v.x;
@@ -191,10 +200,12 @@ __global__ __launch_bounds__(kRowThreads) void k_row_scores(RowTab tab) {
         for (int a = item0; a < item0 + kRowItems && a < L.A; ++a) {
             const int64_t base = (int64_t)a * L.K;
             const uint8_t *al = L.allowed ? L.allowed + (int64_t)(a / L.Ag) * L.K : nullptr;
+            const uint8_t *im = row_inmask(L, a);
             double acc = 0.0;
             for (int i = lane; i < L.K; i += kWave) {
                 float v = L.W[base + i] + L.U[base + i];
                 if (al) v = masked(v, al[i]);
+                else if (im) v = masked(v, im[fdiv((uint32_t)i, L.divCD)]);
                 acc += (double)v * (double)v;
             }
             acc = wave_sum(acc);
@@ -214,7 +225,7 @@ __global__ __launch_bounds__(kRowThreads) void k_row_scores(RowTab tab) {
                 v[q][u] = make_float4(0.f, 0.f, 0.f, 0.f);
                 if (a < L.A && i < K4) {
                     const uint8_t *al = L.allowed ? L.allowed + (int64_t)(a / L.Ag) * L.K : nullptr;
-                    v[q][u] = row_v(L, al, (int64_t)a * L.K, i);
+                    v[q][u] = row_v(L, al, row_inmask(L, a), (int64_t)a * L.K, i);
                 }
             }
 #pragma unroll
@@ -237,11 +248,12 @@ __global__ __launch_bounds__(kRowThreads) void k_row_scores(RowTab tab) {
         const int item = item0 + q;
         const int a = item / L.nchunk, c = item - a * L.nchunk;
         const uint8_t *al = (L.allowed && a < L.A) ? L.allowed + (int64_t)(a / L.Ag) * L.K : nullptr;
+        const uint8_t *im = a < L.A ? row_inmask(L, a) : nullptr;
         const int64_t base = (int64_t)a * L.K;
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
             const int i = c * 4 * kWave + u * kWave + lane;
-            v[q][u] = (a < L.A && i < K4) ? row_v(L, al, base, i) : make_float4(0.f, 0.f, 0.f, 0.f);
+            v[q][u] = (a < L.A && i < K4) ? row_v(L, al, im, base, i) : make_float4(0.f, 0.f, 0.f, 0.f);
         }
     }
 #pragma unroll
@@ -485,8 +497,10 @@ struct ApplyLayer {
     float *G;
     const uint8_t *rowkeep;  // [A] or null
     const uint8_t *colkeep;  // [groups*K] or null
-    FastDiv divK, divAg;
-    int32_t n, K;
+    const uint8_t *inmask;   // [groups*B] or null: column j of conv group gc is kept when
+                             // inmask[gc * B + j / CD] is set
+    FastDiv divK, divAg, divCD;
+    int32_t n, K, B;
     float rho;
 };
 struct ApplyTab {
@@ -508,6 +522,7 @@ __device__ inline void apply_one(const ApplyLayer &L, float w, float u, uint32_t
     bool keep = true;
     if (L.rowkeep) keep = L.rowkeep[row] != 0;
     if (keep && L.colkeep) keep = L.colkeep[(int64_t)fdiv(row, L.divAg) * L.K + col] != 0;
+    if (keep && L.inmask) keep = L.inmask[(int64_t)fdiv(row, L.divAg) * L.B + fdiv(col, L.divCD)] != 0;
     const float v = w + u;
     z = keep ? v : 0.0f;
     if (fused) {
@@ -981,7 +996,7 @@ void plan_layer(const sa_project_desc &d, size_t start, LayerPlan &p) {
         p.off_partials = off;
         off = align256(off + sizeof(double) * (size_t)p.nbands * p.K);
     }
-    if (d.in_ch_mask) {
+    if (d.in_ch_mask && d.kind != SA_FILTER) {
         p.off_allowed = off;
         off = align256(off + (size_t)d.groups * p.K);
     }
@@ -1118,14 +1133,12 @@ int project_impl(const sa_project_desc *layers, int n_layers, void *ws, size_t w
         const LayerPlan &p = plan[i];
         R.W = d.W;
         R.U = d.U;
-        R.Z = d.Z;
-        R.G = d.G;
-        R.rowkeep = d.kind == SA_FILTER ? d.mask : nullptr;
-        if (d.kind == SA_FILTER)
-            R.colkeep = d.in_ch_mask ? ws_at<uint8_t>(ws, p.off_allowed) : nullptr;
-        else
-            R.colkeep = ws_at<uint8_t>(ws, p.off_colkeep);
-        R.allowed = d.in_ch_mask ? ws_at<uint8_t>(ws, p.off_allowed) : nullptr;
+        // filter sets read their support straight from the input-channel mask;
+        // the other sets use its per-column expansion
+        R.allowed = d.in_ch_mask && d.kind != SA_FILTER ? ws_at<uint8_t>(ws, p.off_allowed) : nullptr;
+        R.inmask = d.kind == SA_FILTER ? d.in_ch_mask : nullptr;
+        R.B = (int)d.B;
+        R.divCD = make_fastdiv((uint32_t)p.CD);
         R.scores = d.scores ? d.scores : (p.off_scores != SIZE_MAX ? ws_at<double>(ws, p.off_scores) : nullptr);
         R.A = (int)d.A;
         R.K = p.K;
@@ -1142,10 +1155,11 @@ int project_impl(const sa_project_desc *layers, int n_layers, void *ws, size_t w
         for (int i = 0; i < n_layers; ++i)
             if (level[i] == lv) ids.push_back(i);
 
-        // allowed bytes for layers with a channel support
+        // allowed bytes for layers with a channel support (filter sets read
+        // the mask itself)
         for (int i : ids) {
             const sa_project_desc &d = layers[i];
-            if (!d.in_ch_mask) continue;
+            if (!d.in_ch_mask || d.kind == SA_FILTER) continue;
             const LayerPlan &p = plan[i];
             int64_t total = (int64_t)d.groups * p.K;
             int blocks = (int)std::min<int64_t>(1024, (total + 255) / 256);
@@ -1228,7 +1242,7 @@ int project_impl(const sa_project_desc *layers, int n_layers, void *ws, size_t w
                     L.mask = d.mask;
                     L.kept_idx = d.kept_idx;
                     L.colkeep = p.off_colkeep != SIZE_MAX ? ws_at<uint8_t>(ws, p.off_colkeep) : nullptr;
-                    L.allowed = d.in_ch_mask ? ws_at<uint8_t>(ws, p.off_allowed) : nullptr;
+                    L.allowed = p.off_allowed != SIZE_MAX ? ws_at<uint8_t>(ws, p.off_allowed) : nullptr;
                     L.kind = d.kind;
                     L.G = (int)p.G;
                     L.k = (int)d.k;
@@ -1306,10 +1320,13 @@ int project_impl(const sa_project_desc *layers, int n_layers, void *ws, size_t w
                 ApplyLayer &L = tab.L[t];
                 L.W = R.W;
                 L.U = R.U;
-                L.Z = R.Z;
-                L.G = R.G;
-                L.rowkeep = R.rowkeep;
-                L.colkeep = R.colkeep;
+                L.Z = d.Z;
+                L.G = d.G;
+                L.rowkeep = d.kind == SA_FILTER ? d.mask : nullptr;
+                L.colkeep = d.kind == SA_FILTER ? nullptr : ws_at<uint8_t>(ws, plan[sl[s + t]].off_colkeep);
+                L.inmask = R.inmask;
+                L.B = R.B;
+                L.divCD = R.divCD;
                 L.divK = make_fastdiv((uint32_t)R.K);
                 L.divAg = make_fastdiv((uint32_t)R.Ag);
                 L.n = (int32_t)(d.A * d.B * d.C * d.D);
