@@ -263,7 +263,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
                 const int e0 = c * 8;
                 const uint4 v = *reinterpret_cast<const uint4 *>(sC + e0);
                 if (e0 + 8 <= total) {
-                    *reinterpret_cast<uint4 *>(base + e0) = v;
+                    nt_store16(base + e0, v);
                 } else {
                     const uint16_t *s = sC + e0;
                     for (int q = 0; e0 + q < total; ++q) base[e0 + q] = s[q];
@@ -282,7 +282,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
             const uint16_t *s = sC + pl * CP + ci * 8;
             uint16_t *dst = a.Y + e0 + lo;
             if (lo >= 0 && lo + 8 <= count) {
-                *reinterpret_cast<uint4 *>(dst) = *reinterpret_cast<const uint4 *>(s);
+                nt_store16(dst, *reinterpret_cast<const uint4 *>(s));
             } else {
 #pragma unroll
                 for (int q = 0; q < 8; ++q)
@@ -565,7 +565,7 @@ __global__ __launch_bounds__(256 * KG) void k_igk(IgArgs a) {
             const int e0 = c * 8;
             const uint4 v = *reinterpret_cast<const uint4 *>(sC + e0);
             if (e0 + 8 <= total) {
-                *reinterpret_cast<uint4 *>(base + e0) = v;
+                nt_store16(base + e0, v);
             } else {
                 const uint16_t *s = sC + e0;
                 for (int q = 0; e0 + q < total; ++q) base[e0 + q] = s[q];
@@ -583,7 +583,7 @@ __global__ __launch_bounds__(256 * KG) void k_igk(IgArgs a) {
         const uint16_t *s = sC + pl * CP + ci * 8;
         uint16_t *dst = a.Y + e0 + lo;
         if (lo >= 0 && lo + 8 <= count) {
-            *reinterpret_cast<uint4 *>(dst) = *reinterpret_cast<const uint4 *>(s);
+            nt_store16(dst, *reinterpret_cast<const uint4 *>(s));
         } else {
 #pragma unroll
             for (int q = 0; q < 8; ++q)

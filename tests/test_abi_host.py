@@ -201,11 +201,14 @@ def test_compact_and_conv_validation():
                                              col_tap=FAKE, Y=FAKE, ws=None, ws_bytes=0), **kw})
     assert L.structadmm_conv_workspace(ctypes.byref(desc(Cx=8))) == 0
     # channels not 8-aligned: the input's space-to-depth image (here stride 1: the
-    # zero border folded in, 2 channels padded to 8) goes to caller scratch
+    # zero border folded in, 2 channels padded to 8) goes to caller scratch, then
+    # the 4 kept rows rewritten over the image's taps x channels (3x3 taps of 8
+    # channels = 72 columns, rows of 128)
     need = L.structadmm_conv_workspace(ctypes.byref(desc()))
-    assert need == (10 * 10 * 8 * 2 + 255) // 256 * 256
+    assert need == (10 * 10 * 8 * 2 + 255) // 256 * 256 + 4 * 128 * 2
     s2 = L.structadmm_conv_workspace(ctypes.byref(desc(stride=2)))
-    assert s2 == (5 * 5 * 8 * 2 + 255) // 256 * 256  # 2x2 blocks of 2 channels: 8 channels
+    # 2x2 blocks of 2 channels: 8 channels; 2x2 taps of them: 32 columns, rows of 64
+    assert s2 == (5 * 5 * 8 * 2 + 255) // 256 * 256 + 4 * 64 * 2
     assert conv() == -3
     assert conv(ws=FAKE + 2048, ws_bytes=need - 1) == -3
     assert conv(ws=FAKE + 2048 + 16, ws_bytes=need) == -2
@@ -245,9 +248,20 @@ def test_conv_plan_host_only():
     # batch 1: split over the columns
     rc, info = plan(1, 13, 13, 256, 3, 3, 1, 1, 384, run=256)
     assert rc == 0 and info.ksplit > 1
-    # 3 input channels: the space-to-depth image and the footprint kernel
+    # 3 input channels: the space-to-depth image, then the direct kernels over
+    # its taps x channels
     rc, info = plan(2, 30, 28, 3, 7, 7, 2, 3, 12, cols=147)
-    assert rc == 0 and list(info.path)[:1] == [sa.CONV_FOOTPRINT] and info.space_to_depth == 2
+    assert rc == 0 and list(info.path)[:1] in ([sa.CONV_DIRECT], [sa.CONV_DIRECT_IG]) and info.space_to_depth == 2
+    # the same image under two conv groups: the footprint kernel
+    s.groups = 2
+    s.M[1], s.K[1], s.ldk[1], s.run[1], s.run_base[1], s.ch_lo[1], s.ch_span[1] = 12, 49, 64, 0, 0, 2, 1
+    s.wc_offset[1], s.row_offset[1], s.col_offset[1] = 12 * 64, 12, 49
+    d = sa.ConvDesc(2, 30, 28, 3, 7, 7, 2, 3, ctypes.pointer(s), FAKE, FAKE, FAKE, FAKE, FAKE, None, 0)
+    s.M[0], s.K[0], s.ldk[0], s.run[0], s.ch_lo[0], s.ch_span[0] = 12, 98, 128, 0, 0, 2
+    info = sa.ConvPlanInfo()
+    assert L.structadmm_conv_plan(ctypes.byref(d), ctypes.byref(info)) == 0
+    assert list(info.path)[:2] == [sa.CONV_FOOTPRINT] * 2 and info.space_to_depth == 2
+    s.groups = 1
     # arbitrary columns over 8-aligned channels: the footprint kernel
     rc, info = plan(8, 13, 13, 64, 3, 3, 1, 1, 48, cols=100)
     assert rc == 0 and list(info.path)[:1] == [sa.CONV_FOOTPRINT] and info.space_to_depth == 0

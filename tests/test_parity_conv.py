@@ -201,8 +201,13 @@ PLANNED = [
     ((128, 384, 13, 13, 384, 3, 3, 1, 1, 2, sa.SHAPE, 0.3), {"path": {sa.CONV_FOOTPRINT}, "footprint_tile": (6, 1, 6)}),
     ((400, 16, 13, 13, 128, 3, 3, 1, 1, 1, sa.SHAPE, 0.3), {"path": {sa.CONV_FOOTPRINT}, "footprint_tile": (4, 1, 4)}),
     ((2, 32, 13, 13, 48, 3, 3, 1, 1, 2, sa.SHAPE, 0.3), {"path": {sa.CONV_FOOTPRINT}}),
-    # stem: space-to-depth image, then the footprint kernel
-    ((2, 3, 30, 28, 20, 7, 7, 2, 3, 1, sa.FILTER, 0.6), {"path": {sa.CONV_FOOTPRINT}, "space_to_depth": 2}),
+    # stem: space-to-depth image, then the direct kernels over every tap and
+    # channel of the image (weights rewritten in that column order)
+    ((2, 3, 30, 28, 20, 7, 7, 2, 3, 1, sa.FILTER, 0.6), {"path": {sa.CONV_DIRECT}, "space_to_depth": 2}),
+    ((64, 3, 60, 60, 40, 7, 7, 2, 3, 1, sa.FILTER, 0.6), {"path": {sa.CONV_DIRECT}, "space_to_depth": 2, "ksplit": 1}),
+    ((8, 3, 67, 67, 96, 11, 11, 4, 0, 1, sa.SHAPE, 0.3), {"space_to_depth": 4}),
+    # grouped layer on a space-to-depth image: the footprint kernel
+    ((2, 4, 16, 16, 24, 3, 3, 2, 1, 2, sa.SHAPE, 0.5), {"path": {sa.CONV_FOOTPRINT}, "space_to_depth": 2}),
 ]
 
 
