@@ -1107,7 +1107,9 @@ int direct_pick(const int *Ms, int n, int NPQ, int K, int64_t *blocks) {
 // for groups of at most 32 filters; else the least padded filter work first and,
 // among those, 128 x 128 tiles while the launch has at least 320 of them, else
 // the shape with the most tiles (more wavefronts per CU hide the operand
-// latency better than bigger tiles save LDS reads), the 64-pixel one on a tie.
+// latency better than bigger tiles save LDS reads), the 64-pixel one on a tie;
+// 128 x 128 over at least 512 columns becomes 256 x 128 (eight wavefronts)
+// while that keeps 128 tiles.
 int run_conv(ConvArgs a, hipStream_t stream) {
     if (a.ngroups == 0) return SA_OK;
     for (int i = 0; i < a.ngroups; ++i)
