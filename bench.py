@@ -997,7 +997,7 @@ def progress(msg):
 
 
 # source file of each CONV kernel (its profile summaries hold that file's hash)
-KERNEL_SOURCE = {"k_conv": "conv.hip", "k_conv_patch": "conv.hip", "k_ig": "conv_ig.hip", "k_igk": "conv_ig.hip"}
+KERNEL_SOURCE = {"k_conv": "conv.hip", "k_conv_patch": "conv.hip", "k_ig": "conv_ig.hip"}
 
 
 def kernel_of(sa, plan):
@@ -1011,7 +1011,7 @@ def kernel_of(sa, plan):
     if p == sa.CONV_DIRECT:
         return "k_conv"
     if p == sa.CONV_DIRECT_IG:
-        return "k_igk" if plan["ig_tile"][3] > 1 else "k_ig"
+        return "k_ig"
     if p == sa.CONV_FOOTPRINT:
         return "k_conv_patch"
     return None

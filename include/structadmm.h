@@ -342,8 +342,8 @@ typedef struct sa_conv_plan_info {
     int32_t ksplit;                   /* > 1: columns split over workgroups (small batch) */
     int32_t space_to_depth;           /* stride of the space-to-depth image, 0 = none     */
     int32_t ig_tile[4];               /* SA_CONV_DIRECT_IG: MT, NF, WM = 16*MT*WM filters by
-                                         64*NF/WM pixels per tile, KG = K-groups of four
-                                         wavefronts that share a tile (1: no split)        */
+                                         64*NF/WM pixels per tile, and 1 (every tile
+                                         runs whole in one workgroup of four wavefronts)  */
     int32_t footprint_tile[3];        /* SA_CONV_FOOTPRINT: TM, TN, NW = 32*TM filters by
                                          32*NW*TN pixels per workgroup                    */
 } sa_conv_plan_info;

@@ -1049,67 +1049,44 @@ int launch_conv(ConvArgs a, hipStream_t stream) {
     return check_hip(hipGetLastError(), "k_conv");
 }
 
-// Tile shape of the direct kernel for groups of Ms filters over NPQ pixels
-// and up to K columns: 0 = 128 x 128, 1 = 128 x 64, 2 = 64 x 128 (pixels x
-// filters), 3 = 256 x 32, 4 = 256 x 128 (eight wavefronts); *blocks receives
-// the tile count.
-int direct_pick(const int *Ms, int n, int NPQ, int K, int64_t *blocks) {
-    struct Shape {
-        int BM, BN;
-    };
-    constexpr Shape shapes[4] = {{128, 128}, {128, 64}, {64, 128}, {256, 32}};
+// Tile shape of the direct kernel for groups of Ms filters over NPQ pixels:
+// 0 = 128 x 128, 1 = 128 x 64 (pixels x filters; eight wavefronts, two
+// workgroups per CU by LDS), 2 = 256 x 32 (four wavefronts) for groups of at
+// most 32 filters; *blocks receives the tile count.  The slowest CU runs
+// ceil(tiles / CUs) tiles, and a 128 x 64 tile takes about 3/4 of the time of
+// a 128 x 128 one (0.53-0.87 measured over the ResNet-50 and AlexNet layers,
+// most near 0.75), so 128 x 64 tiles when 3 rounds of them cost no more than
+// 4 rounds of 128 x 128 ones.
+int direct_pick(const int *Ms, int n, int NPQ, int64_t *blocks) {
     int maxM = 0;
-    for (int i = 0; i < n; ++i) maxM = std::max(maxM, Ms[i]);
-    int64_t work[3], nb[4], best = -1;
-    for (int c = 0; c < 4; ++c) {
-        int64_t mt = 0, pm = 0;
-        for (int i = 0; i < n; ++i) {
-            const int t = (Ms[i] + shapes[c].BN - 1) / shapes[c].BN;
-            mt += t;
-            pm += (int64_t)t * shapes[c].BN;
-        }
-        nb[c] = mt * ((NPQ + shapes[c].BM - 1) / shapes[c].BM);
-        if (c < 3) {
-            work[c] = pm;
-            if (best < 0 || pm < best) best = pm;
-        }
+    int64_t t128 = 0, t64 = 0, t32 = 0;
+    for (int i = 0; i < n; ++i) {
+        maxM = std::max(maxM, Ms[i]);
+        t128 += (Ms[i] + 127) / 128;
+        t64 += (Ms[i] + 63) / 64;
+        t32 += (Ms[i] + 31) / 32;
     }
     if (maxM <= 32) {
-        *blocks = nb[3];
-        return 3;
+        *blocks = t32 * ((NPQ + 255) / 256);
+        return 2;
     }
-    auto near = [&](int c) { return work[c] * 50 <= best * 51; };  // within 2% of the least work
-    int pick = -1;
-    if (near(0) && nb[0] >= 320) {
-        pick = 0;
-    } else {
-        for (int c : {2, 1, 0})
-            if (near(c) && (pick < 0 || nb[c] > nb[pick])) pick = c;
+    const int64_t ptiles = (NPQ + 127) / 128, cus = device_cus();
+    t128 *= ptiles;
+    t64 *= ptiles;
+    const int64_t r128 = (t128 + cus - 1) / cus, r64 = (t64 + cus - 1) / cus;
+    if (3 * r64 <= 4 * r128) {
+        *blocks = t64;
+        return 1;
     }
-    // 128 x 128 tiles over at least 512 columns: 256 x 128 ones (eight
-    // wavefronts, one workgroup per CU) load each weight slice for twice the
-    // pixels, as long as the launch keeps 128 tiles (measured on ResNet-50 and
-    // AlexNet: 4-21% faster on those layers, slower with fewer columns)
-    if (pick == 0 && K >= 512) {
-        int64_t mt = 0;
-        for (int i = 0; i < n; ++i) mt += (Ms[i] + 127) / 128;
-        const int64_t nb4 = mt * ((NPQ + 255) / 256);
-        if (nb4 >= 128) {
-            *blocks = nb4;
-            return 4;
-        }
-    }
-    *blocks = nb[pick];
-    return pick;
+    *blocks = t128;
+    return 0;
 }
 
-// One launch for every group of a.  Tile shape (measured on gfx950): 256 x 32
-// for groups of at most 32 filters; else the least padded filter work first and,
-// among those, 128 x 128 tiles while the launch has at least 320 of them, else
-// the shape with the most tiles (more wavefronts per CU hide the operand
-// latency better than bigger tiles save LDS reads), the 64-pixel one on a tie;
-// 128 x 128 over at least 512 columns becomes 256 x 128 (eight wavefronts)
-// while that keeps 128 tiles.
+// One launch for every group of a, in direct_pick's tile shape.  Eight
+// wavefronts per 128-pixel tile (two rows of four, each 32 pixels by 32 or 64
+// filters) keep 16 wavefronts per CU in flight to cover the operand latency:
+// over 94 ResNet-50 layer runs they took 0.73-1.05x (15% less in sum) of the
+// time of four-wavefront tiles of the same size.
 int run_conv(ConvArgs a, hipStream_t stream) {
     if (a.ngroups == 0) return SA_OK;
     for (int i = 0; i < a.ngroups; ++i)
@@ -1118,18 +1095,13 @@ int run_conv(ConvArgs a, hipStream_t stream) {
     a.divCy = make_fastdiv((uint32_t)std::max(1, a.Cy));
     a.divQ = make_fastdiv((uint32_t)a.Q);
     a.divD = make_fastdiv((uint32_t)a.D);
-    int Ms[SA_MAX_CONV_GROUPS], maxK = 0;
-    for (int i = 0; i < a.ngroups; ++i) {
-        Ms[i] = a.g[i].M;
-        maxK = std::max(maxK, a.g[i].K);
-    }
+    int Ms[SA_MAX_CONV_GROUPS];
+    for (int i = 0; i < a.ngroups; ++i) Ms[i] = a.g[i].M;
     int64_t blocks;
-    switch (direct_pick(Ms, a.ngroups, a.NPQ, maxK, &blocks)) {
-        case 0: return launch_conv<128, 128, 2, 2>(a, stream);
-        case 1: return launch_conv<128, 64, 2, 2>(a, stream);
-        case 3: return launch_conv<256, 32, 4, 1>(a, stream);
-        case 4: return launch_conv<256, 128, 4, 2>(a, stream);
-        default: return launch_conv<64, 128, 1, 4>(a, stream);
+    switch (direct_pick(Ms, a.ngroups, a.NPQ, &blocks)) {
+        case 0: return launch_conv<128, 128, 4, 2>(a, stream);
+        case 1: return launch_conv<128, 64, 4, 2>(a, stream);
+        default: return launch_conv<256, 32, 4, 1>(a, stream);
     }
 }
 
@@ -1303,28 +1275,25 @@ int patch_lds(int TM, int TN, int patch_bytes, int tab_bytes, int NW = 4) {
 void split_plan(const sa_compact_sizes &s, ConvPlan *pl) {
     ConvPlan &p = *pl;
     p.ksplit = 1;
-    int nd = 0, ng = 0, Md[SA_MAX_CONV_GROUPS], Mg[SA_MAX_CONV_GROUPS], Kd = 0, Kg = 0;
+    int nd = 0, ng = 0, Md[SA_MAX_CONV_GROUPS], Mg[SA_MAX_CONV_GROUPS];
     int min_sl = 1 << 30;
     for (int g = 0; g < s.groups; ++g) {
         if (p.path[g] == kSkip) continue;
         if (p.path[g] == kPatch) return;
-        if (p.path[g] == kDirect) {
+        if (p.path[g] == kDirect)
             Md[nd++] = s.M[g];
-            Kd = std::max(Kd, s.K[g]);
-        } else {  // two-phase: the direct kernel over the gathered rows
+        else  // two-phase: the direct kernel over the gathered rows
             Mg[ng++] = s.M[g];
-            Kg = std::max(Kg, s.ldk[g]);
-        }
         min_sl = std::min(min_sl, s.ldk[g] / kBK);
     }
     if (nd + ng == 0) return;
     int64_t base = 0, b;
     if (nd > 0) {
-        direct_pick(Md, nd, p.NPQ, Kd, &b);
+        direct_pick(Md, nd, p.NPQ, &b);
         base += b;
     }
     if (ng > 0) {
-        direct_pick(Mg, ng, p.NPQ, Kg, &b);
+        direct_pick(Mg, ng, p.NPQ, &b);
         base += b;
     }
     if (base >= 128) return;
@@ -1338,34 +1307,33 @@ void split_plan(const sa_compact_sizes &s, ConvPlan *pl) {
 
 // Kernel for the groups read straight from the NHWC input (measured on
 // gfx950 over the ResNet-50 and AlexNet layers): k_ig, whose filter tiles grow
-// in steps of 16, when the kept-filter counts are ragged enough that k_conv's
-// 32/64/128-filter tiles would pad the filter work by 15% or more, and either
-// the columns are few (at most 512 per group: 1x1 CONVs and small 3x3 ones,
-// bound by memory, where the padding is pure loss) or k_conv would have fewer
-// than 1024 tiles (late ResNet stages, where k_ig splits the columns over
-// the wavefronts of a workgroup); k_conv's larger LDS-staged tiles otherwise.
-// Not for split K over workgroups (batch 1).
+// in steps of 16, when k_conv's 64- or 128-filter tiles would pad the filter
+// work by 15% or more over 256-512 columns and at least 2^16 pixels, with
+// more than 64 kept filters or at least 384 columns (k_conv's 128 x 64 tiles
+// are the faster ones below that: 1x1 layers over 64 channels, ResNet-50's
+// first layer); the eight-wavefront k_conv tiles otherwise (k_ig ran 5-25%
+// slower on every other layer).  Not for split K over workgroups (batch 1).
 void direct_plan(const sa_compact_sizes &s, ConvPlan *pl) {
     ConvPlan &p = *pl;
     p.direct_ig = false;
     if (p.ksplit > 1) return;
-    int Ms[SA_MAX_CONV_GROUPS], n = 0, maxK = 0;
+    int Ms[SA_MAX_CONV_GROUPS], n = 0, maxK = 0, maxM = 0;
     int64_t fine = 0;
     for (int g = 0; g < s.groups; ++g) {
         if (p.path[g] != kDirect) continue;
         maxK = std::max(maxK, s.K[g]);
+        maxM = std::max(maxM, s.M[g]);
         Ms[n++] = s.M[g];
         fine += (s.M[g] + 15) / 16 * 16;
     }
     if (n == 0) return;
     int64_t blocks;
-    constexpr int kBN[5] = {128, 64, 128, 32, 128};
-    const int pick = direct_pick(Ms, n, p.NPQ, maxK, &blocks);
-    if (pick == 4) return;  // the eight-wavefront tiles (k_ig measured slower there)
-    const int BN = kBN[pick];
+    constexpr int kBN[3] = {128, 64, 32};
+    const int BN = kBN[direct_pick(Ms, n, p.NPQ, &blocks)];
     int64_t coarse = 0;
     for (int i = 0; i < n; ++i) coarse += (int64_t)(Ms[i] + BN - 1) / BN * BN;
-    p.direct_ig = coarse * 100 >= fine * 115 && (maxK <= 512 || blocks < 1024);
+    p.direct_ig = coarse * 100 >= fine * 115 && maxK >= 256 && maxK <= 512 && p.NPQ >= (1 << 16) &&
+                  (maxM > 64 || maxK >= 384);
 }
 
 // Validates the descriptor (beyond validate_conv) and chooses, per conv group,
@@ -1628,7 +1596,7 @@ extern "C" int structadmm_conv_plan(const sa_conv_desc *desc, sa_conv_plan_info 
             if (p.path[g] == kDirect) ia.g[i++].ldk = p.eff.ldk[g];
         const int t = ig_pick(ia);
         ig_tile_shape(t, &info->ig_tile[0], &info->ig_tile[1], &info->ig_tile[2]);
-        info->ig_tile[3] = ig_split(ia, t);
+        info->ig_tile[3] = 1;
     }
     bool patch = false;
     for (int g = 0; g < s.groups; ++g) patch = patch || p.path[g] == kPatch;

@@ -39,8 +39,8 @@ int ig_pick(const IgArgs &a);
 // Number of tile shapes the launcher has, and the shape of tile t.
 int ig_num_tiles();
 void ig_tile_shape(int t, int *MT, int *NF, int *WM);
-// K-groups per workgroup the launcher takes for tile t (1: no split).
-int ig_split(const IgArgs &a, int t);
+// Compute units of the current device (256 when it cannot be asked).
+int device_cus();
 // Launches every group of a (tile < 0: ig_pick's choice).
 int ig_run(IgArgs a, int tile, hipStream_t stream);
 

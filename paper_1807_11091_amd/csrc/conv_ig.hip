@@ -349,249 +349,6 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
     }
 }
 
-// ---------------------------------------------------------------- split K
-// k_igk: one tile per workgroup of KG * 4 wavefronts.  K-group g (wavefronts
-// 4g .. 4g+3) multiplies the 64-column slices g, g + KG, g + 2 KG, ... of the
-// tile with its own pair of LDS weight buffers, all groups in step (a group
-// out of slices idles through the last barriers).  The partial sums of
-// groups 1 .. KG-1 are added to group 0's in group order through LDS (fixed
-// order: identical inputs give identical bits), and the tile's output then
-// leaves as in k_ig.  For launches with fewer tiles than the GPU has
-// workgroup slots: more wavefronts per CU hide the loads' latency.
-template <int MT, int NF, int WM, int KG>
-struct IgkCfg {
-    using Base = IgCfg<MT, NF, WM>;
-    static constexpr int NT = 256 * KG;
-    static constexpr int a_bytes = KG * Base::a_bytes;                  // [KG][2][BM][kARow]
-    static constexpr int r_bytes = (KG - 1) * 4 * MT * NF * 4 * 64 * 4;  // partial sums of groups 1..KG-1
-    static constexpr int c_bytes = Base::c_bytes;
-    static constexpr int lds = (a_bytes > r_bytes ? a_bytes : r_bytes) + c_bytes;
-    static_assert(lds <= kLdsMax, "LDS");
-};
-
-template <int MT, int NF, int WM, int KG>
-__global__ __launch_bounds__(256 * KG) void k_igk(IgArgs a) {
-    using Base = IgCfg<MT, NF, WM>;
-    using Cfg = IgkCfg<MT, NF, WM, KG>;
-    constexpr int WN = Base::WN, BM = Base::BM, BP = Base::BP, AR = Base::AR, CP = Base::CP;
-
-    extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
-    const int tid = threadIdx.x;
-    const int lane = tid & 63, wave = tid >> 6;
-    const int kg = wave >> 2, w4 = wave & 3, t4 = tid & 255;
-    const int wm = w4 / WN, wn = w4 - wm * WN;
-    const int kq = lane >> 4;
-    uint16_t *sA = reinterpret_cast<uint16_t *>(smem) + kg * 2 * BM * kARow;  // this group's [2][BM][kARow]
-    float *sR = reinterpret_cast<float *>(smem);                                // [KG-1][4][MT*NF*4][64], after the loop
-    uint16_t *sC = reinterpret_cast<uint16_t *>(smem + (Cfg::a_bytes > Cfg::r_bytes ? Cfg::a_bytes : Cfg::r_bytes));
-
-    const int t = xcd_remap(blockIdx.x, gridDim.x);
-    const TilePos P = tile_pos<BM, BP>(a, t);
-    const IgGroup &G = a.g[P.gi];
-    const int nst = P.nst;
-    const int nsl = (nst + KG - 1) / KG;  // slice slots per group
-
-    // weights: slice s of the tile into this group's registers
-    const __amdgpu_buffer_rsrc_t wrs = rsrc(G.Wc, (uint32_t)G.M * (uint32_t)G.ldk * 2u);
-    uint4 areg[AR];
-    auto a_load = [&](int slot) {
-        const int s = kg + slot * KG;
-        if (s >= nst) return;
-#pragma unroll
-        for (int i = 0; i < AR; ++i) {
-            const int c = t4 + i * 256;
-            const uint32_t off = ((uint32_t)(P.m0 + (c >> 3)) * (uint32_t)G.ldk + s * kStage + (c & 7) * 8) * 2u;
-            areg[i] = bload16(wrs, c < BM * 8 ? off : kInvalidOffset);
-        }
-    };
-    auto a_store = [&](int buf) {
-#pragma unroll
-        for (int i = 0; i < AR; ++i) {
-            const int c = t4 + i * 256;
-            if (c < BM * 8) *reinterpret_cast<uint4 *>(&sA[(buf * BM + (c >> 3)) * kARow + (c & 7) * 8]) = areg[i];
-        }
-    };
-
-    // activations: this lane's pixels; the column state of the next step to
-    // load (k = tap * run + ch, tap = c * D + d, delta = (c*W + d)*Cx + ch)
-    const __amdgpu_buffer_rsrc_t xrs = rsrc(a.X, a.x_bytes);
-    int hb[NF], wb[NF], pbase[NF];
-#pragma unroll
-    for (int j = 0; j < NF; ++j) {
-        const int px = P.p0 + (wn * NF + j) * 16 + (lane & 15);
-        const int pxc = min(px, a.NPQ - 1);
-        const int n = (int)fdiv((uint32_t)pxc, a.divPQ);
-        const int rem = pxc - n * a.P * a.Q;
-        const int p = (int)fdiv((uint32_t)rem, a.divQ);
-        const int q = rem - p * a.Q;
-        const int h0 = p * a.stride - a.pad, w0 = q * a.stride - a.pad;
-        pbase[j] = ((n * a.H + h0) * a.W + w0) * a.Cx + G.run_base;
-        hb[j] = px < a.NPQ ? h0 : -(1 << 28);
-        wb[j] = w0;
-    }
-    int nk = 0, nch = 0, nc = 0, nd = 0, ndelta = 0;
-    auto advance = [&](int by) {
-        nk += by;
-        nch += by;
-        ndelta += by;
-        while (nch >= G.run) {
-            nch -= G.run;
-            ndelta += a.Cx - G.run;
-            if (++nd == a.D) {
-                nd = 0;
-                ++nc;
-                ndelta += (a.W - a.D) * a.Cx;
-            }
-        }
-    };
-    advance(kg * kStage + kq * 8);
-    int sB = 0;  // steps of this group loaded so far (2 per slice slot)
-    uint4 b[4][NF];
-    auto b_load = [&](auto slot_c) {
-        constexpr int SLOT = decltype(slot_c)::value;
-        if (sB >= 2 * nsl) return;
-        const bool valid = kg + (sB >> 1) * KG < nst;  // a group's last slot may be idle
-        const bool kin = valid && nk < G.K;
-#pragma unroll
-        for (int j = 0; j < NF; ++j) {
-            const int h = hb[j] + nc, w = wb[j] + nd;
-            const bool in = kin && (unsigned)h < (unsigned)a.H && (unsigned)w < (unsigned)a.W;
-            b[SLOT][j] = bload16(xrs, in ? (uint32_t)(pbase[j] + ndelta) * 2u : kInvalidOffset);
-        }
-        // within a slice: the next 32 columns; at its end: the group's next slice
-        advance((sB & 1) ? 32 + (KG - 1) * kStage : 32);
-        ++sB;
-    };
-
-    f32x4 acc[MT][NF];
-#pragma unroll
-    for (int i = 0; i < MT; ++i)
-#pragma unroll
-        for (int j = 0; j < NF; ++j) acc[i][j] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-    auto compute = [&](auto slot_c, int buf, int kk, int slot) {
-        constexpr int SLOT = decltype(slot_c)::value;
-        if (kg + slot * KG >= nst) return;  // idle slot of this group
-        const uint16_t *A = sA + (buf * BM + wm * MT * 16 + (lane & 15)) * kARow + kk + kq * 8;
-#pragma unroll
-        for (int i = 0; i < MT; ++i) {
-            const bf16x8 af = *reinterpret_cast<const bf16x8 *>(A + i * 16 * kARow);
-#pragma unroll
-            for (int j = 0; j < NF; ++j)
-                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, __builtin_bit_cast(bf16x8, b[SLOT][j]),
-                                                                   acc[i][j], 0, 0, 0);
-        }
-    };
-
-    using S0 = std::integral_constant<int, 0>;
-    using S1 = std::integral_constant<int, 1>;
-    using S2 = std::integral_constant<int, 2>;
-    using S3 = std::integral_constant<int, 3>;
-    a_load(0);
-    b_load(S0{});
-    b_load(S1{});
-    b_load(S2{});
-    a_store(0);
-    a_load(1);
-    __syncthreads();
-    for (int sl = 0; sl < nsl; sl += 2) {
-        b_load(S3{});
-        compute(S0{}, 0, 0, sl);
-        b_load(S0{});
-        compute(S1{}, 0, 32, sl);
-        if (sl + 1 >= nsl) break;
-        a_store(1);
-        a_load(sl + 2);
-        __syncthreads();
-        b_load(S1{});
-        compute(S2{}, 1, 0, sl + 1);
-        b_load(S2{});
-        compute(S3{}, 1, 32, sl + 1);
-        if (sl + 2 >= nsl) break;
-        a_store(0);
-        a_load(sl + 3);
-        __syncthreads();
-    }
-    __syncthreads();  // every group is done with its weight buffers (sR overlays them)
-    // partial sums of groups 1 .. KG-1, then group 0 adds them in group order
-    constexpr int NACC = MT * NF * 4;
-    if (kg > 0) {
-        float *r = sR + ((kg - 1) * 4 + w4) * NACC * 64 + lane;
-#pragma unroll
-        for (int i = 0; i < MT; ++i)
-#pragma unroll
-            for (int j = 0; j < NF; ++j)
-#pragma unroll
-                for (int e = 0; e < 4; ++e) r[((i * NF + j) * 4 + e) * 64] = acc[i][j][e];
-    }
-    __syncthreads();
-    const int rows = min(BP, a.NPQ - P.p0);
-    // results, then +0 up to the padded pitch of a row's last channels
-    const int count = min(BM, (G.o_off + G.M == a.Cy ? a.ldy - G.o_off : G.M) - P.m0);
-    const bool whole = G.mtiles == 1 && G.M == a.Cy && a.yshift == 0 && a.ldy == a.Cy;
-    const int64_t e_tile = (int64_t)P.p0 * a.ldy + G.o_off + P.m0;
-    const int pitch = whole ? a.Cy : CP;
-    if (kg == 0) {
-#pragma unroll
-        for (int g = 1; g < KG; ++g) {
-            const float *r = sR + ((g - 1) * 4 + w4) * NACC * 64 + lane;
-#pragma unroll
-            for (int i = 0; i < MT; ++i)
-#pragma unroll
-                for (int j = 0; j < NF; ++j)
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) acc[i][j][e] += r[((i * NF + j) * 4 + e) * 64];
-        }
-#pragma unroll
-        for (int j = 0; j < NF; ++j) {
-            const int pl = (wn * NF + j) * 16 + (lane & 15);
-            const int sh = whole ? 0 : (int)((e_tile + (int64_t)pl * a.ldy + a.yshift) & 7);
-            uint16_t *row = sC + pl * pitch + sh;
-#pragma unroll
-            for (int i = 0; i < MT; ++i) {
-                const int ml = (wm * MT + i) * 16 + kq * 4;
-                uint16_t o[4];
-#pragma unroll
-                for (int e = 0; e < 4; ++e) o[e] = f32_to_bf16_bits(acc[i][j][e]);
-                if (ml >= count) continue;
-                stage_quad(row + ml, o, count - ml);
-            }
-        }
-    }
-    __syncthreads();
-    if (whole) {
-        const int total = rows * a.Cy;
-        uint16_t *base = a.Y + (int64_t)P.p0 * a.Cy;
-        for (int c = tid; c * 8 < total; c += Cfg::NT) {
-            const int e0 = c * 8;
-            const uint4 v = *reinterpret_cast<const uint4 *>(sC + e0);
-            if (e0 + 8 <= total) {
-                nt_store16(base + e0, v);
-            } else {
-                const uint16_t *s = sC + e0;
-                for (int q = 0; e0 + q < total; ++q) base[e0 + q] = s[q];
-            }
-        }
-        return;
-    }
-    constexpr int CPR = BM / 8 + 2;
-    for (int c = tid; c < rows * CPR; c += Cfg::NT) {
-        const int pl = c / CPR, ci = c - pl * CPR;
-        const int64_t e0 = e_tile + (int64_t)pl * a.ldy;
-        const int sh = (int)((e0 + a.yshift) & 7);
-        const int lo = ci * 8 - sh;
-        if (lo >= count) continue;
-        const uint16_t *s = sC + pl * CP + ci * 8;
-        uint16_t *dst = a.Y + e0 + lo;
-        if (lo >= 0 && lo + 8 <= count) {
-            nt_store16(dst, *reinterpret_cast<const uint4 *>(s));
-        } else {
-#pragma unroll
-            for (int q = 0; q < 8; ++q)
-                if (lo + q >= 0 && lo + q < count) dst[q] = s[q];
-        }
-    }
-}
-
 struct Tile {
     int MT, NF, WM;
 };
@@ -601,20 +358,6 @@ constexpr Tile kTiles[] = {
     {4, 4, 1}, {3, 2, 2}, {4, 2, 2}, {5, 2, 2}, {4, 1, 2}, {5, 1, 2},
 };
 constexpr int kNumTiles = sizeof(kTiles) / sizeof(kTiles[0]);
-
-int device_cus() {
-    static std::mutex mu;
-    static int cus[64] = {};
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-    std::lock_guard<std::mutex> lock(mu);
-    if (cus[dev] == 0) {
-        int n = 0;
-        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
-        cus[dev] = n;
-    }
-    return cus[dev];
-}
 
 template <int MT, int NF, int WM>
 int launch(IgArgs a, hipStream_t stream) {
@@ -652,58 +395,6 @@ int launch(IgArgs a, hipStream_t stream) {
     return check_hip(hipGetLastError(), "k_ig");
 }
 
-// the split-K kernel: one tile per workgroup of 256 * KG threads
-template <int MT, int NF, int WM, int KG>
-int launch_k(IgArgs a, hipStream_t stream) {
-    using Base = IgCfg<MT, NF, WM>;
-    using Cfg = IgkCfg<MT, NF, WM, KG>;
-    auto kern = k_igk<MT, NF, WM, KG>;
-    static std::once_flag once;
-    int rc = SA_OK;
-    if (Cfg::lds > 64 * 1024)
-        std::call_once(once, [&] {
-            rc = check_hip(hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
-                                               hipFuncAttributeMaxDynamicSharedMemorySize, Cfg::lds),
-                           "conv_ig: set LDS size");
-        });
-    if (rc) return rc;
-    const int ptiles = (a.NPQ + Base::BP - 1) / Base::BP;
-    int begin = 0;
-    for (int i = 0; i < a.ngroups; ++i) {
-        a.g[i].mtiles = (a.g[i].M + Base::BM - 1) / Base::BM;
-        a.g[i].begin = begin;
-        begin += a.g[i].mtiles * ptiles;
-    }
-    a.ntiles = begin;
-    hipLaunchKernelGGL(kern, dim3(a.ntiles), dim3(Cfg::NT), Cfg::lds, stream, a);
-    return check_hip(hipGetLastError(), "k_igk");
-}
-
-// split-K launch for tile t with KG groups, or SA_E_UNSUPPORTED when that
-// combination is not instantiated
-int launch_tile_k(int t, int KG, const IgArgs &a, hipStream_t stream) {
-    const Tile &T = kTiles[t];
-    const int key = ((T.MT * 10 + T.NF) * 10 + T.WM) * 10 + KG;
-    switch (key) {
-        case 3212: return launch_k<3, 2, 1, 2>(a, stream);
-        case 4212: return launch_k<4, 2, 1, 2>(a, stream);
-        case 5212: return launch_k<5, 2, 1, 2>(a, stream);
-        case 6212: return launch_k<6, 2, 1, 2>(a, stream);
-        case 8212: return launch_k<8, 2, 1, 2>(a, stream);
-        case 4222: return launch_k<4, 2, 2, 2>(a, stream);
-        case 5222: return launch_k<5, 2, 2, 2>(a, stream);
-        case 3214: return launch_k<3, 2, 1, 4>(a, stream);
-        default: return fail(SA_E_UNSUPPORTED, "conv_ig: no split-K kernel for tile %d, %d groups", t, KG);
-    }
-}
-
-bool has_tile_k(int t, int KG) {
-    const Tile &T = kTiles[t];
-    if (T.NF != 2 || (KG != 2 && KG != 4)) return false;
-    if (T.WM == 1) return KG == 2 ? (T.MT == 3 || T.MT == 4 || T.MT == 5 || T.MT == 6 || T.MT == 8) : T.MT == 3;
-    return T.WM == 2 && (T.MT == 4 || T.MT == 5) && KG == 2;
-}
-
 int launch_tile(int t, const IgArgs &a, hipStream_t stream) {
     switch (t) {
         case 0: return launch<2, 2, 1>(a, stream);
@@ -724,6 +415,20 @@ int launch_tile(int t, const IgArgs &a, hipStream_t stream) {
 }
 
 }  // namespace
+
+int device_cus() {
+    static std::mutex mu;
+    static int cus[64] = {};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+    std::lock_guard<std::mutex> lock(mu);
+    if (cus[dev] == 0) {
+        int n = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+        cus[dev] = n;
+    }
+    return cus[dev];
+}
 
 // Tile shape for a launch (measured on gfx950 over the ResNet-50 and AlexNet
 // layers): the least padded filter work first (rows pad to the tile's BM,
@@ -763,26 +468,6 @@ int ig_pick(const IgArgs &a) {
     return best;
 }
 
-// K-groups per workgroup for tile t: when the launch has fewer tiles than
-// the GPU has slots for two workgroups per CU, 2 or 4 groups (as many as
-// keep at least two 64-column slices per group and the tiles times groups
-// within 4 per CU); else 1 (the persistent kernel).
-int ig_split(const IgArgs &a, int t) {
-    const Tile &T = kTiles[t];
-    const int BM = T.WM * T.MT * 16, BP = (4 / T.WM) * T.NF * 16;
-    int64_t tiles = 0;
-    int nst = 1 << 30;
-    for (int i = 0; i < a.ngroups; ++i) {
-        tiles += (int64_t)(a.g[i].M + BM - 1) / BM * ((a.NPQ + BP - 1) / BP);
-        nst = std::min(nst, a.g[i].ldk / kStage);
-    }
-    const int64_t slots = 2 * (int64_t)device_cus();
-    if (tiles >= slots) return 1;
-    for (int kg : {4, 2})
-        if (has_tile_k(t, kg) && nst >= 2 * kg && tiles * kg <= 2 * slots) return kg;
-    return 1;
-}
-
 int ig_run(IgArgs a, int tile, hipStream_t stream) {
     if (a.ngroups == 0) return SA_OK;
     for (int i = 0; i < a.ngroups; ++i) a.g[i].divRun = make_fastdiv((uint32_t)std::max(1, a.g[i].run));
@@ -791,8 +476,7 @@ int ig_run(IgArgs a, int tile, hipStream_t stream) {
     a.divD = make_fastdiv((uint32_t)a.D);
     a.divCy = make_fastdiv((uint32_t)std::max(1, a.Cy));
     if (tile < 0) tile = ig_pick(a);
-    const int kg = ig_split(a, tile);
-    return kg > 1 ? launch_tile_k(tile, kg, a, stream) : launch_tile(tile, a, stream);
+    return launch_tile(tile, a, stream);
 }
 
 int ig_num_tiles() { return kNumTiles; }

@@ -238,10 +238,21 @@ def test_conv_plan_host_only():
         rc = L.structadmm_conv_plan(ctypes.byref(d), ctypes.byref(info))
         return rc, info
 
-    # 38 kept filters of a 1x1 layer over 64 channels, 56x56 at batch 64: the 16-row kernel
-    rc, info = plan(64, 56, 56, 64, 1, 1, 1, 0, 38, run=64)
+    # 77 kept filters of a 1x1 layer over 256 channels, 56x56 at batch 64: the
+    # 16-row kernel (128-filter tiles would pad the filter work by 66%)
+    rc, info = plan(64, 56, 56, 256, 1, 1, 1, 0, 77, run=256)
     assert rc == 0 and list(info.path)[:1] == [sa.CONV_DIRECT_IG] and info.ksplit == 1
-    assert tuple(info.ig_tile)[:3] == (3, 2, 1)
+    assert tuple(info.ig_tile) == (5, 2, 1, 1)
+    # 38 of 64 over 64 channels: the 128 x 64 tiles of the LDS-staged kernel
+    rc, info = plan(64, 56, 56, 64, 1, 1, 1, 0, 38, run=64)
+    assert rc == 0 and list(info.path)[:1] == [sa.CONV_DIRECT]
+    # 77 over 512 channels at 28x28: the LDS-staged kernel again
+    rc, info = plan(64, 28, 28, 512, 1, 1, 1, 0, 77, run=512)
+    assert rc == 0 and list(info.path)[:1] == [sa.CONV_DIRECT]
+    # 512 filters of a 3x3 layer at 7x7, batch 64: 128 x 64 tiles fill the
+    # GPU without splitting the columns
+    rc, info = plan(64, 7, 7, 512, 3, 3, 1, 1, 512, run=512)
+    assert rc == 0 and list(info.path)[:1] == [sa.CONV_DIRECT] and info.ksplit == 1
     # every filter of a 3x3 layer: the LDS-staged kernel
     rc, info = plan(64, 28, 28, 128, 3, 3, 1, 1, 128, run=128)
     assert rc == 0 and list(info.path)[:1] == [sa.CONV_DIRECT]

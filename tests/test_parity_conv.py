@@ -183,13 +183,14 @@ def test_conv_small(case):
 # cases pinned to a kernel and tile shape (the plan is asserted before the
 # parity check, so a change of the selection cannot silently move them)
 PLANNED = [
-    # ragged kept filters over few columns: the 16-row kernel (batches large
-    # enough that the launch is not split over its columns)
-    ((48, 64, 20, 20, 64, 1, 1, 1, 0, 1, sa.FILTER, 0.6), {"path": {sa.CONV_DIRECT_IG}, "ig_tile": (3, 2, 1, 1)}),
-    ((70, 32, 15, 17, 80, 3, 3, 1, 1, 1, sa.FILTER, 0.48), {"path": {sa.CONV_DIRECT_IG}, "ig_tile": (3, 2, 1, 2)}),
-    ((120, 64, 14, 14, 256, 1, 1, 2, 0, 1, sa.FILTER, 0.6), {"path": {sa.CONV_DIRECT_IG}, "ig_tile": (5, 2, 2, 1)}),
-    ((102, 96, 9, 9, 100, 1, 1, 1, 0, 1, sa.FILTER, 0.77), {"path": {sa.CONV_DIRECT_IG}, "ig_tile": (5, 2, 1, 1)}),
+    # ragged kept filters over 256-512 columns and at least 2^16 pixels: the
+    # 16-row kernel (ragged pixel tails: 65,856 and 73,728 pixels)
+    ((21, 256, 56, 56, 128, 1, 1, 1, 0, 1, sa.FILTER, 0.6), {"path": {sa.CONV_DIRECT_IG}, "ig_tile": (5, 2, 1, 1)}),
+    ((128, 48, 24, 24, 64, 3, 3, 1, 1, 1, sa.FILTER, 0.6), {"path": {sa.CONV_DIRECT_IG}, "ig_tile": (3, 2, 1, 1)}),
+    ((65, 256, 32, 32, 256, 1, 1, 1, 0, 1, sa.FILTER, 0.6), {"path": {sa.CONV_DIRECT_IG}, "ig_tile": (5, 2, 2, 1)}),
+    # the same filters over 512 columns or fewer pixels: the LDS-staged kernel
     ((70, 256, 14, 14, 512, 1, 1, 1, 0, 1, sa.FILTER, 0.6), {"path": {sa.CONV_DIRECT}}),
+    ((48, 64, 20, 20, 64, 1, 1, 1, 0, 1, sa.FILTER, 0.6), {"path": {sa.CONV_DIRECT}}),
     # every tap of a channel run, aligned or wide: the LDS-staged kernel
     ((114, 64, 12, 12, 128, 3, 3, 1, 1, 1, sa.FILTER, 1.0), {"path": {sa.CONV_DIRECT}}),
     ((114, 64, 12, 12, 96, 3, 3, 1, 1, 1, sa.FILTER, 0.6), {"path": {sa.CONV_DIRECT}}),
@@ -217,25 +218,26 @@ def test_conv_planned_kernel(case, expect):
 
 
 def test_conv_16row_tile_shapes():
-    """The 16-row kernel over 1x1 layers of 64 input channels at 40k pixels,
-    kept-filter counts that make its launcher take different tile shapes, all
-    against the oracle."""
+    """The 16-row kernel over 1x1 layers of 448 input channels at 65,856
+    pixels, kept-filter counts that make its launcher take different tile
+    shapes, all against the oracle."""
     seen = set()
-    for A, keep in ((64, 0.6), (128, 0.6), (256, 0.6), (512, 0.6), (160, 0.5), (1024, 0.6), (40, 0.5)):
+    rng = np.random.default_rng(448)
+    X = rng.standard_normal((21, 448, 56, 56)).astype(np.float32)
+    Xp = sa.pack_nhwc(to_dev(X))
+    for A, keep in ((64, 0.6), (128, 0.6), (256, 0.6), (512, 0.6), (160, 0.575), (1024, 0.6), (100, 0.6)):
         rng = np.random.default_rng(A + int(100 * keep))
-        X = rng.standard_normal((50, 64, 28, 28)).astype(np.float32)
         k = max(1, int(round(keep * A)))
         mask = np.zeros(A, np.uint8)
         mask[rng.choice(A, size=k, replace=False)] = 1
-        Z = (0.05 * rng.standard_normal((A, 64, 1, 1))).astype(np.float32)
+        Z = (0.05 * rng.standard_normal((A, 448, 1, 1))).astype(np.float32)
         Wc, ri, cc, ct, sizes = sa.compact(to_dev(Z), 1, row_mask=to_dev(mask))
-        Xp = sa.pack_nhwc(to_dev(X))
         plan = sa.conv_plan(Xp, sizes, 1, 1, 1, 0)
         if plan["path"] == [sa.CONV_DIRECT_IG]:
             seen.add(plan["ig_tile"])
         Y = sa.conv_fwd(Xp, Wc, cc, ct, sizes, 1, 1, 1, 0)
         rc = oracle.compact(Z, 1, row_mask=mask)
-        sel = [0, 17, 49]  # three images of the batch
+        sel = [0, 11, 20]  # three images of the batch
         Yr = oracle.conv(oracle.pack(X[sel]), rc, 1, 1, 1, 0)
         err = maxabs_over_rms(bf16_bits_to_f64(Y.cpu().numpy()[sel]), Yr)
         assert err <= TOL, (A, keep, plan, err)
@@ -508,8 +510,8 @@ def test_conv_on_a_non_current_stream():
 PITCH_CASES = [
     ("direct_whole_rows", 32, 64, 64, 64, 64, 3, 3, 1, 1, 1, sa.FILTER, 38, "k_conv"),
     ("direct_tiles", 32, 64, 64, 64, 256, 3, 3, 1, 1, 1, sa.FILTER, 154, "k_conv"),
-    ("ig_1x1", 8, 64, 28, 28, 64, 1, 1, 1, 0, 1, sa.FILTER, 38, "k_ig"),
-    ("igk", 16, 256, 28, 28, 256, 3, 3, 1, 1, 1, sa.FILTER, 154, "k_igk"),
+    ("ig_1x1", 21, 256, 56, 56, 128, 1, 1, 1, 0, 1, sa.FILTER, 77, "k_ig"),
+    ("ig_3x3", 128, 48, 24, 24, 64, 3, 3, 1, 1, 1, sa.FILTER, 38, "k_ig"),
     ("footprint", 4, 64, 20, 20, 96, 3, 3, 1, 1, 1, sa.SHAPE, 173, "footprint"),
     ("space_to_depth", 2, 3, 64, 64, 64, 7, 7, 2, 3, 1, sa.FILTER, 38, "s2d"),
     ("split_k", 1, 512, 7, 7, 512, 3, 3, 1, 1, 1, sa.FILTER, 307, "split"),
@@ -542,8 +544,8 @@ def test_conv_output_pitch(case, pitch):
     paths = set(plan["path"]) - {sa.CONV_NONE}
     if want == "k_conv":
         assert paths == {sa.CONV_DIRECT} and plan["ksplit"] == 1, plan
-    elif want in ("k_ig", "k_igk"):
-        assert paths == {sa.CONV_DIRECT_IG} and (plan["ig_tile"][3] > 1) == (want == "k_igk"), plan
+    elif want == "k_ig":
+        assert paths == {sa.CONV_DIRECT_IG}, plan
     elif want == "footprint":
         assert paths == {sa.CONV_FOOTPRINT}, plan
     elif want == "s2d":
