@@ -1051,24 +1051,16 @@ int launch_conv(ConvArgs a, hipStream_t stream) {
 
 // Tile shape of the direct kernel for groups of Ms filters over NPQ pixels:
 // 0 = 128 x 128, 1 = 128 x 64 (pixels x filters; eight wavefronts, two
-// workgroups per CU by LDS), 2 = 256 x 32 (four wavefronts) for groups of at
-// most 32 filters; *blocks receives the tile count.  The slowest CU runs
+// workgroups per CU by LDS); *blocks receives the tile count.  The slowest CU runs
 // ceil(tiles / CUs) tiles, and a 128 x 64 tile takes about 3/4 of the time of
 // a 128 x 128 one (0.53-0.87 measured over the ResNet-50 and AlexNet layers,
 // most near 0.75), so 128 x 64 tiles when 3 rounds of them cost no more than
 // 4 rounds of 128 x 128 ones.
 int direct_pick(const int *Ms, int n, int NPQ, int64_t *blocks) {
-    int maxM = 0;
-    int64_t t128 = 0, t64 = 0, t32 = 0;
+    int64_t t128 = 0, t64 = 0;
     for (int i = 0; i < n; ++i) {
-        maxM = std::max(maxM, Ms[i]);
         t128 += (Ms[i] + 127) / 128;
         t64 += (Ms[i] + 63) / 64;
-        t32 += (Ms[i] + 31) / 32;
-    }
-    if (maxM <= 32) {
-        *blocks = t32 * ((NPQ + 255) / 256);
-        return 2;
     }
     const int64_t ptiles = (NPQ + 127) / 128, cus = device_cus();
     t128 *= ptiles;
@@ -1086,7 +1078,10 @@ int direct_pick(const int *Ms, int n, int NPQ, int64_t *blocks) {
 // wavefronts per 128-pixel tile (two rows of four, each 32 pixels by 32 or 64
 // filters) keep 16 wavefronts per CU in flight to cover the operand latency:
 // over 94 ResNet-50 layer runs they took 0.73-1.05x (15% less in sum) of the
-// time of four-wavefront tiles of the same size.
+// time of four-wavefront tiles of the same size; for groups of at most 32
+// filters 128 x 64 tiles also beat 256 x 32 ones with four wavefronts (CIFAR
+// 3x3 layer of 32 kept filters 12.6 -> 10.0 us, [256,256,3,3] at 10% kept
+// 39.4 -> 30.9 us).
 int run_conv(ConvArgs a, hipStream_t stream) {
     if (a.ngroups == 0) return SA_OK;
     for (int i = 0; i < a.ngroups; ++i)
@@ -1100,8 +1095,7 @@ int run_conv(ConvArgs a, hipStream_t stream) {
     int64_t blocks;
     switch (direct_pick(Ms, a.ngroups, a.NPQ, &blocks)) {
         case 0: return launch_conv<128, 128, 4, 2>(a, stream);
-        case 1: return launch_conv<128, 64, 4, 2>(a, stream);
-        default: return launch_conv<256, 32, 4, 1>(a, stream);
+        default: return launch_conv<128, 64, 4, 2>(a, stream);
     }
 }
 
@@ -1296,9 +1290,16 @@ void split_plan(const sa_compact_sizes &s, ConvPlan *pl) {
         direct_pick(Mg, ng, p.NPQ, &b);
         base += b;
     }
-    if (base >= 128) return;
-    const int64_t ks = std::min<int64_t>({8, (256 + base - 1) / base, min_sl / 2});
-    if (ks < 2) return;
+    // the columns split over ks workgroups per tile only while the tiles
+    // leave CUs idle (ks <= CUs / tiles: one workgroup per CU), and only when
+    // the slices taken off each tile's serial loop pay for the split: about
+    // 9.5 us for the partial sums and the summing pass against 0.46 us per
+    // 64-column slice of a lone workgroup (measured at batch 1 over the
+    // ResNet-50 and AlexNet layers), i.e. min_sl * (ks - 1) / ks > 20
+    const int64_t cus = device_cus();
+    if (base >= cus) return;
+    const int64_t ks = std::min<int64_t>(8, cus / base);
+    if (ks < 2 || (int64_t)min_sl * (ks - 1) <= 20 * ks) return;
     p.ksplit = (int)ks;
     p.part_stride = ((int64_t)p.NPQ * p.Cy + 3) / 4 * 4;
     p.part_off = (p.ws_need + 255) / 256 * 256;
@@ -1328,7 +1329,7 @@ void direct_plan(const sa_compact_sizes &s, ConvPlan *pl) {
     }
     if (n == 0) return;
     int64_t blocks;
-    constexpr int kBN[3] = {128, 64, 32};
+    constexpr int kBN[2] = {128, 64};
     const int BN = kBN[direct_pick(Ms, n, p.NPQ, &blocks)];
     int64_t coarse = 0;
     for (int i = 0; i < n; ++i) coarse += (int64_t)(Ms[i] + BN - 1) / BN * BN;

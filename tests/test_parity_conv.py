@@ -194,8 +194,10 @@ PLANNED = [
     # every tap of a channel run, aligned or wide: the LDS-staged kernel
     ((114, 64, 12, 12, 128, 3, 3, 1, 1, 1, sa.FILTER, 1.0), {"path": {sa.CONV_DIRECT}}),
     ((114, 64, 12, 12, 96, 3, 3, 1, 1, 1, sa.FILTER, 0.6), {"path": {sa.CONV_DIRECT}}),
-    # split over the columns at a small batch
-    ((1, 64, 12, 12, 96, 3, 3, 1, 1, 1, sa.FILTER, 0.6), {"path": {sa.CONV_DIRECT}, "ksplit": 4}),
+    # split over the columns at a small batch: 36 slices of 64 columns per
+    # tile, two tiles; 9 slices stay whole
+    ((1, 256, 12, 12, 96, 3, 3, 1, 1, 1, sa.FILTER, 0.6), {"path": {sa.CONV_DIRECT}, "ksplit": 8}),
+    ((1, 64, 12, 12, 96, 3, 3, 1, 1, 1, sa.FILTER, 0.6), {"path": {sa.CONV_DIRECT}, "ksplit": 1}),
     # footprint kernel: six-wavefront tiles of 192 filters (AlexNet conv4 at
     # batch 128: one workgroup per CU, 226 tiles of 192 pixels fill one round
     # where 338 of 128 need two) and four-wavefront tiles (two per CU)
