@@ -1259,11 +1259,10 @@ int patch_lds(int TM, int TN, int patch_bytes, int tab_bytes, int NW = 4) {
 }
 
 // Split K when every group takes the direct kernel (on the input, or on its
-// gathered im2col rows) and the launches would have fewer than 128 tiles (a
-// batch-1 layer): the 64-column slices are cut into
-// ksplit chunks (at least two slices each, at most 8 chunks, about 256
-// workgroups in all), each workgroup writes binary32 partial sums, and
-// k_splitk_sum adds them in chunk order.  (The footprint kernel is not split:
+// gathered im2col rows), the launches leave CUs idle and the tiles are long
+// (small batches): the 64-column slices are cut into ksplit chunks (at most 8,
+// at most one workgroup per CU in all), each workgroup writes binary32
+// partial sums, and k_splitk_sum adds them in chunk order.  (The footprint kernel is not split:
 // each of its workgroups copies the whole input footprint, which then
 // dominates; measured slower at batch 1.)
 void split_plan(const sa_compact_sizes &s, ConvPlan *pl) {
