@@ -198,6 +198,9 @@ PLANNED = [
     # tile, two tiles; 9 slices stay whole
     ((1, 256, 12, 12, 96, 3, 3, 1, 1, 1, sa.FILTER, 0.6), {"path": {sa.CONV_DIRECT}, "ksplit": 8}),
     ((1, 64, 12, 12, 96, 3, 3, 1, 1, 1, sa.FILTER, 0.6), {"path": {sa.CONV_DIRECT}, "ksplit": 1}),
+    # gathered im2col rows (input rows too wide for LDS), 27 slices over 50
+    # tiles: the split takes 5 chunks (one workgroup per CU)
+    ((1, 256, 3, 2100, 40, 3, 3, 1, 1, 1, sa.SHAPE, 0.75), {"path": {sa.CONV_GATHER}, "ksplit": 5}),
     # footprint kernel: six-wavefront tiles of 192 filters (AlexNet conv4 at
     # batch 128: one workgroup per CU, 226 tiles of 192 pixels fill one round
     # where 338 of 128 need two) and four-wavefront tiles (two per CU)
