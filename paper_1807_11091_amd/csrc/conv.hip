@@ -1306,13 +1306,15 @@ void split_plan(const sa_compact_sizes &s, ConvPlan *pl) {
 }
 
 // Kernel for the groups read straight from the NHWC input (measured on
-// gfx950 over the ResNet-50 and AlexNet layers): k_ig, whose filter tiles grow
-// in steps of 16, when k_conv's 64- or 128-filter tiles would pad the filter
-// work by 15% or more over 256-512 columns and at least 2^16 pixels, with
-// more than 64 kept filters or at least 384 columns (k_conv's 128 x 64 tiles
-// are the faster ones below that: 1x1 layers over 64 channels, ResNet-50's
-// first layer); the eight-wavefront k_conv tiles otherwise (k_ig ran 5-25%
-// slower on every other layer).  Not for split K over workgroups (batch 1).
+// gfx950 over the ResNet-50 and AlexNet layers, in isolation and inside a
+// block of layers whose inputs come cold from HBM): k_ig, whose filter tiles
+// grow in steps of 16, for groups of at most 64 kept filters that k_conv's
+// 64-filter tiles would pad by 15% or more, over 384-512 columns and at least
+// 2^16 pixels (AlexNet's first layer of 48 kept filters on its space-to-depth
+// image: 62 vs 68 us); the eight-wavefront k_conv tiles otherwise (k_ig was
+// 3-25% slower on every other layer tried, among them ResNet-50's 1x1 layers
+// of 38 and 77 kept filters and its first layer).  Not for split K over
+// workgroups (small batches).
 void direct_plan(const sa_compact_sizes &s, ConvPlan *pl) {
     ConvPlan &p = *pl;
     p.direct_ig = false;
@@ -1332,8 +1334,7 @@ void direct_plan(const sa_compact_sizes &s, ConvPlan *pl) {
     const int BN = kBN[direct_pick(Ms, n, p.NPQ, &blocks)];
     int64_t coarse = 0;
     for (int i = 0; i < n; ++i) coarse += (int64_t)(Ms[i] + BN - 1) / BN * BN;
-    p.direct_ig = coarse * 100 >= fine * 115 && maxK >= 256 && maxK <= 512 && p.NPQ >= (1 << 16) &&
-                  (maxM > 64 || maxK >= 384);
+    p.direct_ig = maxM <= 64 && coarse * 100 >= fine * 115 && maxK >= 384 && maxK <= 512 && p.NPQ >= (1 << 16);
 }
 
 // Validates the descriptor (beyond validate_conv) and chooses, per conv group,

@@ -353,10 +353,7 @@ struct Tile {
     int MT, NF, WM;
 };
 // instantiated tile shapes (filters x pixels per workgroup = WM*MT*16 x (4/WM)*NF*16)
-constexpr Tile kTiles[] = {
-    {2, 2, 1}, {3, 2, 1}, {4, 2, 1}, {5, 2, 1}, {6, 2, 1}, {8, 2, 1}, {3, 4, 1},
-    {4, 4, 1}, {3, 2, 2}, {4, 2, 2}, {5, 2, 2}, {4, 1, 2}, {5, 1, 2},
-};
+constexpr Tile kTiles[] = {{2, 2, 1}, {3, 2, 1}};
 constexpr int kNumTiles = sizeof(kTiles) / sizeof(kTiles[0]);
 
 template <int MT, int NF, int WM>
@@ -399,17 +396,6 @@ int launch_tile(int t, const IgArgs &a, hipStream_t stream) {
     switch (t) {
         case 0: return launch<2, 2, 1>(a, stream);
         case 1: return launch<3, 2, 1>(a, stream);
-        case 2: return launch<4, 2, 1>(a, stream);
-        case 3: return launch<5, 2, 1>(a, stream);
-        case 4: return launch<6, 2, 1>(a, stream);
-        case 5: return launch<8, 2, 1>(a, stream);
-        case 6: return launch<3, 4, 1>(a, stream);
-        case 7: return launch<4, 4, 1>(a, stream);
-        case 8: return launch<3, 2, 2>(a, stream);
-        case 9: return launch<4, 2, 2>(a, stream);
-        case 10: return launch<5, 2, 2>(a, stream);
-        case 11: return launch<4, 1, 2>(a, stream);
-        case 12: return launch<5, 1, 2>(a, stream);
         default: return fail(SA_E_ARG, "conv_ig: no tile shape %d", t);
     }
 }
@@ -430,42 +416,13 @@ int device_cus() {
     return cus[dev];
 }
 
-// Tile shape for a launch (measured on gfx950 over the ResNet-50 and AlexNet
-// layers): the least padded filter work first (rows pad to the tile's BM,
-// within 4%), not counting 32-filter tiles when a group keeps more filters.
-// Among those, a tile whose filter count covers every group's kept filters
-// (its output rows are whole: one contiguous range of Y), else the smallest
-// tile of at least 64 filters; two pixel fragments per wavefront, four
-// wavefronts along the pixels, whenever the table has such a shape.
+// Tile shape for a launch: 32 or 48 filters, the one that covers every
+// group's kept filters (the plan sends this kernel groups of at most 48 kept
+// filters; a tile over whole output rows writes one contiguous range of Y).
 int ig_pick(const IgArgs &a) {
-    int64_t least = -1;
-    int64_t work[kNumTiles];
     int maxM = 0;
     for (int i = 0; i < a.ngroups; ++i) maxM = std::max(maxM, (int)a.g[i].M);
-    for (int t = 0; t < kNumTiles; ++t) {
-        const int BM = kTiles[t].WM * kTiles[t].MT * 16;
-        int64_t w = 0;
-        for (int i = 0; i < a.ngroups; ++i) w += (int64_t)(a.g[i].M + BM - 1) / BM * BM;
-        // 32-filter tiles re-read every pixel's columns once per 32 filters:
-        // the slowest shape on every layer measured unless no group has more
-        work[t] = BM < 48 && maxM > BM ? -1 : w;
-        if (work[t] >= 0 && (least < 0 || w < least)) least = w;
-    }
-    auto score = [&](int t) {  // larger is better
-        const Tile &T = kTiles[t];
-        const int BM = T.WM * T.MT * 16;
-        int sc = BM >= 64 ? 500 - BM : BM;  // the smallest tile of at least 64 filters
-        if (T.WM == 1) sc += 1000;
-        if (BM >= maxM) sc += 10000;         // whole output rows
-        if (T.NF == 2) sc += 100000;
-        return sc;
-    };
-    int best = -1;
-    for (int t = 0; t < kNumTiles; ++t) {
-        if (work[t] < 0 || work[t] * 100 > least * 104) continue;
-        if (best < 0 || score(t) > score(best)) best = t;
-    }
-    return best;
+    return maxM <= 32 ? 0 : 1;
 }
 
 int ig_run(IgArgs a, int tile, hipStream_t stream) {

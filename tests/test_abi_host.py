@@ -238,11 +238,14 @@ def test_conv_plan_host_only():
         rc = L.structadmm_conv_plan(ctypes.byref(d), ctypes.byref(info))
         return rc, info
 
-    # 77 kept filters of a 1x1 layer over 256 channels, 56x56 at batch 64: the
-    # 16-row kernel (128-filter tiles would pad the filter work by 66%)
-    rc, info = plan(64, 56, 56, 256, 1, 1, 1, 0, 77, run=256)
+    # 38 kept filters of a 1x1 layer over 448 channels, 56x56 at batch 64: the
+    # 16-row kernel (64-filter tiles would pad the filter work by a third)
+    rc, info = plan(64, 56, 56, 448, 1, 1, 1, 0, 38, run=448)
     assert rc == 0 and list(info.path)[:1] == [sa.CONV_DIRECT_IG] and info.ksplit == 1
-    assert tuple(info.ig_tile) == (5, 2, 1, 1)
+    assert tuple(info.ig_tile) == (3, 2, 1, 1)
+    # 77 over 256 channels: the LDS-staged kernel
+    rc, info = plan(64, 56, 56, 256, 1, 1, 1, 0, 77, run=256)
+    assert rc == 0 and list(info.path)[:1] == [sa.CONV_DIRECT]
     # 38 of 64 over 64 channels: the 128 x 64 tiles of the LDS-staged kernel
     rc, info = plan(64, 56, 56, 64, 1, 1, 1, 0, 38, run=64)
     assert rc == 0 and list(info.path)[:1] == [sa.CONV_DIRECT]

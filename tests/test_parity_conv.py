@@ -183,12 +183,13 @@ def test_conv_small(case):
 # cases pinned to a kernel and tile shape (the plan is asserted before the
 # parity check, so a change of the selection cannot silently move them)
 PLANNED = [
-    # ragged kept filters over 256-512 columns and at least 2^16 pixels: the
-    # 16-row kernel (ragged pixel tails: 65,856 and 73,728 pixels)
-    ((21, 256, 56, 56, 128, 1, 1, 1, 0, 1, sa.FILTER, 0.6), {"path": {sa.CONV_DIRECT_IG}, "ig_tile": (5, 2, 1, 1)}),
+    # at most 48 kept filters over 384-512 columns and at least 2^16 pixels:
+    # the 16-row kernel (ragged pixel tails: 65,856 and 73,728 pixels)
+    ((21, 448, 56, 56, 64, 1, 1, 1, 0, 1, sa.FILTER, 0.6), {"path": {sa.CONV_DIRECT_IG}, "ig_tile": (3, 2, 1, 1)}),
+    ((21, 448, 56, 56, 64, 1, 1, 1, 0, 1, sa.FILTER, 0.45), {"path": {sa.CONV_DIRECT_IG}, "ig_tile": (2, 2, 1, 1)}),
     ((128, 48, 24, 24, 64, 3, 3, 1, 1, 1, sa.FILTER, 0.6), {"path": {sa.CONV_DIRECT_IG}, "ig_tile": (3, 2, 1, 1)}),
-    ((65, 256, 32, 32, 256, 1, 1, 1, 0, 1, sa.FILTER, 0.6), {"path": {sa.CONV_DIRECT_IG}, "ig_tile": (5, 2, 2, 1)}),
-    # the same filters over 512 columns or fewer pixels: the LDS-staged kernel
+    # more filters, fewer columns or fewer pixels: the LDS-staged kernel
+    ((21, 256, 56, 56, 128, 1, 1, 1, 0, 1, sa.FILTER, 0.6), {"path": {sa.CONV_DIRECT}}),
     ((70, 256, 14, 14, 512, 1, 1, 1, 0, 1, sa.FILTER, 0.6), {"path": {sa.CONV_DIRECT}}),
     ((48, 64, 20, 20, 64, 1, 1, 1, 0, 1, sa.FILTER, 0.6), {"path": {sa.CONV_DIRECT}}),
     # every tap of a channel run, aligned or wide: the LDS-staged kernel
@@ -223,14 +224,14 @@ def test_conv_planned_kernel(case, expect):
 
 
 def test_conv_16row_tile_shapes():
-    """The 16-row kernel over 1x1 layers of 448 input channels at 65,856
-    pixels, kept-filter counts that make its launcher take different tile
-    shapes, all against the oracle."""
+    """1x1 layers of 448 input channels at 65,856 pixels, kept-filter counts
+    that take both tile shapes of the 16-row kernel (and the LDS-staged kernel
+    above 48), all against the oracle."""
     seen = set()
     rng = np.random.default_rng(448)
     X = rng.standard_normal((21, 448, 56, 56)).astype(np.float32)
     Xp = sa.pack_nhwc(to_dev(X))
-    for A, keep in ((64, 0.6), (128, 0.6), (256, 0.6), (512, 0.6), (160, 0.575), (1024, 0.6), (100, 0.6)):
+    for A, keep in ((64, 0.6), (64, 0.45), (40, 0.5), (128, 0.6), (100, 0.6), (512, 0.6)):
         rng = np.random.default_rng(A + int(100 * keep))
         k = max(1, int(round(keep * A)))
         mask = np.zeros(A, np.uint8)
@@ -246,7 +247,7 @@ def test_conv_16row_tile_shapes():
         Yr = oracle.conv(oracle.pack(X[sel]), rc, 1, 1, 1, 0)
         err = maxabs_over_rms(bf16_bits_to_f64(Y.cpu().numpy()[sel]), Yr)
         assert err <= TOL, (A, keep, plan, err)
-    assert len(seen) >= 3, seen
+    assert seen == {(2, 2, 1, 1), (3, 2, 1, 1)}, seen
 
 
 def test_conv_unaligned_channel_window():
@@ -515,7 +516,7 @@ def test_conv_on_a_non_current_stream():
 PITCH_CASES = [
     ("direct_whole_rows", 32, 64, 64, 64, 64, 3, 3, 1, 1, 1, sa.FILTER, 38, "k_conv"),
     ("direct_tiles", 32, 64, 64, 64, 256, 3, 3, 1, 1, 1, sa.FILTER, 154, "k_conv"),
-    ("ig_1x1", 21, 256, 56, 56, 128, 1, 1, 1, 0, 1, sa.FILTER, 77, "k_ig"),
+    ("ig_1x1", 21, 448, 56, 56, 64, 1, 1, 1, 0, 1, sa.FILTER, 38, "k_ig"),
     ("ig_3x3", 128, 48, 24, 24, 64, 3, 3, 1, 1, 1, sa.FILTER, 38, "k_ig"),
     ("footprint", 4, 64, 20, 20, 96, 3, 3, 1, 1, 1, sa.SHAPE, 173, "footprint"),
     ("space_to_depth", 2, 3, 64, 64, 64, 7, 7, 2, 3, 1, sa.FILTER, 38, "s2d"),
