@@ -206,15 +206,20 @@ def run_step(torch, sa, wl, layers, ws, cws, ev, record):
     mark("admm1")
     if any(o.in_mask is not None for o in layers):
         raise SystemExit("the timed step runs workloads without a filter + channel chain (--suite times the chain)")
-    # compaction synchronises with the host (it returns the sizes), so every
-    # layer is compacted first and the CONVs are then enqueued back to back
+    # compaction synchronises with the host (it returns the sizes): every
+    # layer's kept and dense matrices in one call (one wait), then the CONVs
+    # are enqueued back to back
+    items = []
+    for o in layers:
+        cols = o.mask if o.kind == sa.SHAPE else None
+        rows = o.mask if o.kind == sa.FILTER else None
+        items.append(dict(Z=o.Z, groups=o.cfg.groups, row_mask=rows, col_mask=cols, out=o.comp_out))
+        items.append(dict(Z=o.Z, groups=o.cfg.groups, out=o.dense_out))
+    done = sa.compact_many(items, ws=cws)
     comp = []
     for i, o in enumerate(layers):
         L = o.cfg
-        cols = o.mask if o.kind == sa.SHAPE else None
-        rows = o.mask if o.kind == sa.FILTER else None
-        c = sa.compact(o.Z, L.groups, row_mask=rows, col_mask=cols, ws=cws, out=o.comp_out)
-        d = sa.compact(o.Z, L.groups, ws=cws, out=o.dense_out)
+        c, d = done[2 * i], done[2 * i + 1]
         sizes, sized = c[4], d[4]
         if o.Yc is None:
             shape = sa.conv_out_shape(*o.Xp.shape[:3], L.C, L.D, L.stride, L.pad, sizes)
@@ -1023,7 +1028,8 @@ def measure(torch, sa, wl, steps, warmup):
     layers = setup(torch, sa, wl)
     progress(f"{wl.name}: {len(layers)} layers resident, warm-up")
     ws = torch.empty(max(256, sa.project_workspace([o.proj for o in layers])), dtype=torch.uint8, device="cuda")
-    cws = torch.empty(sa.COMPACT_WS_BYTES, dtype=torch.uint8, device="cuda")
+    # compaction scratch: one range per compacted matrix (kept and dense of every layer)
+    cws = torch.empty(2 * len(layers) * sa.COMPACT_WS_BYTES, dtype=torch.uint8, device="cuda")
     ev = {"pdescs": sa._descs([o.proj for o in layers]),
           "ddescs": sa.dual_descs([(o.W, o.Z, o.U, wl.rho, o.G2, False) for o in layers]),
           "lead": lead_cycles(torch, LEAD_US), "lead_conv": 0}

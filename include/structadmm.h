@@ -31,7 +31,7 @@
  *     Caffe OIHW.  The flat index of (a, b, c, d) is ((a*B + b)*C + c)*D + d
  *     and the GEMM column of (b, c, d) is j = (b*C + c)*D + d.
  *   - Work is enqueued asynchronously on the given HIP stream (0 = the null
- *     stream).  Only structadmm_compact synchronises with the host.
+ *     stream).  Only structadmm_compact and structadmm_compact_many synchronise with the host.
  *   - Return value 0 = success; negative = error (codes below).  All
  *     arguments are validated on the host before anything is enqueued, so
  *     an error return leaves every output untouched.
@@ -262,6 +262,17 @@ typedef struct sa_compact_sizes {
 } sa_compact_sizes;
 
 int structadmm_compact(const sa_compact_desc *desc, sa_compact_sizes *sizes, hipStream_t stream);
+
+/* The compactions of n descriptors (the layers of a network after one
+ * projection, Section 3) with one wait of the host: the kernels of every
+ * descriptor are enqueued, then the host waits once for all the sizes
+ * (twice when a descriptor has in_compacted set).  Results are those of n
+ * calls of structadmm_compact; sizes[i] belongs to descs[i].  Every
+ * descriptor needs its own ws (scratch ranges of SA_COMPACT_WS_BYTES may not
+ * overlap: SA_E_ARG) and outputs that no other descriptor writes.  All
+ * descriptors are validated before anything is enqueued, so an error leaves
+ * every output untouched.  n = 0 does nothing. */
+int structadmm_compact_many(const sa_compact_desc *descs, int32_t n, sa_compact_sizes *sizes, hipStream_t stream);
 
 /* ---- input layout: structadmm_pack_nhwc ------------------------------ */
 /*

@@ -137,6 +137,9 @@ def lib():
         L.structadmm_sgd_step.restype = ctypes.c_int
         L.structadmm_compact.argtypes = [ctypes.POINTER(CompactDesc), ctypes.POINTER(CompactSizes), _vp]
         L.structadmm_compact.restype = ctypes.c_int
+        L.structadmm_compact_many.argtypes = [ctypes.POINTER(CompactDesc), ctypes.c_int32,
+                                              ctypes.POINTER(CompactSizes), _vp]
+        L.structadmm_compact_many.restype = ctypes.c_int
         L.structadmm_pack_nhwc.argtypes = [_vp, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
                                            _vp, ctypes.c_int32, _vp, _vp]
         L.structadmm_pack_nhwc.restype = ctypes.c_int
@@ -296,6 +299,47 @@ def compact(Z, groups: int = 1, row_mask=None, col_mask=None, chan_mask=None, in
     _check(lib().structadmm_compact(ctypes.byref(desc), ctypes.byref(sizes), _stream(stream)), "structadmm_compact")
     _keep_for_stream(stream, ws, *(() if out is not None else (Wc, row_idx, col_ch, col_tap)))
     return Wc, row_idx, col_ch, col_tap, sizes
+
+
+def compact_many(items, ws=None, stream=None):
+    """structadmm_compact_many: one call (one wait of the host) for many
+    compactions.  items: dicts of compact()'s arguments (Z, groups, row_mask,
+    col_mask, chan_mask, in_ch_mask, in_compacted, out); ws: uint8 scratch of
+    len(items) * COMPACT_WS_BYTES (allocated here when None).  Returns the
+    list of (Wc, row_idx, col_ch, col_tap, sizes), one per item."""
+    import torch
+    n = len(items)
+    if n == 0:
+        return []
+    dev = items[0]["Z"].device
+    if ws is None:
+        ws = torch.empty(n * COMPACT_WS_BYTES, dtype=torch.uint8, device=dev)
+    elif ws.numel() * ws.element_size() < n * COMPACT_WS_BYTES:
+        raise StructAdmmError(f"compact_many: ws must hold {n} x {COMPACT_WS_BYTES} bytes")
+    descs = (CompactDesc * n)()
+    sizes = (CompactSizes * n)()
+    outs, made = [], []
+    for i, it in enumerate(items):
+        Z = it["Z"]
+        A, B, C, D = Z.shape
+        groups = it.get("groups", 1)
+        K = B * C * D
+        if it.get("out") is None:
+            o = (torch.empty(A * ((K + 63) // 64 * 64), dtype=torch.uint16, device=dev),
+                 torch.empty(A, dtype=torch.int32, device=dev),
+                 torch.empty(groups * K, dtype=torch.int32, device=dev),
+                 torch.empty(groups * K, dtype=torch.int32, device=dev))
+            made.extend(o)
+        else:
+            o = tuple(it["out"])
+        outs.append(o)
+        descs[i] = CompactDesc(A, B, C, D, groups, _ptr(Z), _ptr(it.get("row_mask")), _ptr(it.get("col_mask")),
+                               _ptr(it.get("chan_mask")), _ptr(it.get("in_ch_mask")),
+                               1 if it.get("in_compacted") else 0, _ptr(o[0]), _ptr(o[1]), _ptr(o[2]), _ptr(o[3]),
+                               ws.data_ptr() + i * COMPACT_WS_BYTES)
+    _check(lib().structadmm_compact_many(descs, n, sizes, _stream(stream)), "structadmm_compact_many")
+    _keep_for_stream(stream, ws, *made)
+    return [outs[i] + (CompactSizes.from_buffer_copy(sizes[i]),) for i in range(n)]
 
 
 def pack_nhwc(X, keep=None, Cx: Optional[int] = None, out=None, stream=None):

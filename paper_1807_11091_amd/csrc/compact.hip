@@ -10,6 +10,7 @@
 #include <algorithm>
 #include <cstdint>
 #include <cstring>
+#include <vector>
 
 #include "sa_device.h"
 #include "sa_host.h"
@@ -342,13 +343,16 @@ __global__ __launch_bounds__(256) void k_pack_small(const float *__restrict__ X,
 
 using namespace sa;
 
-extern "C" int structadmm_compact(const sa_compact_desc *desc, sa_compact_sizes *sizes, hipStream_t stream) {
-    clear_error();
-    if (!desc || !sizes) return fail(SA_E_ARG, "compact: desc and sizes are required");
-    const sa_compact_desc &d = *desc;
+namespace {
+
+int check_compact(const sa_compact_desc &d) {
     if (int rc = validate_compact(d)) return rc;
     if (d.in_compacted && (int64_t)d.groups * d.B > 16384)
         return fail(SA_E_UNSUPPORTED, "compact: in_compacted supports at most 16384 input channels");
+    return SA_OK;
+}
+
+CompArgs compact_args(const sa_compact_desc &d) {
     CompArgs a;
     memset(&a, 0, sizeof a);
     a.Z = d.Z;
@@ -367,31 +371,42 @@ extern "C" int structadmm_compact(const sa_compact_desc *desc, sa_compact_sizes 
     a.D = (int)d.D;
     a.groups = d.groups;
     a.in_compacted = d.in_compacted ? 1 : 0;
+    return a;
+}
+
+// The kernels of one compaction that need no host decision: the per-group
+// counts (into ws), the column tables and kept rows, the gathered matrix.
+int launch_compact(const CompArgs &a, hipStream_t stream) {
     const int Ag = a.A / a.groups;
-    hipLaunchKernelGGL(k_compact_count, dim3(d.groups), dim3(kCompThreads), 0, stream, a);
+    hipLaunchKernelGGL(k_compact_count, dim3(a.groups), dim3(kCompThreads), 0, stream, a);
     if (int rc = check_hip(hipGetLastError(), "k_compact_count")) return rc;
-    hipLaunchKernelGGL(k_compact_tables, dim3(d.groups), dim3(kCompThreads), 0, stream, a);
+    hipLaunchKernelGGL(k_compact_tables, dim3(a.groups), dim3(kCompThreads), 0, stream, a);
     if (int rc = check_hip(hipGetLastError(), "k_compact_tables")) return rc;
-    hipLaunchKernelGGL(k_compact_gather, dim3(Ag, d.groups), dim3(256), 0, stream, a);
-    if (int rc = check_hip(hipGetLastError(), "k_compact_gather")) return rc;
-    int32_t counts[kCS * SA_MAX_CONV_GROUPS];
-    if (int rc = check_hip(hipMemcpyAsync(counts, d.ws, sizeof(int32_t) * kCS * d.groups, hipMemcpyDeviceToHost, stream),
-                           "compact: copy sizes"))
-        return rc;
-    if (int rc = check_hip(hipStreamSynchronize(stream), "compact: synchronize")) return rc;
-    int total_cols = 0;
-    for (int g = 0; g < d.groups; ++g) total_cols += counts[kCS * g + 1];
-    if (d.in_compacted && total_cols > 0) {
-        size_t lds = sizeof(int32_t) * (size_t)d.groups * d.B;
-        hipLaunchKernelGGL(k_compact_inpos, dim3(1), dim3(kCompThreads), lds, stream, a, total_cols);
-        if (int rc = check_hip(hipGetLastError(), "k_compact_inpos")) return rc;
-        if (int rc = check_hip(hipStreamSynchronize(stream), "compact: synchronize")) return rc;
-    }
+    hipLaunchKernelGGL(k_compact_gather, dim3(Ag, a.groups), dim3(256), 0, stream, a);
+    return check_hip(hipGetLastError(), "k_compact_gather");
+}
+
+int total_columns(const int32_t *counts, int groups) {
+    int total = 0;
+    for (int g = 0; g < groups; ++g) total += counts[kCS * g + 1];
+    return total;
+}
+
+// For a channel-compacted input: input positions in the column tables.
+int launch_inpos(const CompArgs &a, const int32_t *counts, hipStream_t stream) {
+    const int total = total_columns(counts, a.groups);
+    if (!a.in_compacted || total == 0) return SA_OK;
+    const size_t lds = sizeof(int32_t) * (size_t)a.groups * a.B;
+    hipLaunchKernelGGL(k_compact_inpos, dim3(1), dim3(kCompThreads), lds, stream, a, total);
+    return check_hip(hipGetLastError(), "k_compact_inpos");
+}
+
+void fill_sizes(const int32_t *counts, int groups, sa_compact_sizes *sizes) {
     memset(sizes, 0, sizeof *sizes);
-    sizes->groups = d.groups;
+    sizes->groups = groups;
     int64_t wc_off = 0;
     int32_t row_off = 0, col_off = 0;
-    for (int g = 0; g < d.groups; ++g) {
+    for (int g = 0; g < groups; ++g) {
         sizes->M[g] = counts[kCS * g + 0];
         sizes->K[g] = counts[kCS * g + 1];
         sizes->ldk[g] = (sizes->K[g] + 63) / 64 * 64;
@@ -407,6 +422,54 @@ extern "C" int structadmm_compact(const sa_compact_desc *desc, sa_compact_sizes 
         row_off += sizes->M[g];
         col_off += sizes->K[g];
     }
+}
+
+}  // namespace
+
+extern "C" int structadmm_compact(const sa_compact_desc *desc, sa_compact_sizes *sizes, hipStream_t stream) {
+    clear_error();
+    if (!desc || !sizes) return fail(SA_E_ARG, "compact: desc and sizes are required");
+    return structadmm_compact_many(desc, 1, sizes, stream);
+}
+
+extern "C" int structadmm_compact_many(const sa_compact_desc *descs, int32_t n, sa_compact_sizes *sizes,
+                                       hipStream_t stream) {
+    clear_error();
+    if (n < 0 || (n > 0 && (!descs || !sizes))) return fail(SA_E_ARG, "compact: descs and sizes are required");
+    // every descriptor is checked before anything is enqueued
+    for (int i = 0; i < n; ++i) {
+        if (int rc = check_compact(descs[i])) return rc;
+        const uintptr_t wi = reinterpret_cast<uintptr_t>(descs[i].ws);
+        for (int j = 0; j < i; ++j) {
+            const uintptr_t wj = reinterpret_cast<uintptr_t>(descs[j].ws);
+            if (wi < wj + SA_COMPACT_WS_BYTES && wj < wi + SA_COMPACT_WS_BYTES)
+                return fail(SA_E_ARG, "compact: descriptors %d and %d share scratch", j, i);
+        }
+    }
+    if (n == 0) return SA_OK;
+    std::vector<CompArgs> args(n);
+    for (int i = 0; i < n; ++i) {
+        args[i] = compact_args(descs[i]);
+        if (int rc = launch_compact(args[i], stream)) return rc;
+    }
+    std::vector<int32_t> counts((size_t)n * kCS * SA_MAX_CONV_GROUPS);
+    for (int i = 0; i < n; ++i)
+        if (int rc = check_hip(hipMemcpyAsync(&counts[(size_t)i * kCS * SA_MAX_CONV_GROUPS], descs[i].ws,
+                                              sizeof(int32_t) * kCS * descs[i].groups, hipMemcpyDeviceToHost, stream),
+                               "compact: copy sizes"))
+            return rc;
+    if (int rc = check_hip(hipStreamSynchronize(stream), "compact: synchronize")) return rc;
+    bool inpos = false;
+    for (int i = 0; i < n; ++i) {
+        const int32_t *c = &counts[(size_t)i * kCS * SA_MAX_CONV_GROUPS];
+        if (args[i].in_compacted && total_columns(c, args[i].groups) > 0) {
+            if (int rc = launch_inpos(args[i], c, stream)) return rc;
+            inpos = true;
+        }
+    }
+    if (inpos)
+        if (int rc = check_hip(hipStreamSynchronize(stream), "compact: synchronize")) return rc;
+    for (int i = 0; i < n; ++i) fill_sizes(&counts[(size_t)i * kCS * SA_MAX_CONV_GROUPS], args[i].groups, &sizes[i]);
     return SA_OK;
 }
 

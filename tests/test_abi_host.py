@@ -26,7 +26,8 @@ def declared_functions():
 def test_library_exports_every_declared_symbol():
     names = declared_functions()
     assert {"structadmm_project", "structadmm_project_workspace", "structadmm_dual_update",
-            "structadmm_compact", "structadmm_conv_fwd", "structadmm_pack_nhwc", "structadmm_sgd_step",
+            "structadmm_compact", "structadmm_compact_many", "structadmm_conv_fwd", "structadmm_pack_nhwc",
+            "structadmm_sgd_step",
             "structadmm_csr", "structadmm_conv_sparse_fwd", "structadmm_conv_sparse_workspace",
             "structadmm_last_error", "structadmm_version"} <= names
     L = sa.lib()
@@ -173,6 +174,25 @@ def test_compact_and_conv_validation():
     assert comp(ws=None) == -1
     assert comp(Wc=FAKE + 8) == -2
     assert comp(C=300) == -4
+
+    # the batched form checks every descriptor (and that no two share
+    # scratch) before it enqueues anything: these calls do no GPU work
+    def many(*descs, n=None):
+        arr = (sa.CompactDesc * max(1, len(descs)))()
+        for i, kw in enumerate(descs):
+            d = dict(A=4, B=2, C=3, D=3, groups=1, Z=FAKE, row_mask=None, col_mask=None, chan_mask=None,
+                     in_ch_mask=None, in_compacted=0, Wc=FAKE + 256, row_idx=FAKE + 512, col_ch=FAKE + 768,
+                     col_tap=FAKE + 1024, ws=FAKE + 8192 * (i + 1))
+            d.update(kw)
+            arr[i] = sa.CompactDesc(**d)
+        out = (sa.CompactSizes * max(1, len(descs)))()
+        return L.structadmm_compact_many(arr, len(descs) if n is None else n, out, None)
+    assert many() == 0
+    assert many({}, n=-1) == -1
+    assert many({}, {"ws": FAKE + 8192 + 256}) == -1  # scratch ranges overlap
+    assert many({}, {"groups": 3}) == -1
+    assert many({}, {"Wc": FAKE + 8}) == -2
+    assert L.structadmm_compact_many(None, 1, None, None) == -1
 
     s = sa.CompactSizes()
     s.groups = 1

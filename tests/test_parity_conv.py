@@ -323,6 +323,51 @@ def test_compact_alignment_columns(kept, kpad_expect):
     assert maxabs_over_rms(bf16_bits_to_f64(Y.cpu().numpy()), Yr) <= TOL
 
 
+def test_compact_many_matches_one_by_one():
+    """structadmm_compact_many over layers of every kind (filter-pruned,
+    shape-pruned with groups, channel-masked, channel-compacted input with
+    alignment columns, an empty layer) gives, byte for byte, what one
+    structadmm_compact call per layer gives, and the oracle's matrices."""
+    t = torch()
+    rng = np.random.default_rng(77)
+    items, refs = [], []
+
+    def add(A, B, C, D, groups, **masks):
+        Z = (0.05 * rng.standard_normal((A, B, C, D))).astype(np.float32)
+        dev = {k: (to_dev(v) if isinstance(v, np.ndarray) else v) for k, v in masks.items()}
+        items.append(dict(Z=to_dev(Z), groups=groups, **dev))
+        refs.append((Z, groups, masks))
+
+    def mask(n, k):
+        m = np.zeros(n, np.uint8)
+        m[rng.choice(n, size=k, replace=False)] = 1
+        return m
+
+    add(96, 64, 3, 3, 1, row_mask=mask(96, 58))
+    add(64, 48, 3, 3, 2, col_mask=mask(48 * 9, 130))
+    add(32, 40, 1, 1, 1, chan_mask=mask(40, 24))
+    prev = np.zeros(64, np.uint8)
+    prev[:13] = 1
+    prev[32:51] = 1
+    add(32, 32, 3, 3, 2, row_mask=mask(32, 20), in_ch_mask=prev, in_compacted=True)
+    add(16, 8, 3, 3, 1, row_mask=np.zeros(16, np.uint8))
+    many = sa.compact_many(items)
+    for it, (Z, groups, masks), got in zip(items, refs, many):
+        one = sa.compact(it["Z"], groups, row_mask=it.get("row_mask"), col_mask=it.get("col_mask"),
+                         chan_mask=it.get("chan_mask"), in_ch_mask=it.get("in_ch_mask"),
+                         in_compacted=bool(it.get("in_compacted")))
+        sg, so = got[4], one[4]
+        assert bytes(sg) == bytes(so)
+        used = [sum(sg.M[g] * sg.ldk[g] for g in range(groups)), sum(sg.M[g] for g in range(groups)),
+                sum(sg.K[g] for g in range(groups)), sum(sg.K[g] for g in range(groups))]
+        for a, b, n in zip(got[:4], one[:4], used):  # Wc, row_idx, col_ch, col_tap
+            assert t.equal(a[:n], b[:n])
+        rc = oracle.compact(Z, groups, row_mask=masks.get("row_mask"), col_mask=masks.get("col_mask"),
+                            chan_mask=masks.get("chan_mask"), in_ch_mask=masks.get("in_ch_mask"),
+                            in_compacted=bool(masks.get("in_compacted")))
+        check_compact(got, rc)
+
+
 def sampled_images(N, count):
     """count images spread over the batch, always the first and the last
     (every image when count >= N)."""
