@@ -8,6 +8,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <climits>
 #include <cstdint>
 #include <cstring>
 #include <vector>
@@ -68,21 +69,39 @@ __global__ __launch_bounds__(kCompThreads) void k_compact_count(CompArgs a) {
     __syncthreads();
     uint32_t m = 0, kc = 0, nb = 0;
     for (int r = threadIdx.x; r < Ag; r += kCompThreads) m += (!a.row_mask || a.row_mask[gc * Ag + r]) ? 1 : 0;
+    // first and last kept channel: per thread, then per wavefront, then one
+    // LDS atomic per wavefront (a dense layer keeps every candidate)
+    int cf = INT_MAX, cl = -1;
     for (int64_t i = threadIdx.x; i < (int64_t)taps * a.B; i += kCompThreads) {
         int t = (int)(i / a.B), b = (int)(i - (int64_t)t * a.B);
         if (col_kept(a, gc, t, b)) {
             ++kc;
-            atomicMin(reinterpret_cast<unsigned *>(&s_cfirst), (unsigned)b);  // -1 is the largest unsigned
-            atomicMax(&s_clast, b);
+            cf = min(cf, b);
+            cl = max(cl, b);
         }
     }
     // kept channels ignoring the shape mask (defines the run when there is no shape mask)
+    int bf = INT_MAX, bl = -1;
     for (int b = threadIdx.x; b < a.B; b += kCompThreads) {
         bool keep = (!a.chan_mask || a.chan_mask[b]) && (!a.in_ch_mask || a.in_ch_mask[gc * a.B + b]);
         nb += keep ? 1 : 0;
         if (keep) {
-            atomicMin(reinterpret_cast<unsigned *>(&s_first), (unsigned)b);
-            atomicMax(&s_last, b);
+            bf = min(bf, b);
+            bl = max(bl, b);
+        }
+    }
+    cf = wave_min_i32(cf);
+    cl = wave_max_i32(cl);
+    bf = wave_min_i32(bf);
+    bl = wave_max_i32(bl);
+    if ((threadIdx.x & (kWave - 1)) == 0) {
+        if (cl >= 0) {
+            atomicMin(reinterpret_cast<unsigned *>(&s_cfirst), (unsigned)cf);  // -1 is the largest unsigned
+            atomicMax(&s_clast, cl);
+        }
+        if (bl >= 0) {
+            atomicMin(reinterpret_cast<unsigned *>(&s_first), (unsigned)bf);
+            atomicMax(&s_last, bl);
         }
     }
     // channels of the compacted input (every set bit of in_ch_mask)

@@ -26,6 +26,19 @@ __device__ inline uint32_t wave_sum_u32(uint32_t x) {
     return x;
 }
 
+// Minimum / maximum over the 64 lanes of a wavefront; every lane receives it.
+__device__ inline int wave_min_i32(int x) {
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) x = min(x, __shfl_xor(x, off, kWave));
+    return x;
+}
+
+__device__ inline int wave_max_i32(int x) {
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) x = max(x, __shfl_xor(x, off, kWave));
+    return x;
+}
+
 // Inclusive prefix sum over the lanes of a wavefront (lane order).
 __device__ inline uint32_t wave_incl_scan(uint32_t x) {
     const int lane = threadIdx.x & (kWave - 1);
