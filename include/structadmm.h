@@ -343,7 +343,7 @@ int structadmm_conv_fwd(const sa_conv_desc *desc, hipStream_t stream);
  * GPU work, the device pointers are not read.  Same validation and error
  * codes as structadmm_conv_fwd; on success *info is filled. */
 #define SA_CONV_NONE 0       /* group without output channels                          */
-#define SA_CONV_DIRECT 1     /* every tap of a channel run, LDS-staged 32/64/128-filter tiles */
+#define SA_CONV_DIRECT 1     /* every tap of a channel run, LDS-staged 64/128-filter tiles  */
 #define SA_CONV_DIRECT_IG 2  /* every tap of a channel run, 16-filter-granular tiles       */
 #define SA_CONV_FOOTPRINT 3  /* any columns, input footprint of the pixel tile in LDS      */
 #define SA_CONV_GATHER 4     /* any columns, im2col rows gathered to scratch first         */

@@ -4,10 +4,13 @@
 // Per conv group g the GEMM is  Y^T[m, px] = sum_k Wc_g[m, k] * Xcol[px, k]
 // with px = (n, p, q) an output pixel and k a kept (tap, channel) column.
 // structadmm_conv_fwd takes one of three paths per group, all on MFMA
-// v_mfma_f32_32x32x16_bf16 (A = Wc rows, B = output pixels, fp32 accumulate):
+// v_mfma_f32_32x32x16_bf16 (A = Wc rows, B = output pixels, fp32 accumulate;
+// small ragged filter groups over a few hundred columns take the 16-row
+// variant of the direct path in conv_ig.hip):
 //
 // k_conv (direct): the group's columns are every tap times one run of 8k
-//   input channels (dense, filter- or channel-pruned layers).  B rows are read
+//   input channels (dense, filter- or channel-pruned layers); 128-pixel tiles
+//   of 128 or 64 filters with eight wavefronts.  B rows are read
 //   as 16-byte vectors straight from the NHWC input; both operand tiles are
 //   staged through LDS in two buffers of 64 columns (loads of slice s+2 in
 //   flight while slice s is multiplied); raw buffer loads with 32-bit offsets
